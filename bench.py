@@ -1,0 +1,223 @@
+#!/usr/bin/env python3
+"""Benchmark of the NVFP4 linear-layer hot path on one MI355X.
+
+One step = every linear of one DiT block of the chosen workload (default: the
+FLUX.1-12B-like layers, M = 4 x (4096 + 512) = 18432 tokens; QKV 3072->9216,
+out 3072->3072, MLP 3072->12288->3072), each as
+    nvfp4_quantize(W)            weight re-quantization (once per update)
+    nvfp4_quantize(X)            activation amax + encode
+    nvfp4_gemm(Xq, Wq, bias)     block-scaled FP4 GEMM, BF16 out
+which is exactly the launch sequence of nvfp4_quantize(W) + nvfp4_linear.
+Inputs are synthetic (seeded, from workloads/) and resident in HBM before the
+timed region.  Prints one JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+# MI355X published dense peaks
+PEAK_HBM_GBS = 8000.0
+PEAK_FP16_MFMA_TFLOPS = 2500.0
+PEAK_FP4_MFMA_TFLOPS = 10100.0
+METRIC = "NVFP4 GEMM TFLOPS & % of FP4 MFMA peak; quantize GB/s & % HBM peak"
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="flux-12b")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-rows", type=int, default=256, help="oracle sample: activation rows")
+    ap.add_argument("--cpu-wrows", type=int, default=1024, help="oracle sample: weight rows")
+    return ap.parse_args()
+
+
+def cpu_baseline(wl, rows, wrows):
+    """The CPU oracle on a bounded sample of the same step: per layer, `rows`
+    activation rows and `wrows` weight rows at full K, quantize both and the
+    float64 GEMM; throughput in the metric's unit (TFLOP/s of 2 m n K)."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    import oracle.nvfp4 as O
+    from workloads import ROLE_BIAS, ROLE_W, ROLE_X, draw_activations, draw_bias, draw_weights, seed_for
+    flops, secs = 0.0, 0.0
+    for layer in wl.layers:
+        xb = draw_activations(layer.x_dist, wl.M, layer.K, seed_for(wl.config_id, layer.index, ROLE_X),
+                              row_range=(0, rows))
+        wb = draw_weights(layer.N, layer.K, wl.w_sigma, seed_for(wl.config_id, layer.index, ROLE_W),
+                          row_range=(0, wrows))
+        bias = draw_bias(layer.N, wl.w_sigma, seed_for(wl.config_id, layer.index, ROLE_BIAS))[:wrows]
+        t0 = time.perf_counter()
+        wq = O.nvfp4_quantize_ref(wb)
+        xq = O.nvfp4_quantize_ref(xb)
+        out = O.bf16_output(O.nvfp4_gemm_ref(*xq, *wq, bias))
+        secs += time.perf_counter() - t0
+        flops += 2.0 * rows * wb.shape[0] * layer.K
+        assert out.shape == (rows, wb.shape[0])
+    blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    return {
+        "value": flops / secs / 1e12,
+        "unit": "TFLOP/s",
+        "cores": int(blas_threads),
+        "kind": "oracle",
+        "sample": (f"per layer {rows} activation rows x {wrows} weight rows at full K: oracle "
+                   f"quantize of both (numpy float32, 1 thread) + float64 GEMM (BLAS, "
+                   f"{blas_threads} threads); {secs:.1f} s"),
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the layer shards "
+              f"along tokens with no communication, see the design notes", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2604_06916_amd as sol
+    from workloads import ROLE_BIAS, ROLE_W, ROLE_X, WORKLOADS, draw_activations, draw_bias, \
+        draw_weights, seed_for
+
+    wl = WORKLOADS[args.workload]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    def to_dev(bits):
+        return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).to(dev).view(torch.bfloat16)
+
+    layers = []
+    for layer in wl.layers:
+        M, N, K = wl.M, layer.N, layer.K
+        x = to_dev(draw_activations(layer.x_dist, M, K, seed_for(wl.config_id, layer.index, ROLE_X)))
+        w = to_dev(draw_weights(N, K, wl.w_sigma, seed_for(wl.config_id, layer.index, ROLE_W)))
+        b = to_dev(draw_bias(N, wl.w_sigma, seed_for(wl.config_id, layer.index, ROLE_BIAS)))
+        buf = dict(
+            x=x, w=w, b=b,
+            wc=torch.empty((N, K // 2), dtype=torch.uint8, device=dev),
+            ws=torch.empty((N, K // 16), dtype=torch.uint8, device=dev),
+            wa=torch.empty(1, dtype=torch.float32, device=dev),
+            xc=torch.empty((M, K // 2), dtype=torch.uint8, device=dev),
+            xs=torch.empty((M, K // 16), dtype=torch.uint8, device=dev),
+            xa=torch.empty(1, dtype=torch.float32, device=dev),
+            qws=torch.empty(max(sol.nvfp4_quantize_workspace_bytes(max(M, N), K), 256),
+                            dtype=torch.uint8, device=dev),
+            out=torch.empty((M, N), dtype=torch.bfloat16, device=dev),
+            M=M, N=N, K=K, name=layer.name)
+        layers.append(buf)
+    torch.cuda.synchronize()
+
+    def step(events=None):
+        for i, L in enumerate(layers):
+            e = events[i] if events is not None else None
+            if e:
+                e[0].record()
+            sol.nvfp4_quantize(L["w"], L["wc"], L["ws"], L["wa"], L["qws"])
+            if e:
+                e[1].record()
+            sol.nvfp4_quantize(L["x"], L["xc"], L["xs"], L["xa"], L["qws"])
+            if e:
+                e[2].record()
+            sol.nvfp4_gemm(L["xc"], L["xs"], L["xa"], L["wc"], L["ws"], L["wa"], L["b"], L["out"])
+            if e:
+                e[3].record()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    ev = [[[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in layers]
+          for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        step(ev[s])
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+
+    flops_step = sum(2.0 * L["M"] * L["N"] * L["K"] for L in layers)
+    per_layer = []
+    gemm_ms_tot = wq_ms_tot = xq_ms_tot = 0.0
+    for i, L in enumerate(layers):
+        wq = np.mean([ev[s][i][0].elapsed_time(ev[s][i][1]) for s in range(args.steps)])
+        xq = np.mean([ev[s][i][1].elapsed_time(ev[s][i][2]) for s in range(args.steps)])
+        gm = np.mean([ev[s][i][2].elapsed_time(ev[s][i][3]) for s in range(args.steps)])
+        gemm_ms_tot += gm
+        wq_ms_tot += wq
+        xq_ms_tot += xq
+        fl = 2.0 * L["M"] * L["N"] * L["K"]
+        xbytes = 4.5625 * L["M"] * L["K"]
+        per_layer.append({
+            "layer": L["name"], "M": L["M"], "N": L["N"], "K": L["K"],
+            "gemm_us": round(gm * 1e3, 2), "gemm_tflops": round(fl / (gm * 1e-3) / 1e12, 1),
+            "quantize_x_us": round(xq * 1e3, 2),
+            "quantize_x_gbs": round(xbytes / (xq * 1e-3) / 1e9, 1),
+            "quantize_w_us": round(wq * 1e3, 2),
+        })
+    gemm_tflops = flops_step / (gemm_ms_tot * 1e-3) / 1e12
+    xq_bytes = sum(4.5625 * L["M"] * L["K"] for L in layers)
+    quant_gbs = xq_bytes / (xq_ms_tot * 1e-3) / 1e9
+    ms_per_step = elapsed / args.steps * 1e3
+    value = flops_step / (ms_per_step * 1e-3) / 1e12
+
+    result = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16",
+        "data": "synthetic",
+        "config": {
+            "workload": wl.name, "M": wl.M,
+            "layers": [f"{L['name']} {L['K']}->{L['N']}" for L in layers],
+            "step": "per layer: nvfp4_quantize(W), nvfp4_quantize(X), nvfp4_gemm(+bias)",
+            "operands": "NVFP4 (E2M1 + E4M3/16 + FP32 tensor scale)",
+            "mfma": "exact FP16 dequant, v_mfma_f32_32x32x16_f16, FP32 accumulate",
+            "parallelism": "single GPU",
+        },
+        "roofline": {
+            "bound": "mfma",
+            "kernel": "nvfp4_gemm_kernel",
+            "achieved": round(gemm_tflops, 1),
+            "peak": PEAK_FP16_MFMA_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(gemm_tflops / PEAK_FP16_MFMA_TFLOPS, 4),
+            "traffic": None,
+        },
+        "gemm_frac_fp4_peak": round(gemm_tflops / PEAK_FP4_MFMA_TFLOPS, 4),
+        "quantize": {
+            "kernel": "amax_partial_kernel + nvfp4_encode_kernel (activations)",
+            "achieved_gbs": round(quant_gbs, 1),
+            "bytes_per_element": 4.5625,
+            "peak_gbs": PEAK_HBM_GBS,
+            "frac_hbm": round(quant_gbs / PEAK_HBM_GBS, 4),
+        },
+        "time_split_ms": {"gemm": round(gemm_ms_tot, 4), "quantize_x": round(xq_ms_tot, 4),
+                          "quantize_w": round(wq_ms_tot, 4)},
+        "layers": per_layer,
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(wl, args.cpu_rows, args.cpu_wrows)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,153 @@
+/*
+ * solfp4 -- NVFP4 linear layer for AMD Instinct MI355X (gfx950).
+ *
+ * The hot path of the fast-rollout stage of Sol-RL (arXiv 2604.06916): every
+ * linear layer of the diffusion-transformer denoiser runs on NVFP4 operands
+ * (Sec. 3.4, Stage 1; Sec. 4.1 uses NVFP4 for the whole exploration model).
+ * NVFP4 is defined in the Preliminaries ("FP4 Quantization and Hardware
+ * Acceleration"): E2M1 elements (1 sign, 2 exponent, 1 mantissa bit), one
+ * E4M3 scale per 16 contiguous elements, and Q(x) = S * Pi_FP4(x / S).
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - All data pointers are DEVICE pointers (HIP global memory) owned by the
+ *   caller; the library allocates and frees nothing and keeps no state
+ *   between calls.
+ * - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *   Calls only enqueue work and return; nothing synchronises the host.
+ * - Matrices are row-major and contiguous.  BF16 values travel as their
+ *   uint16_t bit patterns.  K, the reduction length, must be a multiple of
+ *   16 (one NVFP4 block).
+ * - Every pointer must be 16-byte aligned.
+ * - Argument errors are detected on the host and returned BEFORE any HIP
+ *   call, so they are safe to provoke on a machine without a GPU.  Non-finite
+ *   inputs (NaN, Inf) give unspecified codes but never fault.
+ * - Return value: SOLFP4_OK (0) or one of the negative status codes below.
+ *   Nothing throws across this boundary.
+ *
+ * NVFP4 encoding produced and consumed here (paper silent on these details;
+ * this is the library's fixed reading):
+ *   alpha = amax(|x|) / (6 * 448)                       FP32, per tensor
+ *   s_b   = E4M3_RNE_SAT(amax_b / (6 * alpha))          per 16-element block
+ *   q_i   = E2M1_RNE_SAT(x_i * (1 / (s_b * alpha)))     sign kept, also on 0
+ *   decoded value = alpha * s_b * q_i
+ * every step IEEE binary32 round-to-nearest-even in exactly this order.
+ * Rounding to E4M3 and E2M1 is to nearest with ties to the even code and
+ * saturates at 448 and 6.  amax == 0 gives alpha = 0, scales 0 and codes
+ * sign<<3; a block whose scale rounds to 0 gets codes sign<<3.
+ *
+ * Layouts:
+ *   codes  [rows][K/2]  uint8: element 2j in bits 3:0 of byte j, 2j+1 in 7:4
+ *   scales [rows][K/16] uint8: E4M3 (OCP E4M3FN: bias 7, max 448, 0x7F NaN)
+ *   global scale: one float (alpha) in device memory
+ */
+#ifndef SOLFP4_H
+#define SOLFP4_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Every entry point below is exported from libsolfp4.so; nothing else is. */
+#define SOLFP4_API __attribute__((visibility("default")))
+
+#define SOLFP4_OK 0
+#define SOLFP4_EINVAL (-1)     /* null pointer where data is needed, negative size */
+#define SOLFP4_ESHAPE (-2)     /* K not a multiple of 16, or a size beyond 2^31 elements per dimension */
+#define SOLFP4_EALIGN (-3)     /* a pointer is not 16-byte aligned */
+#define SOLFP4_EWORKSPACE (-4) /* workspace missing or smaller than the *_workspace_bytes query */
+#define SOLFP4_EHIP (-5)       /* a HIP launch reported an error */
+
+/* Static, human-readable text for a status code.  Host only; never NULL. */
+SOLFP4_API const char* solfp4_strerror(int status);
+
+/* Library version as 10000*major + 100*minor + patch.  Host only. */
+SOLFP4_API int solfp4_version(void);
+
+/*
+ * Device workspace, in bytes, that nvfp4_quantize needs for a [rows, K]
+ * input (room for the partial maxima of the first pass).  Host only; pure
+ * function of its arguments; 0 for invalid sizes.
+ */
+SOLFP4_API size_t nvfp4_quantize_workspace_bytes(int64_t rows, int64_t K);
+
+/*
+ * NVFP4 quantization of a BF16 matrix (Preliminaries: 16-element blocks,
+ * E4M3 block scales, E2M1 elements, plus the FP32 per-tensor scale above).
+ *
+ *   x            [rows][K] BF16, read only
+ *   codes        [rows][K/2] uint8, written
+ *   scales       [rows][K/16] uint8 (E4M3), written
+ *   global_scale 1 float, written with alpha
+ *   workspace    >= nvfp4_quantize_workspace_bytes(rows, K) bytes of device
+ *                scratch, contents undefined on entry and on exit
+ *
+ * Two kernels run in stream order: a read of x for amax, then the encode
+ * pass.  rows == 0 is valid and writes alpha = 0.  Codes, scales and alpha
+ * are bit-identical to the encoding stated at the top of this header.
+ */
+SOLFP4_API int nvfp4_quantize(const uint16_t* x, int64_t rows, int64_t K,
+                   uint8_t* codes, uint8_t* scales, float* global_scale,
+                   void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Block-scaled NVFP4 GEMM with BF16 output (the "NVFP4 dense operations" of
+ * Sec. 3.4, Stage 1):
+ *
+ *   out[m][n] = bf16_rne( a_gs * b_gs * sum_k (s_A q_A)[m][k] (s_B q_B)[n][k]
+ *                         + bias[n] )
+ *
+ *   a_codes [M][K/2], a_scales [M][K/16], a_global_scale 1 float  (A = X)
+ *   b_codes [N][K/2], b_scales [N][K/16], b_global_scale 1 float  (B = W,
+ *            stored [N][K] as an nn.Linear weight)
+ *   bias    [N] BF16 or NULL
+ *   out     [M][N] BF16, written
+ *
+ * Each product (s q)(s q) is formed exactly (both factors are dequantized
+ * exactly to FP16 and multiplied by the FP16 matrix cores); sums are FP32 in
+ * an unspecified order; alpha = a_gs * b_gs is one FP32 multiply; the output
+ * is bf16_rne(fp32(fma(alpha, acc, bias[n]))): one FP32 fused multiply-add,
+ * then rounding to BF16.  Results may differ from a float64 evaluation by
+ * the FP32 summation and FMA roundings plus the BF16 rounding.  M, N or K
+ * equal to 0 are valid (K == 0 writes the bias, or zeros).
+ */
+SOLFP4_API int nvfp4_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_global_scale,
+               const uint8_t* b_codes, const uint8_t* b_scales, const float* b_global_scale,
+               const uint16_t* bias, uint16_t* out,
+               int64_t M, int64_t N, int64_t K, void* stream);
+
+/* Device workspace, in bytes, that nvfp4_linear needs for [M, K]
+ * activations (their NVFP4 codes, scales, alpha and the quantizer's
+ * scratch).  Host only; 0 for invalid sizes. */
+SOLFP4_API size_t nvfp4_linear_workspace_bytes(int64_t M, int64_t K);
+
+/*
+ * The NVFP4 linear layer of the denoiser (Sec. 4.1: the model's linears run
+ * in NVFP4; Sec. 3.4: weights are quantized once per policy update, the
+ * activations on the fly): quantize x exactly as nvfp4_quantize does, then
+ * nvfp4_gemm against the pre-quantized weight, with bias.
+ *
+ *   x        [M][K] BF16
+ *   w_codes  [N][K/2], w_scales [N][K/16], w_global_scale 1 float
+ *            (the weight quantized with nvfp4_quantize)
+ *   bias     [N] BF16 or NULL
+ *   out      [M][N] BF16
+ *   workspace >= nvfp4_linear_workspace_bytes(M, K) bytes; on return it
+ *            holds the activation codes at offset 0, then their scales and
+ *            alpha (offsets are an implementation detail).
+ *
+ * The result is bit-identical to nvfp4_quantize followed by nvfp4_gemm.
+ */
+SOLFP4_API int nvfp4_linear(const uint16_t* x, const uint8_t* w_codes, const uint8_t* w_scales,
+                 const float* w_global_scale, const uint16_t* bias, uint16_t* out,
+                 void* workspace, size_t workspace_bytes,
+                 int64_t M, int64_t N, int64_t K, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SOLFP4_H */

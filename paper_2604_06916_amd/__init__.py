@@ -1,0 +1,16 @@
+"""solfp4: NVFP4 linear layer (quantize, block-scaled GEMM, linear) for
+AMD MI355X, as a C-ABI HIP library with a thin Python binding.
+
+The binding (and so libsolfp4.so) loads on first use of any name below and
+raises ImportError if the library has not been built.
+"""
+_NAMES = ("EXPORTED", "LIB_PATH", "Solfp4Error", "lib", "nvfp4_gemm", "nvfp4_linear",
+          "nvfp4_linear_workspace_bytes", "nvfp4_quantize", "nvfp4_quantize_workspace_bytes")
+__all__ = list(_NAMES)
+
+
+def __getattr__(name):
+    if name in _NAMES:
+        from . import _binding
+        return getattr(_binding, name)
+    raise AttributeError(name)

@@ -1,0 +1,156 @@
+// C-ABI entry points of libsolfp4 (declared and documented in solfp4.h).
+// Every argument check happens on the host before the first HIP call.
+#include "../../include/solfp4.h"
+#include "kernels.h"
+
+namespace {
+
+constexpr size_t kAlign = 256;
+constexpr int64_t kMaxDim = (int64_t)1 << 31;
+
+size_t round_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+int check_dims(int64_t a, int64_t b) {
+  if (a < 0 || b < 0) return SOLFP4_EINVAL;
+  if (a >= kMaxDim || b >= kMaxDim) return SOLFP4_ESHAPE;
+  return SOLFP4_OK;
+}
+
+size_t quantize_scratch_bytes(int64_t rows, int64_t K) {
+  return round_up((size_t)solfp4::amax_partial_count(rows * K) * sizeof(uint32_t));
+}
+
+struct LinearLayout {
+  size_t codes, scales, alpha, partial, total;
+};
+
+LinearLayout linear_layout(int64_t M, int64_t K) {
+  LinearLayout l;
+  l.codes = 0;
+  l.scales = round_up((size_t)(M * K / 2));
+  l.alpha = l.scales + round_up((size_t)(M * K / 16));
+  l.partial = l.alpha + kAlign;
+  l.total = l.partial + quantize_scratch_bytes(M, K);
+  return l;
+}
+
+int quantize_checks(const uint16_t* x, int64_t rows, int64_t K, const uint8_t* codes,
+                    const uint8_t* scales, const float* gs, const void* ws, size_t ws_bytes) {
+  int rc = check_dims(rows, K);
+  if (rc) return rc;
+  if (K % 16) return SOLFP4_ESHAPE;
+  const bool data = rows > 0 && K > 0;
+  if (!gs || !ws || (data && (!x || !codes || !scales))) return SOLFP4_EINVAL;
+  if (!aligned16(gs) || !aligned16(ws) ||
+      (data && (!aligned16(x) || !aligned16(codes) || !aligned16(scales))))
+    return SOLFP4_EALIGN;
+  if (ws_bytes < quantize_scratch_bytes(rows, K)) return SOLFP4_EWORKSPACE;
+  return SOLFP4_OK;
+}
+
+int gemm_checks(const uint8_t* ac, const uint8_t* as, const float* ags, const uint8_t* bc,
+                const uint8_t* bs, const float* bgs, const uint16_t* bias, const uint16_t* out,
+                int64_t M, int64_t N, int64_t K) {
+  int rc = check_dims(M, N);
+  if (rc) return rc;
+  rc = check_dims(K, 0);
+  if (rc) return rc;
+  if (K % 16) return SOLFP4_ESHAPE;
+  // the grid is one workgroup per 256 x 256 output tile
+  if (((M + 255) / 256) * ((N + 255) / 256) >= kMaxDim) return SOLFP4_ESHAPE;
+  const bool any_out = M > 0 && N > 0;
+  if (!any_out) return SOLFP4_OK;
+  if (!out || !ags || !bgs) return SOLFP4_EINVAL;
+  if (K > 0 && (!ac || !as || !bc || !bs)) return SOLFP4_EINVAL;
+  if (!aligned16(out) || !aligned16(ags) || !aligned16(bgs) || (bias && !aligned16(bias)))
+    return SOLFP4_EALIGN;
+  if (K > 0 && (!aligned16(ac) || !aligned16(as) || !aligned16(bc) || !aligned16(bs)))
+    return SOLFP4_EALIGN;
+  return SOLFP4_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* solfp4_strerror(int status) {
+  switch (status) {
+    case SOLFP4_OK: return "success";
+    case SOLFP4_EINVAL: return "invalid argument (null pointer or negative size)";
+    case SOLFP4_ESHAPE: return "unsupported shape (K must be a multiple of 16; sizes below 2^31)";
+    case SOLFP4_EALIGN: return "pointer not 16-byte aligned";
+    case SOLFP4_EWORKSPACE: return "workspace missing or too small";
+    case SOLFP4_EHIP: return "HIP kernel launch failed";
+    default: return "unknown status";
+  }
+}
+
+int solfp4_version(void) { return 100; }
+
+size_t nvfp4_quantize_workspace_bytes(int64_t rows, int64_t K) {
+  if (check_dims(rows, K) || K % 16) return 0;
+  return quantize_scratch_bytes(rows, K);
+}
+
+int nvfp4_quantize(const uint16_t* x, int64_t rows, int64_t K, uint8_t* codes, uint8_t* scales,
+                   float* global_scale, void* workspace, size_t workspace_bytes, void* stream) {
+  const int rc = quantize_checks(x, rows, K, codes, scales, global_scale, workspace, workspace_bytes);
+  if (rc) return rc;
+  const hipError_t e = solfp4::launch_quantize(x, rows, K, codes, scales, global_scale,
+                                               static_cast<uint32_t*>(workspace),
+                                               static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? SOLFP4_OK : SOLFP4_EHIP;
+}
+
+int nvfp4_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_global_scale,
+               const uint8_t* b_codes, const uint8_t* b_scales, const float* b_global_scale,
+               const uint16_t* bias, uint16_t* out, int64_t M, int64_t N, int64_t K,
+               void* stream) {
+  const int rc = gemm_checks(a_codes, a_scales, a_global_scale, b_codes, b_scales, b_global_scale,
+                             bias, out, M, N, K);
+  if (rc) return rc;
+  if (M == 0 || N == 0) return SOLFP4_OK;
+  const hipError_t e = solfp4::launch_gemm(a_codes, a_scales, a_global_scale, b_codes, b_scales,
+                                           b_global_scale, bias, out, M, N, K,
+                                           static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? SOLFP4_OK : SOLFP4_EHIP;
+}
+
+size_t nvfp4_linear_workspace_bytes(int64_t M, int64_t K) {
+  if (check_dims(M, K) || K % 16) return 0;
+  return linear_layout(M, K).total;
+}
+
+int nvfp4_linear(const uint16_t* x, const uint8_t* w_codes, const uint8_t* w_scales,
+                 const float* w_global_scale, const uint16_t* bias, uint16_t* out,
+                 void* workspace, size_t workspace_bytes, int64_t M, int64_t N, int64_t K,
+                 void* stream) {
+  int rc = check_dims(M, N);
+  if (rc) return rc;
+  rc = check_dims(K, 0);
+  if (rc) return rc;
+  if (K % 16) return SOLFP4_ESHAPE;
+  if (!workspace) return SOLFP4_EINVAL;
+  if (!aligned16(workspace)) return SOLFP4_EALIGN;
+  const LinearLayout l = linear_layout(M, K);
+  if (workspace_bytes < l.total) return SOLFP4_EWORKSPACE;
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  uint8_t* xc = ws + l.codes;
+  uint8_t* xs = ws + l.scales;
+  float* xa = reinterpret_cast<float*>(ws + l.alpha);
+  uint32_t* partial = reinterpret_cast<uint32_t*>(ws + l.partial);
+  rc = quantize_checks(x, M, K, xc, xs, xa, partial, l.total - l.partial);
+  if (rc) return rc;
+  rc = gemm_checks(xc, xs, xa, w_codes, w_scales, w_global_scale, bias, out, M, N, K);
+  if (rc) return rc;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e = solfp4::launch_quantize(x, M, K, xc, xs, xa, partial, s);
+  if (e != hipSuccess) return SOLFP4_EHIP;
+  if (M == 0 || N == 0) return SOLFP4_OK;
+  e = solfp4::launch_gemm(xc, xs, xa, w_codes, w_scales, w_global_scale, bias, out, M, N, K, s);
+  return e == hipSuccess ? SOLFP4_OK : SOLFP4_EHIP;
+}
+
+}  // extern "C"

@@ -1,0 +1,198 @@
+// NVFP4 quantization kernels (Preliminaries of arXiv 2604.06916: E2M1
+// elements, one E4M3 scale per 16 elements, Q(x) = S * Pi_FP4(x / S); plus a
+// per-tensor FP32 scale alpha = amax / (6 * 448)).
+//
+// The tensor is a flat run of 16-element blocks (K % 16 == 0, row-major), so
+// both kernels treat it as one-dimensional:
+//   1. amax_partial_kernel  streams x once and writes one partial |x| maximum
+//      (as a 15-bit BF16 magnitude) per workgroup;
+//   2. nvfp4_encode_kernel  folds the partials into alpha, then streams x
+//      again, one block per lane: block amax, E4M3 scale, reciprocal, then
+//      E2M1 encoding of 16 elements by the hardware converter.
+// Both passes are HBM-bound streaming reads (2 B/element each) plus the
+// 0.5625 B/element of codes and scales written by the second.
+//
+// The FP32 operation order is fixed (it decides the codes bit for bit):
+//   alpha = amax_g / 2688; t = alpha * 6; s_f = amax_b / t; s = E4M3(s_f);
+//   d = s * alpha; r = 1 / d; y = x * r; q = E2M1(y)
+// with correctly rounded division (hipcc's default) and no contraction.
+#include "device_common.h"
+#include "kernels.h"
+
+namespace solfp4 {
+
+constexpr int kQuantThreads = 256;
+
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
+// 16-byte streaming load (each input byte is read exactly once per pass).
+__device__ __forceinline__ u32x4_t stream_load(const uint4* p) {
+  return __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
+}
+constexpr int kEncodeUnroll = 4;   // blocks per lane per iteration
+
+__global__ __launch_bounds__(kQuantThreads) void amax_partial_kernel(
+    const uint4* __restrict__ x, int64_t n_vec, uint32_t* __restrict__ partial) {
+  ushort2_t m = {0, 0};
+  const int64_t stride = (int64_t)gridDim.x * kQuantThreads;
+  int64_t i = (int64_t)blockIdx.x * kQuantThreads + threadIdx.x;
+  // four independent 16-byte loads in flight per lane
+  for (; i + 3 * stride < n_vec; i += 4 * stride) {
+    u32x4_t v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) v[u] = stream_load(&x[i + u * stride]);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      m = absmax_pair(m, v[u].x);
+      m = absmax_pair(m, v[u].y);
+      m = absmax_pair(m, v[u].z);
+      m = absmax_pair(m, v[u].w);
+    }
+  }
+  for (; i < n_vec; i += stride) {
+    const uint4 v = x[i];
+    m = absmax_pair(m, v.x);
+    m = absmax_pair(m, v.y);
+    m = absmax_pair(m, v.z);
+    m = absmax_pair(m, v.w);
+  }
+  uint32_t r = wave_max_u32(max((uint32_t)m.x, (uint32_t)m.y));
+  __shared__ uint32_t red[kQuantThreads / kWave];
+  if ((threadIdx.x & (kWave - 1)) == 0) red[threadIdx.x / kWave] = r;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t t = red[0];
+#pragma unroll
+    for (int w = 1; w < kQuantThreads / kWave; ++w) t = max(t, red[w]);
+    partial[blockIdx.x] = t;
+  }
+}
+
+// Encode one 16-element block held in w[0..7] (two BF16 per word, element
+// 2j in the low half).  Writes the 8 code bytes into c0/c1 and returns the
+// E4M3 scale code.
+__device__ __forceinline__ uint32_t encode_block(const uint32_t (&w)[8], float alpha, float t,
+                                                 bool zero_tensor, uint32_t& c0, uint32_t& c1) {
+  ushort2_t m = as_us2(w[0] & 0x7FFF7FFFu);
+#pragma unroll
+  for (int j = 1; j < 8; ++j) m = absmax_pair(m, w[j]);
+  const uint32_t ab = max((uint32_t)m.x, (uint32_t)m.y);
+  const float amax_b = __uint_as_float(ab << 16);
+  float s_val;
+  const float s_f = zero_tensor ? 0.0f : amax_b / t;
+  const uint32_t sc = e4m3_rne_sat(s_f, &s_val);
+  const float d = s_val * alpha;
+  // a zero scale encodes the block as signed zeros: x * 0 keeps the sign
+  const float r = sc != 0u ? 1.0f / d : 0.0f;
+  float e[16];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    e[2 * j] = __uint_as_float(w[j] << 16) * r;
+    e[2 * j + 1] = __uint_as_float(w[j] & 0xFFFF0000u) * r;
+  }
+  // hardware E2M1 encode, two elements per byte (the first in the low nibble)
+  uint32_t lo = 0, hi = 0;
+  lo = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(lo, e[0], e[1], 1.0f, 0);
+  lo = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(lo, e[2], e[3], 1.0f, 1);
+  lo = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(lo, e[4], e[5], 1.0f, 2);
+  lo = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(lo, e[6], e[7], 1.0f, 3);
+  hi = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(hi, e[8], e[9], 1.0f, 0);
+  hi = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(hi, e[10], e[11], 1.0f, 1);
+  hi = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(hi, e[12], e[13], 1.0f, 2);
+  hi = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(hi, e[14], e[15], 1.0f, 3);
+  c0 = lo;
+  c1 = hi;
+  return sc;
+}
+
+__global__ __launch_bounds__(kQuantThreads) void nvfp4_encode_kernel(
+    const uint4* __restrict__ x, int64_t nblocks, const uint32_t* __restrict__ partial,
+    int npartial, uint2* __restrict__ codes, uint8_t* __restrict__ scales,
+    float* __restrict__ global_scale) {
+  // fold the first pass's partial maxima (every workgroup does it; a few KB
+  // from L2)
+  __shared__ uint32_t red[kQuantThreads / kWave];
+  uint32_t m = 0;
+  for (int i = threadIdx.x; i < npartial; i += kQuantThreads) m = max(m, partial[i]);
+  m = wave_max_u32(m);
+  if ((threadIdx.x & (kWave - 1)) == 0) red[threadIdx.x / kWave] = m;
+  __syncthreads();
+  uint32_t amax_bits = red[0];
+#pragma unroll
+  for (int w = 1; w < kQuantThreads / kWave; ++w) amax_bits = max(amax_bits, red[w]);
+
+  const float amax_g = __uint_as_float(amax_bits << 16);
+  const float alpha = amax_g / kAlphaDivisor;
+  const float t = alpha * 6.0f;
+  const bool zero_tensor = amax_bits == 0u;
+  if (blockIdx.x == 0 && threadIdx.x == 0) *global_scale = alpha;
+
+  const int lane = threadIdx.x & (kWave - 1);
+  const int64_t per_iter = (int64_t)kQuantThreads * kEncodeUnroll;
+  for (int64_t base = (int64_t)blockIdx.x * per_iter; base < nblocks;
+       base += (int64_t)gridDim.x * per_iter) {
+    u32x4_t v[kEncodeUnroll][2];
+#pragma unroll
+    for (int u = 0; u < kEncodeUnroll; ++u) {
+      const int64_t blk = base + u * kQuantThreads + threadIdx.x;
+      if (blk < nblocks) {
+        v[u][0] = stream_load(&x[2 * blk]);
+        v[u][1] = stream_load(&x[2 * blk + 1]);
+      } else {
+        v[u][0] = u32x4_t{0, 0, 0, 0};
+        v[u][1] = u32x4_t{0, 0, 0, 0};
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kEncodeUnroll; ++u) {
+      const int64_t blk = base + u * kQuantThreads + threadIdx.x;
+      const uint32_t w[8] = {v[u][0].x, v[u][0].y, v[u][0].z, v[u][0].w,
+                             v[u][1].x, v[u][1].y, v[u][1].z, v[u][1].w};
+      uint32_t c0, c1;
+      const uint32_t sc = encode_block(w, alpha, t, zero_tensor, c0, c1);
+      if (blk < nblocks) codes[blk] = make_uint2(c0, c1);
+      // gather the scale bytes of each aligned lane quad into its first lane
+      const uint32_t s1 = (uint32_t)__builtin_amdgcn_mov_dpp((int)sc, 0x55, 0xF, 0xF, false);
+      const uint32_t s2 = (uint32_t)__builtin_amdgcn_mov_dpp((int)sc, 0xAA, 0xF, 0xF, false);
+      const uint32_t s3 = (uint32_t)__builtin_amdgcn_mov_dpp((int)sc, 0xFF, 0xF, 0xF, false);
+      if ((lane & 3) == 0) {
+        if (blk + 3 < nblocks) {
+          *reinterpret_cast<uint32_t*>(scales + blk) = sc | (s1 << 8) | (s2 << 16) | (s3 << 24);
+        } else {
+          if (blk < nblocks) scales[blk] = (uint8_t)sc;
+          if (blk + 1 < nblocks) scales[blk + 1] = (uint8_t)s1;
+          if (blk + 2 < nblocks) scales[blk + 2] = (uint8_t)s2;
+        }
+      }
+    }
+  }
+}
+
+int amax_partial_count(int64_t n_elems) {
+  // one workgroup per 64 Ki elements, at most kMaxPartials
+  const int64_t per_wg = 64 * 1024;
+  int64_t p = (n_elems + per_wg - 1) / per_wg;
+  if (p < 1) p = 1;
+  if (p > kMaxPartials) p = kMaxPartials;
+  return (int)p;
+}
+
+hipError_t launch_quantize(const uint16_t* x, int64_t rows, int64_t K, uint8_t* codes,
+                           uint8_t* scales, float* global_scale, uint32_t* partial,
+                           hipStream_t stream) {
+  const int64_t n = rows * K;
+  const int64_t nblocks = n / 16;
+  const int npartial = amax_partial_count(n);
+  hipLaunchKernelGGL(amax_partial_kernel, dim3(npartial), dim3(kQuantThreads), 0, stream,
+                     reinterpret_cast<const uint4*>(x), n / 8, partial);
+  const int64_t per_wg = (int64_t)kQuantThreads * kEncodeUnroll;
+  int64_t grid = (nblocks + per_wg - 1) / per_wg;
+  if (grid > kEncodeMaxGrid) grid = kEncodeMaxGrid;
+  if (grid < 1) grid = 1;
+  hipLaunchKernelGGL(nvfp4_encode_kernel, dim3((unsigned)grid), dim3(kQuantThreads), 0, stream,
+                     reinterpret_cast<const uint4*>(x), nblocks, partial, npartial,
+                     reinterpret_cast<uint2*>(codes), scales, global_scale);
+  return hipGetLastError();
+}
+
+}  // namespace solfp4

@@ -1,0 +1,125 @@
+"""The C-ABI boundary without a GPU: the library loads, exports exactly the
+entry points include/solfp4.h declares, and rejects bad arguments on the host
+before any HIP call."""
+import ctypes
+import os
+import re
+import shutil
+import subprocess
+
+import pytest
+
+import paper_2604_06916_amd as sol
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "solfp4.h")
+
+OK, EINVAL, ESHAPE, EALIGN, EWORKSPACE, EHIP = 0, -1, -2, -3, -4, -5
+
+# fake device addresses: never dereferenced, because every call below fails
+# validation on the host first
+P = ctypes.c_void_p(0x7F0000000000)
+P2 = ctypes.c_void_p(0x7F0000100000)
+P3 = ctypes.c_void_p(0x7F0000200000)
+MIS = ctypes.c_void_p(0x7F0000000008)   # 8-byte aligned only
+NULL = None
+S = None                                  # null stream
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return re.findall(r"SOLFP4_API\s+[\w\s\*]+?\b(\w+)\s*\(", text)
+
+
+def test_header_declares_the_entry_points():
+    names = declared_functions()
+    assert sorted(names) == sorted(sol.EXPORTED)
+    assert {"nvfp4_quantize", "nvfp4_gemm", "nvfp4_linear"} <= set(names)
+
+
+def test_library_exports_every_declared_symbol():
+    for name in declared_functions():
+        assert getattr(sol.lib, name) is not None
+
+
+@pytest.mark.skipif(shutil.which("nm") is None, reason="nm not available")
+def test_library_exports_nothing_else():
+    out = subprocess.run(["nm", "-D", "--defined-only", sol.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    funcs = {ln.split()[-1] for ln in out.splitlines() if " T " in ln}
+    assert funcs == set(declared_functions())
+
+
+def test_strerror_and_version():
+    texts = {c: sol.lib.solfp4_strerror(c) for c in (OK, EINVAL, ESHAPE, EALIGN, EWORKSPACE, EHIP, 7)}
+    assert all(texts.values())
+    assert len(set(texts.values())) == len(texts)
+    assert sol.lib.solfp4_version() >= 100
+
+
+def test_workspace_queries():
+    q = sol.nvfp4_quantize_workspace_bytes
+    assert q(0, 0) >= 4 and q(128, 1152) >= 4 and q(10 ** 6, 4096) <= 4096 * 4
+    assert q(-1, 16) == 0 and q(4, 24) == 0
+    L = sol.nvfp4_linear_workspace_bytes
+    for M, K in [(1, 16), (128, 1152), (18432, 3072), (26574, 9728)]:
+        assert L(M, K) >= M * K // 2 + M * K // 16 + 4 + q(M, K)
+    assert L(-1, 16) == 0 and L(3, 40) == 0
+
+
+def quant(x=P, rows=4, K=32, codes=P2, scales=P3, gs=P, ws=P, wsb=4096):
+    return sol.lib.nvfp4_quantize(x, rows, K, codes, scales, gs, ws, wsb, S)
+
+
+def test_quantize_rejects_bad_arguments():
+    assert quant(rows=-1) == EINVAL
+    assert quant(K=-16) == EINVAL
+    assert quant(K=24) == ESHAPE
+    assert quant(K=1 << 31) == ESHAPE
+    assert quant(x=NULL) == EINVAL
+    assert quant(codes=NULL) == EINVAL
+    assert quant(scales=NULL) == EINVAL
+    assert quant(gs=NULL) == EINVAL
+    assert quant(ws=NULL) == EINVAL
+    assert quant(x=MIS) == EALIGN
+    assert quant(codes=MIS) == EALIGN
+    assert quant(gs=MIS) == EALIGN
+    assert quant(wsb=0) == EWORKSPACE
+
+
+def gemm(ac=P, as_=P2, ag=P3, bc=P, bs=P2, bg=P3, bias=NULL, out=P, M=8, N=8, K=32):
+    return sol.lib.nvfp4_gemm(ac, as_, ag, bc, bs, bg, bias, out, M, N, K, S)
+
+
+def test_gemm_rejects_bad_arguments():
+    assert gemm(M=-1) == EINVAL
+    assert gemm(N=-1) == EINVAL
+    assert gemm(K=-16) == EINVAL
+    assert gemm(K=40) == ESHAPE
+    assert gemm(M=1 << 31) == ESHAPE
+    assert gemm(out=NULL) == EINVAL
+    assert gemm(ag=NULL) == EINVAL
+    assert gemm(bc=NULL) == EINVAL
+    assert gemm(as_=MIS) == EALIGN
+    assert gemm(bias=MIS) == EALIGN
+    assert gemm(out=MIS) == EALIGN
+    # nothing to compute: valid, and no HIP call is made
+    assert gemm(M=0, out=NULL) == OK
+    assert gemm(N=0, out=NULL) == OK
+
+
+def linear(x=P, wc=P2, ws_=P3, wg=P, bias=NULL, out=P2, ws=P3, wsb=1 << 20, M=8, N=8, K=32):
+    return sol.lib.nvfp4_linear(x, wc, ws_, wg, bias, out, ws, wsb, M, N, K, S)
+
+
+def test_linear_rejects_bad_arguments():
+    assert linear(M=-1) == EINVAL
+    assert linear(K=20) == ESHAPE
+    assert linear(ws=NULL) == EINVAL
+    assert linear(ws=MIS) == EALIGN
+    assert linear(wsb=16) == EWORKSPACE
+    assert linear(x=NULL) == EINVAL
+    assert linear(wc=NULL) == EINVAL
+    assert linear(wg=NULL) == EINVAL
+    assert linear(bias=MIS) == EALIGN
+    assert linear(out=MIS) == EALIGN

@@ -1,0 +1,51 @@
+"""nvfp4_linear on the GPU: bit-identical to nvfp4_quantize followed by
+nvfp4_gemm, and within tolerance of the oracle's quantize-then-GEMM."""
+import numpy as np
+import pytest
+import torch
+
+import oracle.nvfp4 as O
+import paper_2604_06916_amd as sol
+from gpu_util import bf16_from_dev, bf16_mismatch_fraction, bf16_to_dev, poison_bf16, rel_fro, say
+from workloads import draw_activations, draw_bias, draw_weights
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("M,N,K", [(1, 16, 16), (7, 33, 48), (128, 1152, 1152), (300, 520, 2240),
+                                   (517, 260, 5600), (1000, 3072, 3072)])
+@pytest.mark.parametrize("with_bias", [False, True])
+def test_linear_matches_quantize_then_gemm_and_oracle(M, N, K, with_bias):
+    xb = draw_activations("t3_1pct", M, K, seed=M + K)
+    wb = draw_weights(N, K, 0.02, seed=N + K)
+    bias = draw_bias(N, 0.02, seed=N) if with_bias else None
+    x, w = bf16_to_dev(xb), bf16_to_dev(wb)
+    b = None if bias is None else bf16_to_dev(bias)
+    wc, ws, wa = sol.nvfp4_quantize(w)
+    out = poison_bf16((M, N))
+    sol.nvfp4_linear(x, wc, ws, wa, b, out)
+    xc, xs, xa = sol.nvfp4_quantize(x)
+    out2 = sol.nvfp4_gemm(xc, xs, xa, wc, ws, wa, b)
+    torch.cuda.synchronize()
+    got = bf16_from_dev(out)
+    assert np.array_equal(got, bf16_from_dev(out2))
+
+    ref, _ = O.nvfp4_linear_ref(xb, *O.nvfp4_quantize_ref(wb), bias)
+    err = rel_fro(got, ref)
+    mism = bf16_mismatch_fraction(got, ref)
+    say(f"linear M={M} N={N} K={K} bias={with_bias}: rel_fro={err:.3e} mismatch={mism:.2e}")
+    assert err <= 2e-3
+    assert mism <= 0.01
+
+
+def test_linear_workspace_holds_the_activation_codes():
+    M, N, K = 64, 48, 256
+    xb = draw_activations("normal", M, K, seed=3)
+    wb = draw_weights(N, K, 0.02, seed=4)
+    x = bf16_to_dev(xb)
+    wc, ws, wa = sol.nvfp4_quantize(bf16_to_dev(wb))
+    wsp = torch.empty(sol.nvfp4_linear_workspace_bytes(M, K), dtype=torch.uint8, device=x.device)
+    sol.nvfp4_linear(x, wc, ws, wa, workspace=wsp)
+    torch.cuda.synchronize()
+    rc, _, _ = O.nvfp4_quantize_ref(xb)
+    assert np.array_equal(wsp[: M * K // 2].cpu().numpy().reshape(M, K // 2), rc)

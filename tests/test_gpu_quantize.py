@@ -1,0 +1,189 @@
+"""GPU parity of nvfp4_quantize against the CPU oracle: codes, scales and
+alpha must be bit-identical."""
+import numpy as np
+import pytest
+import torch
+
+import golden_io
+import oracle.nvfp4 as O
+import paper_2604_06916_amd as sol
+from gpu_util import bf16_to_dev, device, f32_bits, poison_u8, say, u8_from_dev
+from workloads import draw_activations, f32_to_bf16_bits
+
+pytestmark = pytest.mark.gpu
+
+
+def gpu_quantize(xbits: np.ndarray):
+    rows, K = xbits.shape
+    x = bf16_to_dev(xbits)
+    codes = poison_u8((rows, K // 2))
+    scales = poison_u8((rows, K // 16))
+    gs = torch.full((1,), float("nan"), dtype=torch.float32, device=device())
+    sol.nvfp4_quantize(x, codes, scales, gs)
+    torch.cuda.synchronize()
+    return u8_from_dev(codes), u8_from_dev(scales), np.float32(gs.cpu().numpy()[0])
+
+
+def assert_same(xbits, label=""):
+    c, s, a = gpu_quantize(xbits)
+    rc, rs, ra = O.nvfp4_quantize_ref(xbits)
+    assert f32_bits(a) == f32_bits(ra), f"{label}: alpha {a!r} vs {ra!r}"
+    bad_s = np.argwhere(s != rs)
+    assert bad_s.size == 0, f"{label}: {len(bad_s)} scale mismatches, first at {bad_s[:4].tolist()}: " \
+                            f"gpu {s[tuple(bad_s[0])]:#04x} oracle {rs[tuple(bad_s[0])]:#04x}"
+    bad_c = np.argwhere(c != rc)
+    if bad_c.size:
+        r, j = bad_c[0]
+        blk = (2 * j) // 16
+        raise AssertionError(
+            f"{label}: {len(bad_c)} code-byte mismatches; first row {r} byte {j}: gpu {c[r, j]:#04x} "
+            f"oracle {rc[r, j]:#04x}; block scale {rs[r, blk]:#04x}; block x bits "
+            f"{[hex(v) for v in xbits[r, 16 * blk:16 * blk + 16]]}")
+
+
+def test_hand_worked_cases():
+    for name, case in golden_io.load().items():
+        if case["kind"] != "case":
+            continue
+        xb = golden_io.f32_to_bf16_exact(case["x"])[None, :]
+        c, s, a = gpu_quantize(xb)
+        say(name, c.tobytes().hex(" "), s.tobytes().hex(" "), hex(f32_bits(a)))
+        assert c.tobytes() == case["codes"].tobytes(), name
+        assert s.tobytes() == case["scales"].tobytes(), name
+        assert f32_bits(a) == f32_bits(case["alpha"]), name
+
+
+SHAPES = [(1, 16), (1, 48), (3, 32), (5, 208), (7, 1152), (33, 2240), (257, 16), (64, 5600),
+          (129, 3072)]
+KINDS = ["normal", "t3_1pct", "gelu", "rowscale", "uniform", "outlier4x20"]
+
+
+@pytest.mark.parametrize("rows,K", SHAPES)
+def test_random_shapes(rows, K):
+    for i, kind in enumerate(KINDS):
+        xb = draw_activations(kind, rows, K, seed=100 * rows + K + i)
+        assert_same(xb, f"{kind} {rows}x{K}")
+
+
+def test_tie_heavy_and_wide_range():
+    g = np.random.Generator(np.random.PCG64(5))
+    # dyadic values: exact ties of the element and scale rounding are common
+    x = (g.integers(-48, 49, size=(64, 256)) * np.float32(0.0625)).astype(np.float32)
+    assert_same(f32_to_bf16_bits(x), "dyadic")
+    # blocks spanning 2^-30 .. 2^7, many zero-scale blocks
+    x = (g.standard_normal((64, 256)) * np.exp2(g.integers(-30, 8, size=(64, 256)))).astype(np.float32)
+    assert_same(f32_to_bf16_bits(x), "wide")
+    # per-block magnitudes from 2^-24 to 2^6: subnormal and zero E4M3 scales
+    x = g.standard_normal((64, 256)).astype(np.float32)
+    x *= np.repeat(np.exp2(g.integers(-24, 7, size=(64, 16))), 16, axis=1).astype(np.float32)
+    assert_same(f32_to_bf16_bits(x), "blockscale")
+
+
+def test_exact_midpoints_at_every_scale():
+    """Blocks whose elements are E2M1 midpoints times s * alpha for every
+    normal E4M3 scale s: the multiply-by-reciprocal order decides them."""
+    mids = np.array([0.25, 0.75, 1.25, 1.75, 2.5, 3.5, 5.0, 6.0])
+    rows = []
+    for c in range(0x08, 0x7F):
+        d = float(O.e4m3_decode(c)) * 2.0 ** -9
+        blk = np.concatenate([[6.0], mids, mids[:7]]) * d
+        rows.append(blk)
+        rows.append(-blk[::-1])
+    x = np.array(rows, dtype=np.float32).reshape(-1, 32)
+    x[0, 0] = 5.25          # alpha = 2^-9
+    assert_same(f32_to_bf16_bits(x), "midpoints")
+
+
+def _exponent_group_tensor(e_lo, e_hi, rhos):
+    pats = []
+    for e in range(e_lo, e_hi):
+        for m in range(128):
+            v = (e << 7) | m
+            pats += [v, v | 0x8000]
+    pats = np.array(pats, dtype=np.uint16)
+    mags = O.bf16_bits_to_f32(pats & np.uint16(0x7FFF))
+    order = np.argsort(mags, kind="stable")
+    pats = pats[order]
+    blocks = []
+    for rho in rhos:
+        for i in range(0, len(pats), 15):
+            test = pats[i:i + 15]
+            if len(test) < 15:
+                test = np.concatenate([test, np.zeros(15 - len(test), np.uint16)])
+            amax = float(O.bf16_bits_to_f32(test & np.uint16(0x7FFF)).max())
+            anchor = f32_to_bf16_bits(np.array([amax * rho], np.float32))[0]
+            if not np.isfinite(O.bf16_bits_to_f32(anchor)):
+                continue
+            blocks.append(np.concatenate([[anchor], test]))
+    return np.array(blocks, dtype=np.uint16).reshape(-1, 16)
+
+
+def test_every_bf16_pattern_as_element():
+    """Every finite BF16 pattern with amax >= 2^-100, at 28 block-amax ratios
+    (1.13^j: y sweeps (0, 6])."""
+    rhos = [1.13 ** j for j in range(28)]
+    for e_lo in range(27, 255, 8):
+        e_hi = min(e_lo + 8, 255)
+        xb = _exponent_group_tensor(e_lo, e_hi, rhos)
+        assert_same(xb, f"exponents [{e_lo}, {e_hi})")
+
+
+def test_subnormal_elements():
+    g = np.random.Generator(np.random.PCG64(9))
+    sub = g.integers(1, 128, size=(32, 15)).astype(np.uint16) | np.where(
+        g.random((32, 15)) < 0.5, np.uint16(0x8000), np.uint16(0))
+    anchors = f32_to_bf16_bits(np.exp2(np.linspace(-100, -88, 32)).astype(np.float32))
+    xb = np.concatenate([anchors[:, None], sub.astype(np.uint16)], axis=1).reshape(-1, 32)
+    assert_same(xb, "subnormal elements")
+
+
+def test_scale_encoder_sweep():
+    """amax_g at each of the 128 BF16 mantissas in [1, 2); one block per BF16
+    magnitude in [amax_g 2^-20, amax_g]: E4M3 scales from 0 through the
+    subnormals to 448."""
+    g = np.random.Generator(np.random.PCG64(21))
+    for m in range(0, 128, 1):
+        A = np.uint16((127 << 7) | m)
+        Af = float(O.bf16_bits_to_f32(A))
+        lo = f32_to_bf16_bits(np.array([Af * 2.0 ** -20], np.float32))[0]
+        vals = np.arange(lo, A + 1, dtype=np.uint16)
+        sign = np.where(g.random(len(vals)) < 0.5, np.uint16(0x8000), np.uint16(0))
+        blocks = np.zeros((len(vals) + 1, 16), np.uint16)
+        blocks[0, 0] = A
+        blocks[1:, 0] = vals | sign
+        blocks[1:, 5] = vals // 2     # a smaller second element
+        if len(blocks) % 2:
+            blocks = np.concatenate([blocks, np.zeros((1, 16), np.uint16)])
+        assert_same(blocks.reshape(-1, 32), f"scale sweep m={m}")
+
+
+def test_zero_and_empty():
+    assert_same(np.zeros((3, 64), np.uint16), "zeros")
+    assert_same(np.full((2, 32), 0x8000, np.uint16), "negative zeros")
+    x = bf16_to_dev(np.zeros((0, 32), np.uint16))
+    codes, scales, gs = sol.nvfp4_quantize(x)
+    torch.cuda.synchronize()
+    assert codes.shape == (0, 16) and float(gs.cpu()[0]) == 0.0
+
+
+@pytest.mark.parametrize("nblk", [1, 2, 3, 4, 5, 7, 9, 1023, 1024, 1025, 4097])
+def test_block_count_tails(nblk):
+    xb = draw_activations("normal", 1, 16 * nblk, seed=nblk)
+    assert_same(xb, f"{nblk} blocks")
+
+
+def test_grid_stride_loop_and_determinism():
+    # 9.4M blocks: more than one grid-stride iteration of the encode kernel
+    xb = draw_activations("normal", 4608, 32768, seed=77)
+    x = bf16_to_dev(xb)
+    c1, s1, a1 = sol.nvfp4_quantize(x)
+    c2, s2, a2 = sol.nvfp4_quantize(x)
+    torch.cuda.synchronize()
+    assert torch.equal(c1, c2) and torch.equal(s1, s2) and torch.equal(a1, a2)
+    # rows spread over the tensor, incl. the one holding the global max
+    amax_row = int(np.argmax((xb & np.uint16(0x7FFF)).max(axis=1)))
+    rows = np.unique(np.r_[np.arange(0, 4608, 97), 4607, amax_row])
+    rc, rs, ra = O.nvfp4_quantize_ref(xb[rows])
+    assert f32_bits(a1.cpu().numpy()[0]) == f32_bits(ra)
+    assert np.array_equal(u8_from_dev(s1)[rows], rs)
+    assert np.array_equal(u8_from_dev(c1)[rows], rc)

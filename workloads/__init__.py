@@ -8,10 +8,12 @@ Shapes follow the denoisers the paper trains (Sec. 4.1 and the hyper-parameter
 table of the appendix: SANA at 1024^2, FLUX.1 and SD3.5-Large; rollouts per
 GPU from the Best-of-N setting).  The paper's prompts, weights and reward
 models are not used: activations and weights are random with the value
-distributions listed in ``LAYER_SETS``.
+distributions listed in ``WORKLOADS``.
 """
 from __future__ import annotations
 
+import os
+from concurrent.futures import ThreadPoolExecutor
 from dataclasses import dataclass, field
 
 import numpy as np
@@ -64,36 +66,42 @@ WORKLOADS = {
 
 ROLE_X, ROLE_W, ROLE_BIAS = 1, 2, 3
 
+#: Rows per independently seeded chunk: chunk c of a tensor with seed s draws
+#: from PCG64(SeedSequence(s).spawn(n_chunks)[c]), so tensors are generated in
+#: parallel and any row range can be regenerated on its own.
+CHUNK_ROWS = 256
+_THREADS = max(1, min(16, os.cpu_count() or 1))
+
 
 def seed_for(config_id: int, layer_index: int, role: int) -> int:
     return 1000 * config_id + 10 * layer_index + role
 
 
-def rng(seed: int) -> np.random.Generator:
+def rng(seed) -> np.random.Generator:
     return np.random.Generator(np.random.PCG64(seed))
 
 
 def f32_to_bf16_bits(a) -> np.ndarray:
     """Round float32 to BF16 bit patterns (nearest, ties to even); finite only."""
     u = np.ascontiguousarray(a, dtype=np.float32).view(np.uint32)
-    r = (u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))) >> np.uint32(16)
-    return r.astype(np.uint16)
+    t = u >> np.uint32(16)
+    t &= np.uint32(1)
+    t += np.uint32(0x7FFF)
+    t += u
+    t >>= np.uint32(16)
+    return t.astype(np.uint16)
 
 
 def _gelu_erf(z: np.ndarray) -> np.ndarray:
     from scipy.special import erf
-    z64 = z.astype(np.float64)
-    return (0.5 * z64 * (1.0 + erf(z64 / np.sqrt(2.0)))).astype(np.float32)
+    return (np.float32(0.5) * z * (np.float32(1.0) + erf(z * np.float32(0.70710677)))).astype(np.float32)
 
 
-def draw_activations(dist: str, rows: int, K: int, seed: int) -> np.ndarray:
-    """BF16 bit patterns [rows, K] of the named activation distribution."""
-    g = rng(seed)
+def _draw_chunk(dist: str, g: np.random.Generator, rows: int, K: int, cols) -> np.ndarray:
     if dist == "normal":
         x = g.standard_normal((rows, K), dtype=np.float32)
     elif dist == "outlier4x20":
         x = g.standard_normal((rows, K), dtype=np.float32)
-        cols = g.choice(K, size=min(4, K), replace=False)
         x[:, cols] *= np.float32(20.0)
     elif dist == "t3_1pct":
         x = g.standard_normal((rows, K), dtype=np.float32)
@@ -111,9 +119,52 @@ def draw_activations(dist: str, rows: int, K: int, seed: int) -> np.ndarray:
     return f32_to_bf16_bits(x)
 
 
-def draw_weights(N: int, K: int, sigma: float, seed: int) -> np.ndarray:
-    g = rng(seed)
-    return f32_to_bf16_bits(g.standard_normal((N, K), dtype=np.float32) * np.float32(sigma))
+def draw_activations(dist: str, rows: int, K: int, seed: int, row_range=None) -> np.ndarray:
+    """BF16 bit patterns [rows, K] of the named activation distribution; with
+    ``row_range=(r0, r1)`` only those rows of the same tensor."""
+    r0, r1 = (0, rows) if row_range is None else row_range
+    n_chunks = max(1, -(-rows // CHUNK_ROWS))
+    seeds = np.random.SeedSequence(seed).spawn(n_chunks)
+    cols = rng(seed).choice(K, size=min(4, K), replace=False) if dist == "outlier4x20" else None
+    out = np.empty((r1 - r0, K), dtype=np.uint16)
+    c0, c1 = r0 // CHUNK_ROWS, -(-r1 // CHUNK_ROWS)
+
+    def work(c):
+        lo, hi = c * CHUNK_ROWS, min(rows, (c + 1) * CHUNK_ROWS)
+        blk = _draw_chunk(dist, rng(seeds[c]), hi - lo, K, cols)
+        a, b = max(lo, r0), min(hi, r1)
+        out[a - r0:b - r0] = blk[a - lo:b - lo]
+
+    if c1 - c0 > 1:
+        with ThreadPoolExecutor(_THREADS) as ex:
+            list(ex.map(work, range(c0, c1)))
+    elif c1 > c0:
+        work(c0)
+    return out
+
+
+def draw_weights(N: int, K: int, sigma: float, seed: int, row_range=None) -> np.ndarray:
+    """BF16 bit patterns of an [N, K] weight ~ N(0, sigma^2)."""
+    r0, r1 = (0, N) if row_range is None else row_range
+    n_chunks = max(1, -(-N // CHUNK_ROWS))
+    seeds = np.random.SeedSequence(seed).spawn(n_chunks)
+    out = np.empty((r1 - r0, K), dtype=np.uint16)
+    c0, c1 = r0 // CHUNK_ROWS, -(-r1 // CHUNK_ROWS)
+
+    def work(c):
+        lo, hi = c * CHUNK_ROWS, min(N, (c + 1) * CHUNK_ROWS)
+        w = rng(seeds[c]).standard_normal((hi - lo, K), dtype=np.float32)
+        w *= np.float32(sigma)
+        blk = f32_to_bf16_bits(w)
+        a, b = max(lo, r0), min(hi, r1)
+        out[a - r0:b - r0] = blk[a - lo:b - lo]
+
+    if c1 - c0 > 1:
+        with ThreadPoolExecutor(_THREADS) as ex:
+            list(ex.map(work, range(c0, c1)))
+    elif c1 > c0:
+        work(c0)
+    return out
 
 
 def draw_bias(N: int, sigma: float, seed: int) -> np.ndarray:
