@@ -1,28 +1,39 @@
 // Block-scaled NVFP4 GEMM with BF16 output for gfx950.
 //
-//   out[m][n] = bf16( aA * aB * sum_k (sA qA)[m][k] (sB qB)[n][k] + bias[n] )
+//   out[m][n] = bf16( fp32( aA * aB * sum_k (sA qA)[m][k] (sB qB)[n][k] + bias[n] ) )
 //
 // How the E4M3-per-16 scales are applied.  CDNA4's scaled matrix
 // instructions take one power-of-two (E8M0) scale per 32 K-elements, while an
 // NVFP4 element decodes to q * s with an E4M3 s: up to 2 + 4 = 6 significant
-// bits per operand, more than any FP4/FP6/FP8 matrix input format carries.
-// The kernel therefore keeps the operands packed (0.5 B/element codes plus
-// 1/16 B/element scales) in HBM and LDS and dequantizes each element exactly
-// to FP16 in registers (hardware FP4->FP16 convert, then one packed FP16
-// multiply by the block scale: products of <= 6 significant bits in
-// [2^-10, 2688], exact), feeding the FP16 matrix cores
-// (v_mfma_f32_32x32x16_f16) with FP32 accumulation.  Every product
-// (sA qA)(sB qB) is exact; only the FP32 sums and the final BF16 rounding
-// round.  The per-tensor scales and the bias are applied once, in the
-// epilogue.
+// bits per operand, more than any FP4/FP6/FP8 matrix input carries.  So the
+// operands stay packed (0.5 B/element codes + 1/16 B/element scales) in HBM
+// and L2, and each element is dequantized exactly to FP16 (q * s has at most
+// 6 significant bits and lies in [2^-10, 2688]) before the FP16 matrix cores
+// (v_mfma_f32_32x32x16_f16, FP32 accumulation) consume it.  Every product
+// (sA qA)(sB qB) is exact; only the FP32 sums, the epilogue FMA and the BF16
+// rounding round.  The per-tensor scales and the bias are applied once, in
+// the epilogue.
 //
-// Tiling: 256 x 256 output tile per workgroup of 4 waves (2 x 2), each wave
-// owning 128 x 128 (4 x 4 MFMA tiles of 32 x 32, accumulators in AGPRs); K
-// advances 128 elements (8 NVFP4 blocks) per LDS stage, double buffered.
-// Inside a stage the wave walks 32-element chunks; lane (i, g) of a fragment
-// takes row i and the whole 16-element block 2c+g of chunk c, whose first 8
-// elements feed the chunk's first MFMA and last 8 its second (the same
-// K permutation is used for both operands, so the sum is unchanged).
+// Dequantization is shared by the whole workgroup: per K stage each pair of
+// threads owns one row of the A tile and one row of the B tile, each thread
+// converting 32 codes of each to FP16 and storing them to LDS, where all
+// eight waves read their MFMA operands.  Each element is converted once per
+// 256 x 256 output tile.
+// The conversion avoids the (half-rate) FP4 convert instructions: E2M1 values
+// have at most 2 significant bits, so the low byte of their FP16 encoding is
+// zero and the high byte comes from an 8-entry byte table indexed with
+// v_perm_b32 (sign bits are copied in by mask); one packed FP16 multiply then
+// applies the E4M3 block scale.
+//
+// Tiling: 256 x 256 output tile per workgroup of 8 waves (2 x 4, two per
+// SIMD so one wave's waits are covered by the other's MFMAs), each wave
+// owning 128 x 64 (4 x 2 MFMA tiles of 32 x 32, accumulators in AGPRs); K
+// advances 64 elements (4 NVFP4 blocks) per stage.  LDS holds two stages of
+// FP16 A and B tiles (rows padded to 144 bytes: conflict-free 16-byte row
+// accesses).  Packed codes for stage s+2 are fetched into registers while
+// stage s runs its MFMAs and stage s+1 is converted into the other LDS
+// buffer, so each stage ends with a single barrier.  The two threads of a
+// row load its 32 code bytes (and 4 scale bytes) with one coalesced request.
 // The MFMA's first operand is the weight tile, so each lane's accumulators
 // hold 4 consecutive output columns of one row (8-byte BF16 stores).
 #include "device_common.h"
@@ -32,122 +43,131 @@ namespace solfp4 {
 
 constexpr int kBM = 256;
 constexpr int kBN = 256;
-constexpr int kBKB = 8;                    // NVFP4 blocks per K stage (128 elements)
-constexpr int kCodeRow = kBKB * 8;         // code bytes per row per stage
-constexpr int kCodeStride = kCodeRow + 8;  // padded LDS row, bytes
-constexpr int kScaleStride = kBKB + 1;     // padded LDS row of f16x2 scales, words
-constexpr int kGemmThreads = 256;
-constexpr int kWaveTile = 128;
-constexpr int kFrags = kWaveTile / 32;     // 32x32 MFMA tiles per wave dimension
+constexpr int kBK = 64;                       // K elements per stage
+constexpr int kBlocksPerStage = kBK / 16;     // NVFP4 blocks per row per stage
+constexpr int kRowHalves = kBK + 8;           // padded LDS row (144 bytes)
+constexpr int kGemmThreads = 512;
+constexpr int kWaveTileM = 128;
+constexpr int kWaveTileN = 64;
+constexpr int kFragsM = kWaveTileM / 32;      // 32x32 MFMA tiles per wave, along M
+constexpr int kFragsN = kWaveTileN / 32;      // and along N
+constexpr int kSteps = kBK / 16;              // MFMA K-steps per stage
 
-struct Stage {
-  uint8_t a_codes[kBM * kCodeStride];
-  uint8_t b_codes[kBN * kCodeStride];
-  uint32_t a_scales[kBM * kScaleStride];
-  uint32_t b_scales[kBN * kScaleStride];
+struct Smem {
+  _Float16 a[2][kBM * kRowHalves];
+  _Float16 b[2][kBN * kRowHalves];
 };
 
-// f16x2 (s, s) bit pattern of an E4M3 scale byte (exact: every finite E4M3
-// value is a normal FP16 number).
-__device__ __forceinline__ uint32_t scale_f16x2(uint32_t c) {
-  const _Float16 sub = (_Float16)(float)c * (_Float16)0x1p-9f;
-  const uint32_t h = c >= 8u ? (c << 7) + 0x2000u : (uint32_t)__builtin_bit_cast(uint16_t, sub);
-  return h | (h << 16);
+// High bytes of the FP16 encodings of the E2M1 magnitudes 0, .5, 1, 1.5, 2,
+// 3, 4, 6 (their low bytes are 0), as the two source words of v_perm_b32.
+constexpr uint32_t kLutLo = 0x3E3C3800u;
+constexpr uint32_t kLutHi = 0x46444240u;
+
+// 8 E2M1 codes (element 2j in the low nibble of byte j) times the block
+// scale s2 = (s, s) in FP16, as 4 words of FP16 pairs (elements 2j, 2j+1).
+__device__ __forceinline__ void dequant8(uint32_t w, uint32_t s2, uint32_t (&d)[4]) {
+  // high bytes of the even elements (0, 2, 4, 6), signs in bit 7
+  const uint32_t ev = __builtin_amdgcn_perm(kLutHi, kLutLo, w & 0x07070707u) |
+                      ((w << 4) & 0x80808080u);
+  // and of the odd elements (1, 3, 5, 7)
+  const uint32_t od = __builtin_amdgcn_perm(kLutHi, kLutLo, (w >> 4) & 0x07070707u) |
+                      (w & 0x80808080u);
+  // interleave into FP16 pairs: [0, ev.byte j, 0, od.byte j]
+  const half2_t s = as_h2(s2);
+  d[0] = h2_as_u32(as_h2(__builtin_amdgcn_perm(od, ev, 0x040C000Cu)) * s);
+  d[1] = h2_as_u32(as_h2(__builtin_amdgcn_perm(od, ev, 0x050C010Cu)) * s);
+  d[2] = h2_as_u32(as_h2(__builtin_amdgcn_perm(od, ev, 0x060C020Cu)) * s);
+  d[3] = h2_as_u32(as_h2(__builtin_amdgcn_perm(od, ev, 0x070C030Cu)) * s);
 }
 
-// 8 E2M1 codes (one 32-bit word, element 2j in the low nibble of byte j)
-// times the block scale, as 8 exact FP16 values.
-__device__ __forceinline__ half8_t dequant8(uint32_t codes, uint32_t scale2) {
-  const half2_t s = as_h2(scale2);
-  const half2_t p0 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(codes, 1.0f, 0) * s;
-  const half2_t p1 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(codes, 1.0f, 1) * s;
-  const half2_t p2 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(codes, 1.0f, 2) * s;
-  const half2_t p3 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(codes, 1.0f, 3) * s;
-  return half8_t{p0.x, p0.y, p1.x, p1.y, p2.x, p2.y, p3.x, p3.y};
-}
-
-// Register-staged copy of one operand's stage: 4 x 16 code bytes and 8
-// scale bytes per thread.
-struct OperandRegs {
-  uint4 codes[4];
-  uint32_t sc_lo, sc_hi;
+// One thread's share of a stage: half a row of one operand, 32 codes (16
+// bytes, two NVFP4 blocks) and their 2 scales.
+struct HalfRow {
+  uint4 c;
+  uint32_t sc;   // two scale bytes in bits 0..15
 };
 
-// Thread t loads code units u = t + 256 p (p < 4), unit u = row u/4, bytes
-// 16 (u%4) .. +16 of the stage; and the 8 scale bytes of row t.
-// kFast: K % 128 == 0 (no partial stage; 16-byte code rows, 8-byte scale
-// rows are aligned).  Otherwise loads go by 8-byte block and scale byte,
-// each guarded against K.
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+
+// Buffer resources for one operand's 256-row tile: rows past the end of the
+// matrix fall outside num_records and read as zeros (code 0 with scale 0:
+// the value 0), so no load needs a branch.
+struct TileSrc {
+  __amdgpu_buffer_rsrc_t codes, scales;
+  uint32_t code_off, scale_off;   // this thread's half row, in bytes
+};
+
+__device__ __forceinline__ TileSrc make_tile_src(const uint8_t* codes, const uint8_t* scales,
+                                                 int64_t row0, int64_t rows, int64_t K, int t) {
+  const int64_t valid = min<int64_t>(rows - row0, 256);
+  const int r = t >> 1, h = t & 1;
+  TileSrc s;
+  s.codes = __builtin_amdgcn_make_buffer_rsrc((void*)(codes + row0 * (K / 2)), (short)0,
+                                              (int)(valid * (K / 2)), 0x00020000);
+  s.scales = __builtin_amdgcn_make_buffer_rsrc((void*)(scales + row0 * (K / 16)), (short)0,
+                                               (int)(valid * (K / 16)), 0x00020000);
+  s.code_off = (uint32_t)(r * (K / 2) + 16 * h);
+  s.scale_off = (uint32_t)(r * (K / 16) + 2 * h);
+  return s;
+}
+
+// Load this thread's half row of `stage`.  kFast: K % 64 == 0 (every stage
+// full; 16-byte code and 2-byte scale offsets aligned).  Otherwise 8-byte
+// code and 1-byte scale loads, and blocks past K are zeroed.
 template <bool kFast>
-__device__ __forceinline__ void load_operand(OperandRegs& r, const uint8_t* __restrict__ codes,
-                                             const uint8_t* __restrict__ scales, int64_t row0,
-                                             int64_t rows, int64_t K, int stage) {
-  const int t = threadIdx.x;
-  const int64_t kb_total = K / 16;
-  const int64_t kb0 = (int64_t)stage * kBKB;
+__device__ __forceinline__ void load_half(HalfRow& r, const TileSrc& src, int64_t K, int stage,
+                                          int h) {
+  const uint32_t co = src.code_off + (uint32_t)stage * (kBK / 2);
+  const uint32_t so = src.scale_off + (uint32_t)stage * kBlocksPerStage;
+  if (kFast) {
+    const u32x4_t a = __builtin_amdgcn_raw_buffer_load_b128(src.codes, co, 0, 0);
+    r.c = make_uint4(a.x, a.y, a.z, a.w);
+    r.sc = __builtin_amdgcn_raw_buffer_load_b16(src.scales, so, 0, 0);
+  } else {
+    const int64_t kb_left = K / 16 - (int64_t)stage * kBlocksPerStage - 2 * h;
+    u32x2_t blk[2];
+    uint32_t sc = 0;
 #pragma unroll
-  for (int p = 0; p < 4; ++p) {
-    const int u = t + kGemmThreads * p;
-    const int64_t row = row0 + (u >> 2);
-    const int col = u & 3;
-    const int64_t kb = kb0 + 2 * col;
-    uint4 v = make_uint4(0, 0, 0, 0);
-    if (row < rows) {
-      const uint8_t* src = codes + row * (K / 2) + kb * 8;
-      if (kFast) {
-        v = *reinterpret_cast<const uint4*>(src);
-      } else {
-        if (kb < kb_total) {
-          const uint2 lo = *reinterpret_cast<const uint2*>(src);
-          v.x = lo.x;
-          v.y = lo.y;
-        }
-        if (kb + 1 < kb_total) {
-          const uint2 hi = *reinterpret_cast<const uint2*>(src + 8);
-          v.z = hi.x;
-          v.w = hi.y;
-        }
-      }
+    for (int j = 0; j < 2; ++j) {
+      blk[j] = __builtin_amdgcn_raw_buffer_load_b64(src.codes, co + 8 * j, 0, 0);
+      const uint32_t b = __builtin_amdgcn_raw_buffer_load_b8(src.scales, so + j, 0, 0);
+      const bool ok = j < kb_left;
+      blk[j] = ok ? blk[j] : u32x2_t{0, 0};
+      sc |= (ok ? b : 0u) << (8 * j);
     }
-    r.codes[p] = v;
-  }
-  const int64_t srow = row0 + t;
-  r.sc_lo = 0;
-  r.sc_hi = 0;
-  if (srow < rows) {
-    const uint8_t* src = scales + srow * kb_total + kb0;
-    if (kFast) {
-      const uint2 s = *reinterpret_cast<const uint2*>(src);
-      r.sc_lo = s.x;
-      r.sc_hi = s.y;
-    } else {
-      uint32_t lo = 0, hi = 0;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        if (kb0 + j < kb_total) lo |= (uint32_t)src[j] << (8 * j);
-        if (kb0 + 4 + j < kb_total) hi |= (uint32_t)src[4 + j] << (8 * j);
-      }
-      r.sc_lo = lo;
-      r.sc_hi = hi;
-    }
+    r.c = make_uint4(blk[0].x, blk[0].y, blk[1].x, blk[1].y);
+    r.sc = sc;
   }
 }
 
-__device__ __forceinline__ void store_operand(const OperandRegs& r, uint8_t* lds_codes,
-                                              uint32_t* lds_scales) {
-  const int t = threadIdx.x;
+// Convert block j (0 or 1) of a half row and store its 16 FP16 values.  The
+// E4M3 scale byte shifted into an FP16 bit pattern reads as s * 2^-8 (the
+// two formats align their mantissa fields, and E4M3 subnormals become FP16
+// subnormals); one exact multiply by 2^8 restores s.
+__device__ __forceinline__ void convert_block(const HalfRow& r, int j, _Float16* dst) {
+  const half2_t k256 = {(_Float16)256.0f, (_Float16)256.0f};
+  const uint32_t c = (r.sc >> (8 * j)) & 0xFFu;
+  const uint32_t s2 = h2_as_u32(as_h2((c << 7) | (c << 23)) * k256);
+  const uint32_t w0 = j == 0 ? r.c.x : r.c.z;
+  const uint32_t w1 = j == 0 ? r.c.y : r.c.w;
+  uint32_t d[4], e[4];
+  dequant8(w0, s2, d);
+  dequant8(w1, s2, e);
+  *reinterpret_cast<uint4*>(dst + 16 * j) = make_uint4(d[0], d[1], d[2], d[3]);
+  *reinterpret_cast<uint4*>(dst + 16 * j + 8) = make_uint4(e[0], e[1], e[2], e[3]);
+}
+
+// Scheduling of one K-step segment (after its operand reads are fenced
+// off): each of the 8 MFMAs is followed by up to 5 VALU instructions of the
+// next stage's conversion, and the conversion's 2 LDS stores go last, so the
+// conversion runs in the shadow of the matrix pipeline.
+__device__ __forceinline__ void interleave_step() {
 #pragma unroll
-  for (int p = 0; p < 4; ++p) {
-    const int u = t + kGemmThreads * p;
-    uint8_t* dst = lds_codes + (u >> 2) * kCodeStride + (u & 3) * 16;
-    *reinterpret_cast<uint2*>(dst) = make_uint2(r.codes[p].x, r.codes[p].y);
-    *reinterpret_cast<uint2*>(dst + 8) = make_uint2(r.codes[p].z, r.codes[p].w);
-  }
-  uint32_t* srow = lds_scales + t * kScaleStride;
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    srow[j] = scale_f16x2((r.sc_lo >> (8 * j)) & 0xFFu);
-    srow[4 + j] = scale_f16x2((r.sc_hi >> (8 * j)) & 0xFFu);
+  for (int i = 0; i < kFragsM * kFragsN; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
+    __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);   // VALU
+    if (i >= 6) __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);    // DS write
   }
 }
 
@@ -179,7 +199,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void nvfp4_gemm_kernel(
     const uint8_t* __restrict__ b_scales, const float* __restrict__ b_gs,
     const uint16_t* __restrict__ bias, uint16_t* __restrict__ out, int64_t M, int64_t N,
     int64_t K) {
-  __shared__ Stage smem[2];
+  __shared__ Smem smem;
 
   const int tiles_m = (int)((M + kBM - 1) / kBM);
   const int tiles_n = (int)((N + kBN - 1) / kBN);
@@ -188,81 +208,105 @@ __global__ __launch_bounds__(kGemmThreads, 1) void nvfp4_gemm_kernel(
   const int64_t m0 = (int64_t)tm * kBM;
   const int64_t n0 = (int64_t)tn * kBN;
 
-  const int lane = threadIdx.x & (kWave - 1);
-  const int wave = threadIdx.x / kWave;
-  const int wm = wave >> 1;
-  const int wn = wave & 1;
+  const int t = threadIdx.x;
+  const int lane = t & (kWave - 1);
+  const int wave = t / kWave;
+  const int wm = wave >> 2;
+  const int wn = wave & 3;
   const int li = lane & 31;
   const int lg = lane >> 5;
+  const int h = t & 1;
 
-  floatx16_t acc[kFrags][kFrags];
+  floatx16_t acc[kFragsN][kFragsM];
 #pragma unroll
-  for (int i = 0; i < kFrags; ++i)
+  for (int i = 0; i < kFragsN; ++i)
 #pragma unroll
-    for (int j = 0; j < kFrags; ++j) acc[i][j] = floatx16_t{};
+    for (int j = 0; j < kFragsM; ++j) acc[i][j] = floatx16_t{};
 
-  const int nstages = (int)((K + kBKB * 16 - 1) / (kBKB * 16));
-  OperandRegs ra, rb;
-  if (nstages > 0) {
-    load_operand<kFast>(ra, a_codes, a_scales, m0, M, K, 0);
-    load_operand<kFast>(rb, b_codes, b_scales, n0, N, K, 0);
-    store_operand(ra, smem[0].a_codes, smem[0].a_scales);
-    store_operand(rb, smem[0].b_codes, smem[0].b_scales);
-  }
+  const int nstages = (int)((K + kBK - 1) / kBK);
+  const TileSrc src_a = make_tile_src(a_codes, a_scales, m0, M, K, t);
+  const TileSrc src_b = make_tile_src(b_codes, b_scales, n0, N, K, t);
+  // this thread's half row in an LDS stage buffer
+  const int my = (t >> 1) * kRowHalves + 32 * h;
+  HalfRow pa[2], pb[2];
+  // prologue: stage 0 converted into buffer 0, stage 1 in flight
+  load_half<kFast>(pa[0], src_a, K, 0, h);
+  load_half<kFast>(pb[0], src_b, K, 0, h);
+  load_half<kFast>(pa[1], src_a, K, 1, h);
+  load_half<kFast>(pb[1], src_b, K, 1, h);
+  convert_block(pa[0], 0, &smem.a[0][my]);
+  convert_block(pa[0], 1, &smem.a[0][my]);
+  convert_block(pb[0], 0, &smem.b[0][my]);
+  convert_block(pb[0], 1, &smem.b[0][my]);
   __syncthreads();
 
-  for (int s = 0; s < nstages; ++s) {
-    const bool more = s + 1 < nstages;
-    if (more) {
-      load_operand<kFast>(ra, a_codes, a_scales, m0, M, K, s + 1);
-      load_operand<kFast>(rb, b_codes, b_scales, n0, N, K, s + 1);
-    }
-    const Stage& st = smem[s & 1];
+  // One stage, branch free: MFMAs on buffer cur (stage s); conversion of the
+  // registers holding stage s+1 into buffer cur^1; loads of stage s+2 into
+  // the registers stage s used.  Past the last stage the loads read zeros or
+  // unused data and the conversion fills the buffer nobody reads again.
+  auto run_stage = [&](int s, HalfRow& ld_a, HalfRow& ld_b, const HalfRow& cv_a,
+                       const HalfRow& cv_b) {
+    const int cur = s & 1;
+    load_half<kFast>(ld_a, src_a, K, s + 2, h);
+    load_half<kFast>(ld_b, src_b, K, s + 2, h);
+    const _Float16* sa = smem.a[cur] + (wm * kWaveTileM + li) * kRowHalves + 8 * lg;
+    const _Float16* sb = smem.b[cur] + (wn * kWaveTileN + li) * kRowHalves + 8 * lg;
+    _Float16* na = &smem.a[cur ^ 1][my];
+    _Float16* nb = &smem.b[cur ^ 1][my];
+    half8_t af[2][kFragsM], bf[2][kFragsN];
 #pragma unroll
-    for (int c = 0; c < kBKB / 2; ++c) {
-      const int blk = 2 * c + lg;
-      half8_t af[kFrags][2], bf[kFrags][2];
+    for (int f = 0; f < kFragsM; ++f) af[0][f] = *reinterpret_cast<const half8_t*>(sa + f * 32 * kRowHalves);
 #pragma unroll
-      for (int f = 0; f < kFrags; ++f) {
-        const int ra_row = wm * kWaveTile + f * 32 + li;
-        const uint2 ac = *reinterpret_cast<const uint2*>(st.a_codes + ra_row * kCodeStride + blk * 8);
-        const uint32_t as = st.a_scales[ra_row * kScaleStride + blk];
-        af[f][0] = dequant8(ac.x, as);
-        af[f][1] = dequant8(ac.y, as);
-        const int rb_row = wn * kWaveTile + f * 32 + li;
-        const uint2 bc = *reinterpret_cast<const uint2*>(st.b_codes + rb_row * kCodeStride + blk * 8);
-        const uint32_t bs = st.b_scales[rb_row * kScaleStride + blk];
-        bf[f][0] = dequant8(bc.x, bs);
-        bf[f][1] = dequant8(bc.y, bs);
+    for (int f = 0; f < kFragsN; ++f) bf[0][f] = *reinterpret_cast<const half8_t*>(sb + f * 32 * kRowHalves);
+#pragma unroll
+    for (int st = 0; st < kSteps; ++st) {
+      const int c = st & 1;
+      // operand reads for the next K-step go out first: they have this
+      // step's MFMAs to complete
+      if (st + 1 < kSteps) {
+#pragma unroll
+        for (int f = 0; f < kFragsM; ++f)
+          af[c ^ 1][f] = *reinterpret_cast<const half8_t*>(sa + f * 32 * kRowHalves + 16 * (st + 1));
+#pragma unroll
+        for (int f = 0; f < kFragsN; ++f)
+          bf[c ^ 1][f] = *reinterpret_cast<const half8_t*>(sb + f * 32 * kRowHalves + 16 * (st + 1));
       }
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int h = 0; h < 2; ++h)
+      for (int fn = 0; fn < kFragsN; ++fn)
 #pragma unroll
-        for (int fn = 0; fn < kFrags; ++fn)
-#pragma unroll
-          for (int fm = 0; fm < kFrags; ++fm)
-            acc[fn][fm] = __builtin_amdgcn_mfma_f32_32x32x16_f16(bf[fn][h], af[fm][h], acc[fn][fm], 0, 0, 0);
-    }
-    if (more) {
-      Stage& nx = smem[(s + 1) & 1];
-      store_operand(ra, nx.a_codes, nx.a_scales);
-      store_operand(rb, nx.b_codes, nx.b_scales);
+        for (int fm = 0; fm < kFragsM; ++fm)
+          acc[fn][fm] = __builtin_amdgcn_mfma_f32_32x32x16_f16(bf[c][fn], af[c][fm], acc[fn][fm], 0, 0, 0);
+      // a quarter of the next stage's conversion per K-step
+      if (st == 0) convert_block(cv_a, 0, na);
+      if (st == 1) convert_block(cv_a, 1, na);
+      if (st == 2) convert_block(cv_b, 0, nb);
+      if (st == 3) convert_block(cv_b, 1, nb);
+      interleave_step();
+      __builtin_amdgcn_sched_barrier(0);
     }
     __syncthreads();
-  }
+  };
 
-  // epilogue: out = bf16(alpha * acc + bias), alpha = aA * aB in FP32
+  int s = 0;
+  for (; s + 1 < nstages; s += 2) {
+    run_stage(s, pa[0], pb[0], pa[1], pb[1]);
+    run_stage(s + 1, pa[1], pb[1], pa[0], pb[0]);
+  }
+  if (s < nstages) run_stage(s, pa[0], pb[0], pa[1], pb[1]);
+
+  // epilogue: out = bf16(fp32(alpha * acc + bias)), alpha = aA * aB in FP32
   const float alpha = a_gs[0] * b_gs[0];
 #pragma unroll
-  for (int fm = 0; fm < kFrags; ++fm) {
-    const int64_t m = m0 + wm * kWaveTile + fm * 32 + li;
+  for (int fm = 0; fm < kFragsM; ++fm) {
+    const int64_t m = m0 + wm * kWaveTileM + fm * 32 + li;
     if (m >= M) continue;
     uint16_t* orow = out + m * N;
 #pragma unroll
-    for (int fn = 0; fn < kFrags; ++fn) {
+    for (int fn = 0; fn < kFragsN; ++fn) {
 #pragma unroll
       for (int k = 0; k < 4; ++k) {
-        const int64_t n = n0 + wn * kWaveTile + fn * 32 + 8 * k + 4 * lg;
+        const int64_t n = n0 + wn * kWaveTileN + fn * 32 + 8 * k + 4 * lg;
         float v[4];
 #pragma unroll
         for (int q = 0; q < 4; ++q) v[q] = acc[fn][fm][4 * k + q];
@@ -300,7 +344,7 @@ hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const fl
   if (M == 0 || N == 0) return hipSuccess;
   const int64_t tiles = ((M + kBM - 1) / kBM) * ((N + kBN - 1) / kBN);
   const dim3 grid((unsigned)tiles), block(kGemmThreads);
-  const bool fast = K % 128 == 0;
+  const bool fast = K % kBK == 0;
   const bool vec = N % 4 == 0;
   if (fast && vec)
     hipLaunchKernelGGL((nvfp4_gemm_kernel<true, true>), grid, block, 0, stream, a_codes, a_scales,
