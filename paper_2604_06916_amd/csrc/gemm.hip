@@ -36,6 +36,8 @@
 // row load its 32 code bytes (and 4 scale bytes) with one coalesced request.
 // The MFMA's first operand is the weight tile, so each lane's accumulators
 // hold 4 consecutive output columns of one row (8-byte BF16 stores).
+#include <type_traits>
+
 #include "device_common.h"
 #include "kernels.h"
 
@@ -81,10 +83,9 @@ __device__ __forceinline__ void dequant8(uint32_t w, uint32_t s2, uint32_t (&d)[
 }
 
 // One thread's share of a stage: half a row of one operand, 32 codes (16
-// bytes, two NVFP4 blocks) and their 2 scales.
+// bytes, two NVFP4 blocks).  Scales arrive separately, four stages at a time.
 struct HalfRow {
   uint4 c;
-  uint32_t sc;   // two scale bytes in bits 0..15
 };
 
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
@@ -95,59 +96,93 @@ typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 // the value 0), so no load needs a branch.
 struct TileSrc {
   __amdgpu_buffer_rsrc_t codes, scales;
-  uint32_t code_off, scale_off;   // this thread's half row, in bytes
+  uint32_t code_off, scale_off;   // this thread's half row / row, in bytes
 };
+
+// A buffer resource from wave-uniform values: readfirstlane pins the base
+// and size to scalar registers, so loads through it need no per-lane
+// descriptor handling.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t uniform_rsrc(const void* base, int64_t bytes) {
+  const uint64_t p = (uint64_t)base;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)p);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(p >> 32));
+  const int n = __builtin_amdgcn_readfirstlane((int)bytes);
+  return __builtin_amdgcn_make_buffer_rsrc((void*)(((uint64_t)hi << 32) | lo), (short)0, n,
+                                           0x00020000);
+}
 
 __device__ __forceinline__ TileSrc make_tile_src(const uint8_t* codes, const uint8_t* scales,
                                                  int64_t row0, int64_t rows, int64_t K, int t) {
   const int64_t valid = min<int64_t>(rows - row0, 256);
   const int r = t >> 1, h = t & 1;
   TileSrc s;
-  s.codes = __builtin_amdgcn_make_buffer_rsrc((void*)(codes + row0 * (K / 2)), (short)0,
-                                              (int)(valid * (K / 2)), 0x00020000);
-  s.scales = __builtin_amdgcn_make_buffer_rsrc((void*)(scales + row0 * (K / 16)), (short)0,
-                                               (int)(valid * (K / 16)), 0x00020000);
+  s.codes = uniform_rsrc(codes + row0 * (K / 2), valid * (K / 2));
+  s.scales = uniform_rsrc(scales + row0 * (K / 16), valid * (K / 16));
   s.code_off = (uint32_t)(r * (K / 2) + 16 * h);
-  s.scale_off = (uint32_t)(r * (K / 16) + 2 * h);
+  s.scale_off = (uint32_t)(r * (K / 16));
   return s;
 }
 
-// Load this thread's half row of `stage`.  kFast: K % 64 == 0 (every stage
-// full; 16-byte code and 2-byte scale offsets aligned).  Otherwise 8-byte
-// code and 1-byte scale loads, and blocks past K are zeroed.
+// Load this thread's 16 code bytes of `stage`.  kFast: K % 64 == 0 (every
+// stage full, 16-byte offsets aligned).  Otherwise two 8-byte loads, and
+// blocks past K are zeroed.
 template <bool kFast>
-__device__ __forceinline__ void load_half(HalfRow& r, const TileSrc& src, int64_t K, int stage,
-                                          int h) {
+__device__ __forceinline__ void load_codes(HalfRow& r, const TileSrc& src, int64_t K, int stage,
+                                           int h) {
   const uint32_t co = src.code_off + (uint32_t)stage * (kBK / 2);
-  const uint32_t so = src.scale_off + (uint32_t)stage * kBlocksPerStage;
   if (kFast) {
     const u32x4_t a = __builtin_amdgcn_raw_buffer_load_b128(src.codes, co, 0, 0);
     r.c = make_uint4(a.x, a.y, a.z, a.w);
-    r.sc = __builtin_amdgcn_raw_buffer_load_b16(src.scales, so, 0, 0);
   } else {
     const int64_t kb_left = K / 16 - (int64_t)stage * kBlocksPerStage - 2 * h;
     u32x2_t blk[2];
-    uint32_t sc = 0;
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
       blk[j] = __builtin_amdgcn_raw_buffer_load_b64(src.codes, co + 8 * j, 0, 0);
-      const uint32_t b = __builtin_amdgcn_raw_buffer_load_b8(src.scales, so + j, 0, 0);
-      const bool ok = j < kb_left;
-      blk[j] = ok ? blk[j] : u32x2_t{0, 0};
-      sc |= (ok ? b : 0u) << (8 * j);
+      blk[j] = j < kb_left ? blk[j] : u32x2_t{0, 0};
     }
     r.c = make_uint4(blk[0].x, blk[0].y, blk[1].x, blk[1].y);
-    r.sc = sc;
   }
 }
 
-// Convert block j (0 or 1) of a half row and store its 16 FP16 values.  The
+// The row's 16 scale bytes for stages 4g .. 4g+3 (both threads of a row load
+// the same bytes: one coalesced request).  Byte 4j + b is block b of stage
+// 4g + j.  Blocks past K are zeroed.
+template <bool kFast>
+__device__ __forceinline__ u32x4_t load_scales(const TileSrc& src, int64_t K, int g) {
+  const uint32_t so = src.scale_off + (uint32_t)g * 16;
+  if (kFast && (K / 16) % 16 == 0) {
+    return __builtin_amdgcn_raw_buffer_load_b128(src.scales, so, 0, 0);
+  } else if (kFast) {
+    // 4-byte aligned (K % 64 == 0); stages past K read other rows or zeros
+    // and are never converted into a used buffer
+    u32x4_t v;
+    v.x = __builtin_amdgcn_raw_buffer_load_b32(src.scales, so, 0, 0);
+    v.y = __builtin_amdgcn_raw_buffer_load_b32(src.scales, so + 4, 0, 0);
+    v.z = __builtin_amdgcn_raw_buffer_load_b32(src.scales, so + 8, 0, 0);
+    v.w = __builtin_amdgcn_raw_buffer_load_b32(src.scales, so + 12, 0, 0);
+    return v;
+  } else {
+    const int64_t kb_left = K / 16 - (int64_t)g * 16;
+    uint32_t w[4] = {0, 0, 0, 0};
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const uint32_t b = __builtin_amdgcn_raw_buffer_load_b8(src.scales, so + i, 0, 0);
+      w[i / 4] |= (i < kb_left ? b : 0u) << (8 * (i % 4));
+    }
+    return u32x4_t{w[0], w[1], w[2], w[3]};
+  }
+}
+
+// Convert block j (0 or 1) of a half row (scale bytes of its two blocks in
+// sc2) and store its 16 FP16 values.  The
 // E4M3 scale byte shifted into an FP16 bit pattern reads as s * 2^-8 (the
 // two formats align their mantissa fields, and E4M3 subnormals become FP16
 // subnormals); one exact multiply by 2^8 restores s.
-__device__ __forceinline__ void convert_block(const HalfRow& r, int j, _Float16* dst) {
+__device__ __forceinline__ void convert_block(const HalfRow& r, uint32_t sc2, int j,
+                                              _Float16* dst) {
   const half2_t k256 = {(_Float16)256.0f, (_Float16)256.0f};
-  const uint32_t c = (r.sc >> (8 * j)) & 0xFFu;
+  const uint32_t c = (sc2 >> (8 * j)) & 0xFFu;
   const uint32_t s2 = h2_as_u32(as_h2((c << 7) | (c << 23)) * k256);
   const uint32_t w0 = j == 0 ? r.c.x : r.c.z;
   const uint32_t w1 = j == 0 ? r.c.y : r.c.w;
@@ -228,27 +263,50 @@ __global__ __launch_bounds__(kGemmThreads, 1) void nvfp4_gemm_kernel(
   const TileSrc src_b = make_tile_src(b_codes, b_scales, n0, N, K, t);
   // this thread's half row in an LDS stage buffer
   const int my = (t >> 1) * kRowHalves + 32 * h;
-  HalfRow pa[2], pb[2];
-  // prologue: stage 0 converted into buffer 0, stage 1 in flight
-  load_half<kFast>(pa[0], src_a, K, 0, h);
-  load_half<kFast>(pb[0], src_b, K, 0, h);
-  load_half<kFast>(pa[1], src_a, K, 1, h);
-  load_half<kFast>(pb[1], src_b, K, 1, h);
-  convert_block(pa[0], 0, &smem.a[0][my]);
-  convert_block(pa[0], 1, &smem.a[0][my]);
-  convert_block(pb[0], 0, &smem.b[0][my]);
-  convert_block(pb[0], 1, &smem.b[0][my]);
+  // this thread's two scale bytes of stage s sit in word s%4 of its group's
+  // scale registers, at byte offset 2h
+  const int sshift = 16 * h;
+  HalfRow ca[2], cb[2];
+  u32x4_t sa4[2], sb4[2];
+  // prologue: scales of stages 0-7, codes of stages 0-1; stage 0 converted
+  // into buffer 0
+  sa4[0] = load_scales<kFast>(src_a, K, 0);
+  sb4[0] = load_scales<kFast>(src_b, K, 0);
+  sa4[1] = load_scales<kFast>(src_a, K, 1);
+  sb4[1] = load_scales<kFast>(src_b, K, 1);
+  load_codes<kFast>(ca[0], src_a, K, 0, h);
+  load_codes<kFast>(cb[0], src_b, K, 0, h);
+  load_codes<kFast>(ca[1], src_a, K, 1, h);
+  load_codes<kFast>(cb[1], src_b, K, 1, h);
+  convert_block(ca[0], sa4[0].x >> sshift, 0, &smem.a[0][my]);
+  convert_block(ca[0], sa4[0].x >> sshift, 1, &smem.a[0][my]);
+  convert_block(cb[0], sb4[0].x >> sshift, 0, &smem.b[0][my]);
+  convert_block(cb[0], sb4[0].x >> sshift, 1, &smem.b[0][my]);
   __syncthreads();
 
-  // One stage, branch free: MFMAs on buffer cur (stage s); conversion of the
-  // registers holding stage s+1 into buffer cur^1; loads of stage s+2 into
-  // the registers stage s used.  Past the last stage the loads read zeros or
-  // unused data and the conversion fills the buffer nobody reads again.
-  auto run_stage = [&](int s, HalfRow& ld_a, HalfRow& ld_b, const HalfRow& cv_a,
-                       const HalfRow& cv_b) {
+  // One stage, branch free.  P = s % 8 selects the register sets: codes of
+  // stage s+1 (converted now into buffer cur^1) are in set (P+1)%2 and the
+  // loads of stage s+2 go to set P%2; scales of stage s+1 are in group set
+  // ((P+1)/4)%2, and at P == 0 / P == 4 the scales of the group after next
+  // are fetched into the set the previous group used.  Past the last stage
+  // the loads read zeros or unused data and the conversion fills the buffer
+  // nobody reads again.
+  auto run_stage = [&](auto phase, int s) {
+    constexpr int P = decltype(phase)::value;
+    constexpr int kc = P & 1;              // code set loaded now (stage s+2)
+    constexpr int kn = (P + 1) & 1;        // code set converted now (stage s+1)
+    constexpr int gn = ((P + 1) >> 2) & 1; // scale set of stage s+1
+    constexpr int wn_ = (P + 1) & 3;       // word of stage s+1 in its group
     const int cur = s & 1;
-    load_half<kFast>(ld_a, src_a, K, s + 2, h);
-    load_half<kFast>(ld_b, src_b, K, s + 2, h);
+    if (P == 0 || P == 4) {
+      constexpr int gl = P == 0 ? 1 : 0;   // set receiving group s/4 + 1
+      sa4[gl] = load_scales<kFast>(src_a, K, s / 4 + 1);
+      sb4[gl] = load_scales<kFast>(src_b, K, s / 4 + 1);
+    }
+    load_codes<kFast>(ca[kc], src_a, K, s + 2, h);
+    load_codes<kFast>(cb[kc], src_b, K, s + 2, h);
+    const uint32_t sca = sa4[gn][wn_] >> sshift;
+    const uint32_t scb = sb4[gn][wn_] >> sshift;
     const _Float16* sa = smem.a[cur] + (wm * kWaveTileM + li) * kRowHalves + 8 * lg;
     const _Float16* sb = smem.b[cur] + (wn * kWaveTileN + li) * kRowHalves + 8 * lg;
     _Float16* na = &smem.a[cur ^ 1][my];
@@ -278,22 +336,43 @@ __global__ __launch_bounds__(kGemmThreads, 1) void nvfp4_gemm_kernel(
         for (int fm = 0; fm < kFragsM; ++fm)
           acc[fn][fm] = __builtin_amdgcn_mfma_f32_32x32x16_f16(bf[c][fn], af[c][fm], acc[fn][fm], 0, 0, 0);
       // a quarter of the next stage's conversion per K-step
-      if (st == 0) convert_block(cv_a, 0, na);
-      if (st == 1) convert_block(cv_a, 1, na);
-      if (st == 2) convert_block(cv_b, 0, nb);
-      if (st == 3) convert_block(cv_b, 1, nb);
+      if (st == 0) convert_block(ca[kn], sca, 0, na);
+      if (st == 1) convert_block(ca[kn], sca, 1, na);
+      if (st == 2) convert_block(cb[kn], scb, 0, nb);
+      if (st == 3) convert_block(cb[kn], scb, 1, nb);
       interleave_step();
       __builtin_amdgcn_sched_barrier(0);
     }
     __syncthreads();
   };
 
+  using P0 = std::integral_constant<int, 0>;
+  using P1 = std::integral_constant<int, 1>;
+  using P2 = std::integral_constant<int, 2>;
+  using P3 = std::integral_constant<int, 3>;
+  using P4 = std::integral_constant<int, 4>;
+  using P5 = std::integral_constant<int, 5>;
+  using P6 = std::integral_constant<int, 6>;
+  using P7 = std::integral_constant<int, 7>;
   int s = 0;
-  for (; s + 1 < nstages; s += 2) {
-    run_stage(s, pa[0], pb[0], pa[1], pb[1]);
-    run_stage(s + 1, pa[1], pb[1], pa[0], pb[0]);
+  for (; s + 8 <= nstages; s += 8) {
+    run_stage(P0{}, s);
+    run_stage(P1{}, s + 1);
+    run_stage(P2{}, s + 2);
+    run_stage(P3{}, s + 3);
+    run_stage(P4{}, s + 4);
+    run_stage(P5{}, s + 5);
+    run_stage(P6{}, s + 6);
+    run_stage(P7{}, s + 7);
   }
-  if (s < nstages) run_stage(s, pa[0], pb[0], pa[1], pb[1]);
+  const int rest = nstages - s;
+  if (rest > 0) run_stage(P0{}, s);
+  if (rest > 1) run_stage(P1{}, s + 1);
+  if (rest > 2) run_stage(P2{}, s + 2);
+  if (rest > 3) run_stage(P3{}, s + 3);
+  if (rest > 4) run_stage(P4{}, s + 4);
+  if (rest > 5) run_stage(P5{}, s + 5);
+  if (rest > 6) run_stage(P6{}, s + 6);
 
   // epilogue: out = bf16(fp32(alpha * acc + bias)), alpha = aA * aB in FP32
   const float alpha = a_gs[0] * b_gs[0];
