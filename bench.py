@@ -38,7 +38,34 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=256, help="oracle sample: activation rows")
     ap.add_argument("--cpu-wrows", type=int, default=1024, help="oracle sample: weight rows")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
+                    help="after the benchmark, run a plain device-to-device copy of BYTES "
+                         "three times (reference for HBM traffic counters)")
     return ap.parse_args()
+
+
+GEMM_SOURCE = os.path.join(ROOT, "paper_2604_06916_amd", "csrc", "gemm.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "nvfp4_gemm_flux-12b_traffic.txt")
+
+
+def source_hash(path):
+    import hashlib
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def measured_traffic():
+    """HBM bytes per GEMM launch (FETCH_SIZE + WRITE_SIZE, scaled by a plain
+    copy's reading of the same counters) from the committed counter summary,
+    or None when the kernel source changed since the counters were taken."""
+    try:
+        lines = open(TRAFFIC_FILE).read().splitlines()
+    except OSError:
+        return None
+    kv = dict(l.split("=", 1) for l in lines if "=" in l and not l.startswith("#"))
+    if kv.get("gemm_source_sha256_16") != source_hash(GEMM_SOURCE):
+        return None
+    return float(kv["gemm_hbm_bytes_per_launch_avg"])
 
 
 def cpu_baseline(wl, rows, wrows):
@@ -199,7 +226,9 @@ def main():
             "peak": PEAK_FP16_MFMA_TFLOPS,
             "unit": "TFLOP/s",
             "frac": round(gemm_tflops / PEAK_FP16_MFMA_TFLOPS, 4),
-            "traffic": None,
+            "traffic": measured_traffic(),
+            "traffic_unit": "HBM bytes per launch (mean over the step's GEMMs)",
+            "algorithmic_flops_per_launch": flops_step / len(layers),
         },
         "gemm_frac_fp4_peak": round(gemm_tflops / PEAK_FP4_MFMA_TFLOPS, 4),
         "quantize": {
@@ -216,6 +245,13 @@ def main():
     }
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, args.cpu_rows, args.cpu_wrows)
+    if args.copy_calibration:
+        n = args.copy_calibration
+        src = torch.empty(n, dtype=torch.uint8, device=dev)
+        dst = torch.empty(n, dtype=torch.uint8, device=dev)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
     print(json.dumps(result), flush=True)
 
 
