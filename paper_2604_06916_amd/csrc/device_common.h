@@ -35,29 +35,17 @@ __device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
   return v;
 }
 
-// E4M3 (OCP E4M3FN) of a non-negative binary32 value: nearest, ties to the
-// even code, saturating at 448.  Returns the code and writes the exact value
-// of that code to *value.  Normal range: round the binary32 significand to 3
-// bits with the carry allowed into the exponent; subnormal range (< 2^-6):
-// the E4M3 grid is k * 2^-9, so round s * 512 (exact) to an integer.
-__device__ __forceinline__ uint32_t e4m3_rne_sat(float s, float* value) {
+// E4M3 (OCP E4M3FN) code of a non-negative binary32 value: nearest, ties to
+// the even code, saturating at 448.  Normal range: round the binary32
+// significand to 3 bits with the carry allowed into the exponent; subnormal
+// range (< 2^-6): the E4M3 grid is k * 2^-9, so round s * 512 (exact) to an
+// integer.  Branch free: both candidates are formed and one is selected.
+__device__ __forceinline__ uint32_t e4m3_rne_sat(float s) {
   const uint32_t u = __float_as_uint(s);
-  const uint32_t rn = (u + 0x7FFFFu + ((u >> 20) & 1u)) & 0xFFF00000u;
-  const float sub = __builtin_rintf(s * 512.0f);
-  uint32_t code;
-  float v;
-  if (!(s < 448.0f)) {
-    code = 0x7Eu;
-    v = 448.0f;
-  } else if (s < 0x1p-6f) {
-    code = (uint32_t)sub;
-    v = sub * 0x1p-9f;
-  } else {
-    code = (rn >> 20) - (120u << 3);
-    v = __uint_as_float(rn);
-  }
-  *value = v;
-  return code;
+  const uint32_t normal = ((u + 0x7FFFFu + ((u >> 20) & 1u)) >> 20) - (120u << 3);
+  const uint32_t sub = (uint32_t)__builtin_rintf(s * 512.0f);
+  const uint32_t code = s < 0x1p-6f ? sub : normal;
+  return s < 448.0f ? code : 0x7Eu;
 }
 
 // Exact value of an E4M3 byte (finite codes 0x00..0x7E).

@@ -4,11 +4,14 @@
 //
 // The tensor is a flat run of 16-element blocks (K % 16 == 0, row-major), so
 // both kernels treat it as one-dimensional:
-//   1. amax_partial_kernel  streams x once and writes one partial |x| maximum
-//      (as a 15-bit BF16 magnitude) per workgroup;
-//   2. nvfp4_encode_kernel  folds the partials into alpha, then streams x
-//      again, one block per lane: block amax, E4M3 scale, reciprocal, then
-//      E2M1 encoding of 16 elements by the hardware converter.
+//   1. amax_partial_kernel  streams x once, one contiguous chunk per
+//      workgroup, and writes one partial |x| maximum (as a 15-bit BF16
+//      magnitude) per workgroup;
+//   2. nvfp4_encode_kernel  folds the partials into alpha, tabulates
+//      r(s) = 1 / (s * alpha) for the 126 nonzero finite E4M3 scales in LDS,
+//      then streams x again, one block per lane: block amax, E4M3 scale,
+//      table lookup of r, then E2M1 encoding of 16 elements by the hardware
+//      converter.
 // Both passes are HBM-bound streaming reads (2 B/element each) plus the
 // 0.5625 B/element of codes and scales written by the second.
 //
@@ -33,23 +36,27 @@ constexpr int kEncodeUnroll = 4;   // blocks per lane per iteration
 
 __global__ __launch_bounds__(kQuantThreads) void amax_partial_kernel(
     const uint4* __restrict__ x, int64_t n_vec, uint32_t* __restrict__ partial) {
+  // each workgroup streams one contiguous chunk, 8 x 4 KiB per iteration
+  // (long sequential runs keep HBM pages open)
+  constexpr int kU = 8;
   ushort2_t m = {0, 0};
-  const int64_t stride = (int64_t)gridDim.x * kQuantThreads;
-  int64_t i = (int64_t)blockIdx.x * kQuantThreads + threadIdx.x;
-  // four independent 16-byte loads in flight per lane
-  for (; i + 3 * stride < n_vec; i += 4 * stride) {
-    u32x4_t v[4];
+  const int64_t per = (n_vec + gridDim.x - 1) / gridDim.x;
+  const int64_t lo = (int64_t)blockIdx.x * per;
+  const int64_t hi = min(n_vec, lo + per);
+  int64_t i = lo + threadIdx.x;
+  for (; i + (kU - 1) * kQuantThreads < hi; i += kU * kQuantThreads) {
+    u32x4_t v[kU];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) v[u] = stream_load(&x[i + u * stride]);
+    for (int u = 0; u < kU; ++u) v[u] = stream_load(&x[i + u * kQuantThreads]);
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+    for (int u = 0; u < kU; ++u) {
       m = absmax_pair(m, v[u].x);
       m = absmax_pair(m, v[u].y);
       m = absmax_pair(m, v[u].z);
       m = absmax_pair(m, v[u].w);
     }
   }
-  for (; i < n_vec; i += stride) {
+  for (; i < hi; i += kQuantThreads) {
     const uint4 v = x[i];
     m = absmax_pair(m, v.x);
     m = absmax_pair(m, v.y);
@@ -70,20 +77,19 @@ __global__ __launch_bounds__(kQuantThreads) void amax_partial_kernel(
 
 // Encode one 16-element block held in w[0..7] (two BF16 per word, element
 // 2j in the low half).  Writes the 8 code bytes into c0/c1 and returns the
-// E4M3 scale code.
-__device__ __forceinline__ uint32_t encode_block(const uint32_t (&w)[8], float alpha, float t,
-                                                 bool zero_tensor, uint32_t& c0, uint32_t& c1) {
+// E4M3 scale code.  rtab[c] = 1 / (value(c) * alpha) (0 for c == 0, so a
+// zero-scale block becomes signed zeros: x * 0 keeps the sign).
+__device__ __forceinline__ uint32_t encode_block(const uint32_t (&w)[8], float t,
+                                                 bool zero_tensor, const float* rtab,
+                                                 uint32_t& c0, uint32_t& c1) {
   ushort2_t m = as_us2(w[0] & 0x7FFF7FFFu);
 #pragma unroll
   for (int j = 1; j < 8; ++j) m = absmax_pair(m, w[j]);
   const uint32_t ab = max((uint32_t)m.x, (uint32_t)m.y);
   const float amax_b = __uint_as_float(ab << 16);
-  float s_val;
-  const float s_f = zero_tensor ? 0.0f : amax_b / t;
-  const uint32_t sc = e4m3_rne_sat(s_f, &s_val);
-  const float d = s_val * alpha;
-  // a zero scale encodes the block as signed zeros: x * 0 keeps the sign
-  const float r = sc != 0u ? 1.0f / d : 0.0f;
+  const float q = amax_b / t;
+  const uint32_t sc = e4m3_rne_sat(zero_tensor ? 0.0f : q);
+  const float r = rtab[sc];
   float e[16];
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
@@ -105,6 +111,51 @@ __device__ __forceinline__ uint32_t encode_block(const uint32_t (&w)[8], float a
   return sc;
 }
 
+// One grid-stride iteration: kEncodeUnroll blocks per lane starting at
+// `base`.  kGuard: the iteration reaches past the last block, so loads and
+// stores are guarded (uniform choice per iteration).
+template <bool kGuard>
+__device__ __forceinline__ void encode_iter(const uint4* __restrict__ x, int64_t nblocks,
+                                            int64_t base, float t, bool zero_tensor,
+                                            const float* rtab, uint2* __restrict__ codes,
+                                            uint8_t* __restrict__ scales) {
+  const int lane = threadIdx.x & (kWave - 1);
+  u32x4_t v[kEncodeUnroll][2];
+#pragma unroll
+  for (int u = 0; u < kEncodeUnroll; ++u) {
+    const int64_t blk = base + u * kQuantThreads + threadIdx.x;
+    if (!kGuard || blk < nblocks) {
+      v[u][0] = stream_load(&x[2 * blk]);
+      v[u][1] = stream_load(&x[2 * blk + 1]);
+    } else {
+      v[u][0] = u32x4_t{0, 0, 0, 0};
+      v[u][1] = u32x4_t{0, 0, 0, 0};
+    }
+  }
+#pragma unroll
+  for (int u = 0; u < kEncodeUnroll; ++u) {
+    const int64_t blk = base + u * kQuantThreads + threadIdx.x;
+    const uint32_t w[8] = {v[u][0].x, v[u][0].y, v[u][0].z, v[u][0].w,
+                           v[u][1].x, v[u][1].y, v[u][1].z, v[u][1].w};
+    uint32_t c0, c1;
+    const uint32_t sc = encode_block(w, t, zero_tensor, rtab, c0, c1);
+    if (!kGuard || blk < nblocks) codes[blk] = make_uint2(c0, c1);
+    // gather the scale bytes of each aligned lane quad into its first lane
+    const uint32_t s1 = (uint32_t)__builtin_amdgcn_mov_dpp((int)sc, 0x55, 0xF, 0xF, false);
+    const uint32_t s2 = (uint32_t)__builtin_amdgcn_mov_dpp((int)sc, 0xAA, 0xF, 0xF, false);
+    const uint32_t s3 = (uint32_t)__builtin_amdgcn_mov_dpp((int)sc, 0xFF, 0xF, 0xF, false);
+    if ((lane & 3) == 0) {
+      if (!kGuard || blk + 3 < nblocks) {
+        *reinterpret_cast<uint32_t*>(scales + blk) = sc | (s1 << 8) | (s2 << 16) | (s3 << 24);
+      } else {
+        if (blk < nblocks) scales[blk] = (uint8_t)sc;
+        if (blk + 1 < nblocks) scales[blk + 1] = (uint8_t)s1;
+        if (blk + 2 < nblocks) scales[blk + 2] = (uint8_t)s2;
+      }
+    }
+  }
+}
+
 __global__ __launch_bounds__(kQuantThreads) void nvfp4_encode_kernel(
     const uint4* __restrict__ x, int64_t nblocks, const uint32_t* __restrict__ partial,
     int npartial, uint2* __restrict__ codes, uint8_t* __restrict__ scales,
@@ -112,6 +163,7 @@ __global__ __launch_bounds__(kQuantThreads) void nvfp4_encode_kernel(
   // fold the first pass's partial maxima (every workgroup does it; a few KB
   // from L2)
   __shared__ uint32_t red[kQuantThreads / kWave];
+  __shared__ float rtab[128];
   uint32_t m = 0;
   for (int i = threadIdx.x; i < npartial; i += kQuantThreads) m = max(m, partial[i]);
   m = wave_max_u32(m);
@@ -126,45 +178,22 @@ __global__ __launch_bounds__(kQuantThreads) void nvfp4_encode_kernel(
   const float t = alpha * 6.0f;
   const bool zero_tensor = amax_bits == 0u;
   if (blockIdx.x == 0 && threadIdx.x == 0) *global_scale = alpha;
+  // r(s) = 1 / (s * alpha), both operations rounded exactly as the encoding
+  // prescribes; code 0 (and the unused NaN code) map to 0
+  if (threadIdx.x < 128) {
+    const uint32_t c = threadIdx.x;
+    const float d = e4m3_value(c) * alpha;
+    rtab[c] = (c == 0u || c == 0x7Fu) ? 0.0f : 1.0f / d;
+  }
+  __syncthreads();
 
-  const int lane = threadIdx.x & (kWave - 1);
   const int64_t per_iter = (int64_t)kQuantThreads * kEncodeUnroll;
   for (int64_t base = (int64_t)blockIdx.x * per_iter; base < nblocks;
        base += (int64_t)gridDim.x * per_iter) {
-    u32x4_t v[kEncodeUnroll][2];
-#pragma unroll
-    for (int u = 0; u < kEncodeUnroll; ++u) {
-      const int64_t blk = base + u * kQuantThreads + threadIdx.x;
-      if (blk < nblocks) {
-        v[u][0] = stream_load(&x[2 * blk]);
-        v[u][1] = stream_load(&x[2 * blk + 1]);
-      } else {
-        v[u][0] = u32x4_t{0, 0, 0, 0};
-        v[u][1] = u32x4_t{0, 0, 0, 0};
-      }
-    }
-#pragma unroll
-    for (int u = 0; u < kEncodeUnroll; ++u) {
-      const int64_t blk = base + u * kQuantThreads + threadIdx.x;
-      const uint32_t w[8] = {v[u][0].x, v[u][0].y, v[u][0].z, v[u][0].w,
-                             v[u][1].x, v[u][1].y, v[u][1].z, v[u][1].w};
-      uint32_t c0, c1;
-      const uint32_t sc = encode_block(w, alpha, t, zero_tensor, c0, c1);
-      if (blk < nblocks) codes[blk] = make_uint2(c0, c1);
-      // gather the scale bytes of each aligned lane quad into its first lane
-      const uint32_t s1 = (uint32_t)__builtin_amdgcn_mov_dpp((int)sc, 0x55, 0xF, 0xF, false);
-      const uint32_t s2 = (uint32_t)__builtin_amdgcn_mov_dpp((int)sc, 0xAA, 0xF, 0xF, false);
-      const uint32_t s3 = (uint32_t)__builtin_amdgcn_mov_dpp((int)sc, 0xFF, 0xF, 0xF, false);
-      if ((lane & 3) == 0) {
-        if (blk + 3 < nblocks) {
-          *reinterpret_cast<uint32_t*>(scales + blk) = sc | (s1 << 8) | (s2 << 16) | (s3 << 24);
-        } else {
-          if (blk < nblocks) scales[blk] = (uint8_t)sc;
-          if (blk + 1 < nblocks) scales[blk + 1] = (uint8_t)s1;
-          if (blk + 2 < nblocks) scales[blk + 2] = (uint8_t)s2;
-        }
-      }
-    }
+    if (base + per_iter <= nblocks)
+      encode_iter<false>(x, nblocks, base, t, zero_tensor, rtab, codes, scales);
+    else
+      encode_iter<true>(x, nblocks, base, t, zero_tensor, rtab, codes, scales);
   }
 }
 
