@@ -1,6 +1,6 @@
 // C-ABI entry points of libsolfp4 (declared and documented in solfp4.h).
 // Every argument check happens on the host before the first HIP call.
-#include "../../include/solfp4.h"
+#include "solfp4.h"
 #include "kernels.h"
 
 namespace {
