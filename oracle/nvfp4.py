@@ -46,6 +46,14 @@ R6  GEMM:  out[m, n] = bf16_rne( alpha_A * alpha_B * sum_k (s_A q_A)(s_B q_B)
     + bias[n] ), B stored [N, K] (nn.Linear layout).  The oracle evaluates the
     sum in float64 on exactly dequantized operands.
 
+MXFP4 (the OCP variant named beside NVFP4 in the same paragraph: 32
+elements under one E8M0 scale) follows the OCP MX conversion rule:
+RM1 shared exponent E = floor(log2(amax_b)) - 2 (2 = largest E2M1
+    exponent), scale 2^E stored as the E8M0 byte E + 127 clamped to
+    [0, 254]; an all-zero block stores 0 (2^-127);
+RM2 q = E2M1_RNE_SAT(x / 2^E), sign kept on zero (x / 2^E is exact);
+RM3 no per-tensor scale; GEMM out = bf16_rne(sum_k (X_A q_A)(X_B q_B) + bias).
+
 Every function below cites the passage or reading it follows.  Parity of the
 quantizer is pinned by hand-worked tensors, exhaustive format tables, an
 exact-rational scalar re-implementation and invariants (tests/); the GEMM by
@@ -297,3 +305,59 @@ def nvfp4_linear_ref(x_bits, w_codes, w_scales, w_alpha, bias_bits=None):
 def bf16_output(out_f64) -> np.ndarray:
     """The BF16 rounding of R6's output (nearest, ties to even)."""
     return f64_to_bf16_bits_rne(out_f64)
+
+
+# ---------------------------------------------------------------------------
+# MXFP4 (Preliminaries: OCP MXFP4 = 32 elements under one E8M0 scale; RM1-RM3)
+# ---------------------------------------------------------------------------
+
+def mxfp4_quantize_ref(x_bits: np.ndarray):
+    """MXFP4 quantization of a BF16 matrix ([rows, K], K % 32 == 0).
+
+    Per 32-element block: E = floor(log2(max|x|)) - 2 (reading RM1, exact
+    through frexp), the E8M0 byte E + 127 clamped to [0, 254] (0 for an
+    all-zero block), and codes E2M1_RNE_SAT(x / 2^E) with the sign of x kept
+    (RM2).  Returns ``(codes uint8 [rows, K/2], scales uint8 [rows, K/32])``.
+    """
+    x_bits = np.asarray(x_bits, dtype=np.uint16)
+    if x_bits.ndim != 2:
+        raise ValueError("expects a 2-D [rows, K] array")
+    rows, K = x_bits.shape
+    if K % MXFP4_BLOCK:
+        raise ValueError("K must be a multiple of 32")
+    nb = K // MXFP4_BLOCK
+    x = bf16_bits_to_f32(x_bits).astype(np.float64).reshape(rows, nb, MXFP4_BLOCK)
+    amax = np.abs(x).max(axis=2) if x.size else np.zeros((rows, nb))
+    _, e = np.frexp(np.where(amax > 0, amax, 1.0))       # amax = m 2^e, m in [0.5, 1)
+    floor_log2 = e.astype(np.int64) - 1
+    code = np.clip(floor_log2 - 2 + 127, 0, 254)
+    code = np.where(amax > 0, code, 0).astype(np.int64)
+    X = np.exp2((code - 127).astype(np.float64))
+    y = x / X[:, :, None]                                # exact: power-of-two scaling
+    q = e2m1_encode_rne_sat(y.astype(np.float32), sign_source=x.astype(np.float32))
+    assert np.array_equal(y.astype(np.float32).astype(np.float64), y)
+    return pack_codes(q.reshape(rows, K)), code.astype(np.uint8)
+
+
+def mxfp4_unscaled_ref(codes: np.ndarray, scales: np.ndarray) -> np.ndarray:
+    """X * q per element, float64 (exact)."""
+    q = e2m1_decode(unpack_codes(codes))
+    rows, K = q.shape
+    X = e8m0_decode(scales).reshape(rows, K // MXFP4_BLOCK, 1)
+    return (q.reshape(rows, K // MXFP4_BLOCK, MXFP4_BLOCK) * X).reshape(rows, K)
+
+
+def mxfp4_gemm_ref(a_codes, a_scales, b_codes, b_scales, bias_bits=None) -> np.ndarray:
+    """MXFP4 GEMM (RM3) in float64 before the BF16 output rounding: A [M, K],
+    B [N, K].  Products X_A q_A X_B q_B are exact powers of two times at most
+    4 significant bits; the float64 sum is exact up to summation rounding."""
+    out = mxfp4_unscaled_ref(a_codes, a_scales) @ mxfp4_unscaled_ref(b_codes, b_scales).T
+    if bias_bits is not None:
+        out = out + bf16_bits_to_f32(bias_bits).astype(np.float64)[None, :]
+    return out
+
+
+def mxfp4_linear_ref(x_bits, w_codes, w_scales, bias_bits=None):
+    """MXFP4 linear: quantize the activations, then the MXFP4 GEMM."""
+    xc, xs = mxfp4_quantize_ref(x_bits)
+    return mxfp4_gemm_ref(xc, xs, w_codes, w_scales, bias_bits), (xc, xs)

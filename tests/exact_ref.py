@@ -160,3 +160,47 @@ def gemm_exact(a_codes, a_scales, a_alpha, b_codes, b_scales, b_alpha, bias=None
             row.append(v)
         out.append(row)
     return out
+
+
+def mx_quantize_exact(rows_bits):
+    """MXFP4 by exact rationals: per 32-element block E = floor(log2 amax) - 2
+    (the OCP MX rule), byte clamp(E + 127, 0, 254), 0 for an all-zero block,
+    q = nearest E2M1 of x / 2^E (exact division by a power of two)."""
+    codes, scales = [], []
+    for row in rows_bits:
+        xs = [bf16_bits_to_fraction(b) for b in row]
+        crow, srow = [], []
+        for b0 in range(0, len(row), 32):
+            blk = xs[b0:b0 + 32]
+            amax = max(abs(v) for v in blk)
+            if amax == 0:
+                sc = 0
+            else:
+                sc = min(max(_floor_log2(amax) - 2 + 127, 0), 254)
+            srow.append(sc)
+            X = F(2) ** (sc - 127)
+            for v, bits in zip(blk, row[b0:b0 + 32]):
+                crow.append((((bits >> 15) & 1) << 3) | nearest_code(abs(v / X), E2M1))
+        codes.append(crow)
+        scales.append(srow)
+    return codes, scales
+
+
+def mx_gemm_exact(a_codes, a_scales, b_codes, b_scales, bias=None):
+    """Exact rational sum_k (X q)_A (X q)_B + bias[n]; codes [rows][K], scales
+    [rows][K/32]."""
+    def dec(c, s):
+        q = E2M1[c & 7]
+        return (-q if c & 8 else q) * F(2) ** (s - 127)
+    out = []
+    for m in range(len(a_codes)):
+        row = []
+        for n in range(len(b_codes)):
+            acc = F(0)
+            for k in range(len(a_codes[m])):
+                acc += dec(a_codes[m][k], a_scales[m][k // 32]) * dec(b_codes[n][k], b_scales[n][k // 32])
+            if bias is not None:
+                acc += bias[n]
+            row.append(acc)
+        out.append(row)
+    return out

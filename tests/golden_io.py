@@ -18,7 +18,7 @@ def load(name="nvfp4_hand_worked.txt"):
             if not line or line.startswith("#"):
                 continue
             key, *rest = line.split()
-            if key in ("case", "gemm"):
+            if key in ("case", "gemm", "mxcase", "mxgemm"):
                 cur = {"kind": key, "name": rest[0]}
             elif key == "end":
                 cases[cur["name"]] = cur

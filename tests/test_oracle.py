@@ -254,7 +254,82 @@ def pin_bf16_rounding(seed=13):
         assert have == want or (math.isinf(have) and r >= 2 ** 128), val
 
 
-ALL_PINS = [pin_e2m1_table, pin_e2m1_midpoints, pin_e4m3_table, pin_e4m3_encode,
+def pin_e8m0_table():
+    v = O.e8m0_decode(np.arange(256))
+    assert np.isnan(v[255]) and not np.isnan(v[:255]).any()
+    assert v[127] == 1.0 and v[0] == 2.0 ** -127 and v[254] == 2.0 ** 127 and v[124] == 0.125
+    assert np.all(np.diff(v[:255]) > 0)
+
+
+def pin_golden_mx():
+    cases = golden_io.load()
+    for name, c in cases.items():
+        if c["kind"] == "mxcase":
+            codes, scales = O.mxfp4_quantize_ref(bf16(c["x"])[None, :])
+            assert codes.tobytes() == c["codes"].tobytes(), name
+            assert scales.tobytes() == c["mxscales"].tobytes(), name
+        elif c["kind"] == "mxgemm":
+            out = O.mxfp4_gemm_ref(c["a_codes"][None], c["a_scales"][None],
+                                   c["b_codes"][None], c["b_scales"][None])
+            assert out[0, 0] == c["exact"], name
+            assert int(O.bf16_output(out)[0, 0]) == c["bf16"], name
+
+
+def pin_mx_exact_reference(seed=19):
+    g = np.random.Generator(np.random.PCG64(seed))
+    kinds = ["normal", "dyadic", "wide", "blockscale"]
+    for i in range(16):
+        rows = int(g.integers(1, 4))
+        K = 32 * int(g.integers(1, 3))
+        xb = _tiny_tensor(g, rows, K, kinds[i % len(kinds)])
+        codes, scales = O.mxfp4_quantize_ref(xb)
+        ec, es = X.mx_quantize_exact([[int(v) for v in r] for r in xb])
+        assert np.array_equal(scales, np.array(es, dtype=np.uint8)), i
+        assert np.array_equal(O.unpack_codes(codes), np.array(ec, dtype=np.uint8)), i
+
+
+def pin_mx_gemm_exact(seed=23):
+    g = np.random.Generator(np.random.PCG64(seed))
+    for i in range(8):
+        M, N = int(g.integers(1, 5)), int(g.integers(1, 5))
+        K = 32 * int(g.integers(1, 3))
+        ac = g.integers(0, 256, size=(M, K // 2), dtype=np.uint8)
+        bc = g.integers(0, 256, size=(N, K // 2), dtype=np.uint8)
+        as_ = g.integers(100, 150, size=(M, K // 32), dtype=np.uint8)
+        bs = g.integers(100, 150, size=(N, K // 32), dtype=np.uint8)
+        bias = bf16(np.round(g.standard_normal(N) * 64) / 64) if i % 2 else None
+        out = O.mxfp4_gemm_ref(ac, as_, bc, bs, bias)
+        ex = X.mx_gemm_exact(O.unpack_codes(ac).tolist(), as_.tolist(), O.unpack_codes(bc).tolist(),
+                             bs.tolist(), None if bias is None else [F(float(v)) for v in O.bf16_bits_to_f32(bias)])
+        for m in range(M):
+            for n in range(N):
+                e = float(ex[m][n])
+                assert abs(out[m, n] - e) <= 1e-14 * max(1.0, abs(e)), (i, m, n)
+
+
+def pin_mx_invariants(seed=29):
+    g = np.random.Generator(np.random.PCG64(seed))
+    xb = _tiny_tensor(g, 3, 64, "normal")
+    c0, s0 = O.mxfp4_quantize_ref(xb)
+    x = O.bf16_bits_to_f32(xb)
+    from workloads import f32_to_bf16_bits
+    for k in (-5, 3, 11):
+        ck, sk = O.mxfp4_quantize_ref(f32_to_bf16_bits(x * np.float32(2.0 ** k)))
+        assert np.array_equal(ck, c0) and np.array_equal(sk.astype(int), s0.astype(int) + k)
+    cn, sn = O.mxfp4_quantize_ref(xb ^ np.uint16(0x8000))
+    assert np.array_equal(sn, s0) and np.array_equal(cn, c0 ^ np.uint8(0x88))
+    # every block's largest magnitude decodes within [4, 8) * 2^E and
+    # elements round to within half an E2M1 step of x / 2^E (or saturate)
+    deq = O.mxfp4_unscaled_ref(c0, s0)
+    X_ = np.repeat(O.e8m0_decode(s0), 32, axis=1)
+    y = np.abs(x) / X_
+    assert np.all((y.reshape(3, 2, 32).max(axis=2) >= 4) & (y.reshape(3, 2, 32).max(axis=2) < 8))
+    h = np.where(y < 2, 0.25, np.where(y < 4, 0.5, 1.0)) + np.maximum(y - 6, 0)
+    assert np.all(np.abs(x - deq) <= X_ * h * (1 + 1e-9))
+
+
+ALL_PINS = [pin_e8m0_table, pin_golden_mx, pin_mx_exact_reference, pin_mx_gemm_exact,
+            pin_mx_invariants, pin_e2m1_table, pin_e2m1_midpoints, pin_e4m3_table, pin_e4m3_encode,
             pin_golden_quantize, pin_golden_gemm, pin_exact_reference, pin_gemm_exact,
             pin_gemm_one_hot, pin_invariants, pin_bf16_rounding]
 
@@ -383,9 +458,35 @@ def _mut_e4m3_bias(mp):
     mp.setattr(O, "e4m3_decode", lambda c: orig(c) * 2.0)
 
 
+def _mut_mx_exponent_offset(mp):
+    # shared exponent floor(log2 amax) - 1 instead of - 2
+
+    def variant(x_bits):
+        x_bits = np.asarray(x_bits, dtype=np.uint16)
+        rows, K = x_bits.shape
+        x = O.bf16_bits_to_f32(x_bits).astype(np.float64).reshape(rows, K // 32, 32)
+        amax = np.abs(x).max(axis=2)
+        _, e = np.frexp(np.where(amax > 0, amax, 1.0))
+        code = np.where(amax > 0, np.clip(e - 1 - 1 + 127, 0, 254), 0)
+        y = x / np.exp2(code - 127.0)[:, :, None]
+        q = O.e2m1_encode_rne_sat(y.astype(np.float32), sign_source=x.astype(np.float32))
+        return O.pack_codes(q.reshape(rows, K)), code.astype(np.uint8)
+    mp.setattr(O, "mxfp4_quantize_ref", variant)
+
+
+def _mut_mx_scale_broadcast(mp):
+    # scale broadcast along the wrong axis: element k takes scale k mod (K/32)
+    def variant(codes, scales):
+        q = O.e2m1_decode(O.unpack_codes(codes))
+        rows, K = q.shape
+        return q * np.tile(O.e8m0_decode(scales), (1, 32))[:, :K]
+    mp.setattr(O, "mxfp4_unscaled_ref", variant)
+
+
 @pytest.mark.parametrize("mutation", [_mut_nibble_order, _mut_ties_away, _mut_alpha_divisor,
                                       _mut_division_order, _mut_transposed_b, _mut_dropped_bias,
-                                      _mut_scale_per_32, _mut_e4m3_bias],
+                                      _mut_scale_per_32, _mut_e4m3_bias,
+                                      _mut_mx_exponent_offset, _mut_mx_scale_broadcast],
                          ids=lambda f: f.__name__[5:])
 def test_planted_mistake_is_caught(monkeypatch, mutation):
     assert not _any_pin_fails()
