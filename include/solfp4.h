@@ -56,7 +56,8 @@ extern "C" {
 
 #define SOLFP4_OK 0
 #define SOLFP4_EINVAL (-1)     /* null pointer where data is needed, negative size */
-#define SOLFP4_ESHAPE (-2)     /* K not a multiple of 16, or a size beyond 2^31 elements per dimension */
+#define SOLFP4_ESHAPE (-2)     /* K not a multiple of the block (16 NVFP4, 32 MXFP4), a size of
+                                  2^31 or more, or a GEMM K of 2^24 or more */
 #define SOLFP4_EALIGN (-3)     /* a pointer is not 16-byte aligned */
 #define SOLFP4_EWORKSPACE (-4) /* workspace missing or smaller than the *_workspace_bytes query */
 #define SOLFP4_EHIP (-5)       /* a HIP launch reported an error */
@@ -144,6 +145,82 @@ SOLFP4_API size_t nvfp4_linear_workspace_bytes(int64_t M, int64_t K);
 SOLFP4_API int nvfp4_linear(const uint16_t* x, const uint8_t* w_codes, const uint8_t* w_scales,
                  const float* w_global_scale, const uint16_t* bias, uint16_t* out,
                  void* workspace, size_t workspace_bytes,
+                 int64_t M, int64_t N, int64_t K, void* stream);
+
+/*
+ * MXFP4 variant (Preliminaries: the OCP MX format, E2M1 elements with one
+ * power-of-two E8M0 scale per 32 elements; this is the block format that
+ * CDNA4's scaled FP4 matrix instructions consume natively).
+ *
+ * Encoding produced and consumed here (the OCP MX conversion rule):
+ *   E     = floor(log2(amax_b)) - 2           per 32-element block (2 is the
+ *                                             exponent of 6, the largest E2M1)
+ *   scale = clamp(E + 127, 0, 254)            E8M0 byte; 0 for an all-zero block
+ *   q_i   = E2M1_RNE_SAT(x_i / 2^(scale - 127))   exact division, ties to the
+ *                                             even code, saturating at 6,
+ *                                             sign kept on zero
+ *   decoded value = 2^(scale - 127) * q_i
+ * No per-tensor scale.  Layouts:
+ *   codes  [rows][K/2]  uint8: as for NVFP4 (element 2j in bits 3:0 of byte j)
+ *   scales [rows][K/32] uint8: E8M0, value 2^(byte - 127); 0xFF (NaN) is
+ *          never produced and must not be passed in
+ * K must be a multiple of 32.
+ */
+
+/*
+ * MXFP4 quantization of a BF16 matrix: one pass over x.
+ *
+ *   x       [rows][K] BF16, read only
+ *   codes   [rows][K/2] uint8, written
+ *   scales  [rows][K/32] uint8 (E8M0), written
+ *
+ * Needs no workspace.  rows == 0 or K == 0 is valid and launches nothing.
+ */
+SOLFP4_API int mxfp4_quantize(const uint16_t* x, int64_t rows, int64_t K,
+                   uint8_t* codes, uint8_t* scales, void* stream);
+
+/*
+ * MXFP4 GEMM with BF16 output on the scaled FP4 matrix instructions:
+ *
+ *   out[m][n] = bf16_rne( sum_k (X_A q_A)[m][k] (X_B q_B)[n][k] + bias[n] )
+ *
+ *   a_codes [M][K/2], a_scales [M][K/32]     (A = X, activations)
+ *   b_codes [N][K/2], b_scales [N][K/32]     (B = W, stored [N][K])
+ *   bias    [N] BF16 or NULL
+ *   out     [M][N] BF16, written
+ *
+ * The matrix cores form each product of two decoded elements and sum them
+ * into FP32 accumulators in an unspecified order; the bias is added in FP32
+ * (one rounding), then the sum is rounded to BF16.  Products or sums outside
+ * the FP32 range are unspecified.  M, N or K equal to 0 are valid (K == 0
+ * writes the bias, or zeros).
+ */
+SOLFP4_API int mxfp4_gemm(const uint8_t* a_codes, const uint8_t* a_scales,
+               const uint8_t* b_codes, const uint8_t* b_scales,
+               const uint16_t* bias, uint16_t* out,
+               int64_t M, int64_t N, int64_t K, void* stream);
+
+/* Device workspace, in bytes, that mxfp4_linear needs for [M, K]
+ * activations (their MXFP4 codes and scales).  Host only; 0 for invalid
+ * sizes. */
+SOLFP4_API size_t mxfp4_linear_workspace_bytes(int64_t M, int64_t K);
+
+/*
+ * MXFP4 linear layer: mxfp4_quantize of x into the workspace, then
+ * mxfp4_gemm against the pre-quantized weight, with bias.
+ *
+ *   x        [M][K] BF16
+ *   w_codes  [N][K/2], w_scales [N][K/32] (the weight quantized with
+ *            mxfp4_quantize)
+ *   bias     [N] BF16 or NULL
+ *   out      [M][N] BF16
+ *   workspace >= mxfp4_linear_workspace_bytes(M, K) bytes; on return it
+ *            holds the activation codes at offset 0, then their scales.
+ *
+ * The result is bit-identical to mxfp4_quantize followed by mxfp4_gemm.
+ */
+SOLFP4_API int mxfp4_linear(const uint16_t* x, const uint8_t* w_codes, const uint8_t* w_scales,
+                 const uint16_t* bias, uint16_t* out, void* workspace, size_t workspace_bytes,
                  int64_t M, int64_t N, int64_t K, void* stream);
 
 #ifdef __cplusplus

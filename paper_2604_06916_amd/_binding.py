@@ -37,8 +37,18 @@ lib.nvfp4_linear_workspace_bytes.argtypes = [_i64, _i64]
 lib.nvfp4_linear.restype = ctypes.c_int
 lib.nvfp4_linear.argtypes = [_p, _p, _p, _p, _p, _p, _p, _sz, _i64, _i64, _i64, _p]
 
+lib.mxfp4_quantize.restype = ctypes.c_int
+lib.mxfp4_quantize.argtypes = [_p, _i64, _i64, _p, _p, _p]
+lib.mxfp4_gemm.restype = ctypes.c_int
+lib.mxfp4_gemm.argtypes = [_p, _p, _p, _p, _p, _p, _i64, _i64, _i64, _p]
+lib.mxfp4_linear_workspace_bytes.restype = _sz
+lib.mxfp4_linear_workspace_bytes.argtypes = [_i64, _i64]
+lib.mxfp4_linear.restype = ctypes.c_int
+lib.mxfp4_linear.argtypes = [_p, _p, _p, _p, _p, _p, _sz, _i64, _i64, _i64, _p]
+
 EXPORTED = ["solfp4_strerror", "solfp4_version", "nvfp4_quantize_workspace_bytes",
-            "nvfp4_quantize", "nvfp4_gemm", "nvfp4_linear_workspace_bytes", "nvfp4_linear"]
+            "nvfp4_quantize", "nvfp4_gemm", "nvfp4_linear_workspace_bytes", "nvfp4_linear",
+            "mxfp4_quantize", "mxfp4_gemm", "mxfp4_linear_workspace_bytes", "mxfp4_linear"]
 
 
 class Solfp4Error(RuntimeError):
@@ -132,4 +142,56 @@ def nvfp4_linear(x, w_codes, w_scales, w_global_scale, bias=None, out=None, work
     _check(lib.nvfp4_linear(_ptr(x), _ptr(w_codes), _ptr(w_scales), _ptr(w_global_scale),
                             _ptr(bias), _ptr(out), _ptr(workspace), workspace.numel(),
                             M, N, K, _stream(stream)))
+    return out
+
+
+def mxfp4_linear_workspace_bytes(M: int, K: int) -> int:
+    return lib.mxfp4_linear_workspace_bytes(M, K)
+
+
+def mxfp4_quantize(x, codes=None, scales=None, stream=None):
+    """x: BF16 [rows, K] (K % 32 == 0) -> (codes uint8 [rows, K/2],
+    scales uint8 [rows, K/32], E8M0)."""
+    rows, K = x.shape
+    _need(x, torch.bfloat16, (rows, K), "x")
+    if codes is None:
+        codes = torch.empty((rows, K // 2), dtype=torch.uint8, device=x.device)
+    if scales is None:
+        scales = torch.empty((rows, K // 32), dtype=torch.uint8, device=x.device)
+    _check(lib.mxfp4_quantize(_ptr(x), rows, K, _ptr(codes), _ptr(scales), _stream(stream)))
+    return codes, scales
+
+
+def mxfp4_gemm(a_codes, a_scales, b_codes, b_scales, bias=None, out=None, stream=None):
+    """MXFP4 GEMM: A [M, K] (packed), B [N, K] (packed) -> BF16 [M, N]."""
+    M, N = a_codes.shape[0], b_codes.shape[0]
+    K = a_codes.shape[1] * 2
+    if b_codes.shape[1] * 2 != K:
+        raise ValueError("A and B disagree on K")
+    if out is None:
+        out = torch.empty((M, N), dtype=torch.bfloat16, device=a_codes.device)
+    _need(out, torch.bfloat16, (M, N), "out")
+    if bias is not None:
+        _need(bias, torch.bfloat16, (N,), "bias")
+    _check(lib.mxfp4_gemm(_ptr(a_codes), _ptr(a_scales), _ptr(b_codes), _ptr(b_scales),
+                          _ptr(bias), _ptr(out), M, N, K, _stream(stream)))
+    return out
+
+
+def mxfp4_linear(x, w_codes, w_scales, bias=None, out=None, workspace=None, stream=None):
+    """MXFP4 linear: quantize BF16 x [M, K] on the fly, GEMM with the packed
+    weight [N, K], add bias -> BF16 [M, N]."""
+    M, K = x.shape
+    N = w_codes.shape[0]
+    _need(x, torch.bfloat16, (M, K), "x")
+    if out is None:
+        out = torch.empty((M, N), dtype=torch.bfloat16, device=x.device)
+    _need(out, torch.bfloat16, (M, N), "out")
+    if bias is not None:
+        _need(bias, torch.bfloat16, (N,), "bias")
+    if workspace is None:
+        workspace = torch.empty(mxfp4_linear_workspace_bytes(M, K), dtype=torch.uint8,
+                                device=x.device)
+    _check(lib.mxfp4_linear(_ptr(x), _ptr(w_codes), _ptr(w_scales), _ptr(bias), _ptr(out),
+                            _ptr(workspace), workspace.numel(), M, N, K, _stream(stream)))
     return out

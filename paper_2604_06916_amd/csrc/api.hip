@@ -7,6 +7,8 @@ namespace {
 
 constexpr size_t kAlign = 256;
 constexpr int64_t kMaxDim = (int64_t)1 << 31;
+// a GEMM addresses one 256-row operand tile through a 32-bit byte range
+constexpr int64_t kMaxGemmK = (int64_t)1 << 24;
 
 size_t round_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 
@@ -57,7 +59,7 @@ int gemm_checks(const uint8_t* ac, const uint8_t* as, const float* ags, const ui
   if (rc) return rc;
   rc = check_dims(K, 0);
   if (rc) return rc;
-  if (K % 16) return SOLFP4_ESHAPE;
+  if (K % 16 || K >= kMaxGemmK) return SOLFP4_ESHAPE;
   // the grid is one workgroup per 256 x 256 output tile
   if (((M + 255) / 256) * ((N + 255) / 256) >= kMaxDim) return SOLFP4_ESHAPE;
   const bool any_out = M > 0 && N > 0;
@@ -71,6 +73,48 @@ int gemm_checks(const uint8_t* ac, const uint8_t* as, const float* ags, const ui
   return SOLFP4_OK;
 }
 
+struct MxLinearLayout {
+  size_t codes, scales, total;
+};
+
+MxLinearLayout mx_linear_layout(int64_t M, int64_t K) {
+  MxLinearLayout l;
+  l.codes = 0;
+  l.scales = round_up((size_t)(M * K / 2));
+  l.total = l.scales + round_up((size_t)(M * K / 32));
+  if (l.total == 0) l.total = kAlign;
+  return l;
+}
+
+int mx_quantize_checks(const uint16_t* x, int64_t rows, int64_t K, const uint8_t* codes,
+                       const uint8_t* scales) {
+  int rc = check_dims(rows, K);
+  if (rc) return rc;
+  if (K % 32) return SOLFP4_ESHAPE;
+  if (rows > 0 && K > 0) {
+    if (!x || !codes || !scales) return SOLFP4_EINVAL;
+    if (!aligned16(x) || !aligned16(codes) || !aligned16(scales)) return SOLFP4_EALIGN;
+  }
+  return SOLFP4_OK;
+}
+
+int mx_gemm_checks(const uint8_t* ac, const uint8_t* as, const uint8_t* bc, const uint8_t* bs,
+                   const uint16_t* bias, const uint16_t* out, int64_t M, int64_t N, int64_t K) {
+  int rc = check_dims(M, N);
+  if (rc) return rc;
+  rc = check_dims(K, 0);
+  if (rc) return rc;
+  if (K % 32 || K >= kMaxGemmK) return SOLFP4_ESHAPE;
+  if (((M + 255) / 256) * ((N + 255) / 256) >= kMaxDim) return SOLFP4_ESHAPE;
+  if (M == 0 || N == 0) return SOLFP4_OK;
+  if (!out) return SOLFP4_EINVAL;
+  if (K > 0 && (!ac || !as || !bc || !bs)) return SOLFP4_EINVAL;
+  if (!aligned16(out) || (bias && !aligned16(bias))) return SOLFP4_EALIGN;
+  if (K > 0 && (!aligned16(ac) || !aligned16(as) || !aligned16(bc) || !aligned16(bs)))
+    return SOLFP4_EALIGN;
+  return SOLFP4_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -79,7 +123,9 @@ const char* solfp4_strerror(int status) {
   switch (status) {
     case SOLFP4_OK: return "success";
     case SOLFP4_EINVAL: return "invalid argument (null pointer or negative size)";
-    case SOLFP4_ESHAPE: return "unsupported shape (K must be a multiple of 16; sizes below 2^31)";
+    case SOLFP4_ESHAPE:
+      return "unsupported shape (K must be a multiple of 16, or of 32 for MXFP4; sizes below 2^31; "
+             "GEMM K below 2^24)";
     case SOLFP4_EALIGN: return "pointer not 16-byte aligned";
     case SOLFP4_EWORKSPACE: return "workspace missing or too small";
     case SOLFP4_EHIP: return "HIP kernel launch failed";
@@ -131,7 +177,7 @@ int nvfp4_linear(const uint16_t* x, const uint8_t* w_codes, const uint8_t* w_sca
   if (rc) return rc;
   rc = check_dims(K, 0);
   if (rc) return rc;
-  if (K % 16) return SOLFP4_ESHAPE;
+  if (K % 16 || K >= kMaxGemmK) return SOLFP4_ESHAPE;
   if (!workspace) return SOLFP4_EINVAL;
   if (!aligned16(workspace)) return SOLFP4_EALIGN;
   const LinearLayout l = linear_layout(M, K);
@@ -150,6 +196,56 @@ int nvfp4_linear(const uint16_t* x, const uint8_t* w_codes, const uint8_t* w_sca
   if (e != hipSuccess) return SOLFP4_EHIP;
   if (M == 0 || N == 0) return SOLFP4_OK;
   e = solfp4::launch_gemm(xc, xs, xa, w_codes, w_scales, w_global_scale, bias, out, M, N, K, s);
+  return e == hipSuccess ? SOLFP4_OK : SOLFP4_EHIP;
+}
+
+int mxfp4_quantize(const uint16_t* x, int64_t rows, int64_t K, uint8_t* codes, uint8_t* scales,
+                   void* stream) {
+  const int rc = mx_quantize_checks(x, rows, K, codes, scales);
+  if (rc) return rc;
+  const hipError_t e =
+      solfp4::launch_mx_quantize(x, rows, K, codes, scales, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? SOLFP4_OK : SOLFP4_EHIP;
+}
+
+int mxfp4_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const uint8_t* b_codes,
+               const uint8_t* b_scales, const uint16_t* bias, uint16_t* out, int64_t M, int64_t N,
+               int64_t K, void* stream) {
+  const int rc = mx_gemm_checks(a_codes, a_scales, b_codes, b_scales, bias, out, M, N, K);
+  if (rc) return rc;
+  const hipError_t e = solfp4::launch_mx_gemm(a_codes, a_scales, b_codes, b_scales, bias, out, M,
+                                              N, K, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? SOLFP4_OK : SOLFP4_EHIP;
+}
+
+size_t mxfp4_linear_workspace_bytes(int64_t M, int64_t K) {
+  if (check_dims(M, K) || K % 32) return 0;
+  return mx_linear_layout(M, K).total;
+}
+
+int mxfp4_linear(const uint16_t* x, const uint8_t* w_codes, const uint8_t* w_scales,
+                 const uint16_t* bias, uint16_t* out, void* workspace, size_t workspace_bytes,
+                 int64_t M, int64_t N, int64_t K, void* stream) {
+  int rc = check_dims(M, N);
+  if (rc) return rc;
+  rc = check_dims(K, 0);
+  if (rc) return rc;
+  if (K % 32 || K >= kMaxGemmK) return SOLFP4_ESHAPE;
+  if (!workspace) return SOLFP4_EINVAL;
+  if (!aligned16(workspace)) return SOLFP4_EALIGN;
+  const MxLinearLayout l = mx_linear_layout(M, K);
+  if (workspace_bytes < l.total) return SOLFP4_EWORKSPACE;
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  uint8_t* xc = ws + l.codes;
+  uint8_t* xs = ws + l.scales;
+  rc = mx_quantize_checks(x, M, K, xc, xs);
+  if (rc) return rc;
+  rc = mx_gemm_checks(xc, xs, w_codes, w_scales, bias, out, M, N, K);
+  if (rc) return rc;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e = solfp4::launch_mx_quantize(x, M, K, xc, xs, s);
+  if (e != hipSuccess) return SOLFP4_EHIP;
+  e = solfp4::launch_mx_gemm(xc, xs, w_codes, w_scales, bias, out, M, N, K, s);
   return e == hipSuccess ? SOLFP4_OK : SOLFP4_EHIP;
 }
 

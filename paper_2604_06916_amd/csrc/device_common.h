@@ -11,6 +11,8 @@ typedef _Float16 half8_t __attribute__((ext_vector_type(8)));
 typedef float floatx4_t __attribute__((ext_vector_type(4)));
 typedef float floatx16_t __attribute__((ext_vector_type(16)));
 typedef unsigned short ushort2_t __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kWave = 64;
 
@@ -57,6 +59,39 @@ __device__ __forceinline__ float e4m3_value(uint32_t c) {
 __device__ __forceinline__ uint32_t f32_to_bf16_rne(float f) {
   const uint32_t u = __float_as_uint(f);
   return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+}
+
+// A buffer resource from wave-uniform values: readfirstlane pins the base
+// and size to scalar registers, so loads through it need no per-lane
+// descriptor handling.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t uniform_rsrc(const void* base, int64_t bytes) {
+  const uint64_t p = (uint64_t)base;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)p);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(p >> 32));
+  const int n = __builtin_amdgcn_readfirstlane((int)bytes);
+  return __builtin_amdgcn_make_buffer_rsrc((void*)(((uint64_t)hi << 32) | lo), (short)0, n,
+                                           0x00020000);
+}
+
+// Tile order: consecutive workgroups are dispatched round-robin over the 8
+// XCDs, each with its own L2.  Remap so each XCD gets a contiguous range of
+// tile ids, then walk tiles in groups of kGroupM row-tiles so the tiles an
+// XCD runs together share A rows and B columns.
+constexpr int kXcds = 8;
+constexpr int kGroupM = 8;
+
+__device__ __forceinline__ void tile_coords(int tiles_m, int tiles_n, int& tm, int& tn) {
+  const int total = tiles_m * tiles_n;
+  const int b = blockIdx.x;
+  const int per_xcd = total / kXcds;
+  const int t = b < per_xcd * kXcds ? (b % kXcds) * per_xcd + b / kXcds : b;
+  const int group_size = kGroupM * tiles_n;
+  const int group = t / group_size;
+  const int first_m = group * kGroupM;
+  const int gm = min(tiles_m - first_m, kGroupM);
+  const int in_group = t % group_size;
+  tm = first_m + in_group % gm;
+  tn = in_group / gm;
 }
 
 }  // namespace solfp4

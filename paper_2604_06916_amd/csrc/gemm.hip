@@ -88,9 +88,6 @@ struct HalfRow {
   uint4 c;
 };
 
-typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
-
 // Buffer resources for one operand's 256-row tile: rows past the end of the
 // matrix fall outside num_records and read as zeros (code 0 with scale 0:
 // the value 0), so no load needs a branch.
@@ -98,18 +95,6 @@ struct TileSrc {
   __amdgpu_buffer_rsrc_t codes, scales;
   uint32_t code_off, scale_off;   // this thread's half row / row, in bytes
 };
-
-// A buffer resource from wave-uniform values: readfirstlane pins the base
-// and size to scalar registers, so loads through it need no per-lane
-// descriptor handling.
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t uniform_rsrc(const void* base, int64_t bytes) {
-  const uint64_t p = (uint64_t)base;
-  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)p);
-  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(p >> 32));
-  const int n = __builtin_amdgcn_readfirstlane((int)bytes);
-  return __builtin_amdgcn_make_buffer_rsrc((void*)(((uint64_t)hi << 32) | lo), (short)0, n,
-                                           0x00020000);
-}
 
 __device__ __forceinline__ TileSrc make_tile_src(const uint8_t* codes, const uint8_t* scales,
                                                  int64_t row0, int64_t rows, int64_t K, int t) {
@@ -204,27 +189,6 @@ __device__ __forceinline__ void interleave_step() {
     __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);   // VALU
     if (i >= 6) __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);    // DS write
   }
-}
-
-// Tile order: consecutive workgroups are dispatched round-robin over the 8
-// XCDs, each with its own L2.  Remap so each XCD gets a contiguous range of
-// tile ids, then walk tiles in groups of kGroupM row-tiles so the tiles an
-// XCD runs together share A rows and B columns.
-constexpr int kXcds = 8;
-constexpr int kGroupM = 8;
-
-__device__ __forceinline__ void tile_coords(int tiles_m, int tiles_n, int& tm, int& tn) {
-  const int total = tiles_m * tiles_n;
-  const int b = blockIdx.x;
-  const int per_xcd = total / kXcds;
-  const int t = b < per_xcd * kXcds ? (b % kXcds) * per_xcd + b / kXcds : b;
-  const int group_size = kGroupM * tiles_n;
-  const int group = t / group_size;
-  const int first_m = group * kGroupM;
-  const int gm = min(tiles_m - first_m, kGroupM);
-  const int in_group = t % group_size;
-  tm = first_m + in_group % gm;
-  tn = in_group / gm;
 }
 
 template <bool kFast, bool kVecOut>

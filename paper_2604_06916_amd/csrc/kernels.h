@@ -22,4 +22,13 @@ hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const fl
                        const uint16_t* bias, uint16_t* out, int64_t M, int64_t N, int64_t K,
                        hipStream_t stream);
 
+// MXFP4 (32-element blocks, E8M0 scales): one quantize pass, and the GEMM
+// on the scaled FP4 matrix instructions.
+hipError_t launch_mx_quantize(const uint16_t* x, int64_t rows, int64_t K, uint8_t* codes,
+                              uint8_t* scales, hipStream_t stream);
+
+hipError_t launch_mx_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const uint8_t* b_codes,
+                          const uint8_t* b_scales, const uint16_t* bias, uint16_t* out, int64_t M,
+                          int64_t N, int64_t K, hipStream_t stream);
+
 }  // namespace solfp4

@@ -26,8 +26,6 @@ namespace solfp4 {
 
 constexpr int kQuantThreads = 256;
 
-typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
-
 // 16-byte streaming load (each input byte is read exactly once per pass).
 __device__ __forceinline__ u32x4_t stream_load(const uint4* p) {
   return __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));

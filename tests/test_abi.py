@@ -123,3 +123,66 @@ def test_linear_rejects_bad_arguments():
     assert linear(wg=NULL) == EINVAL
     assert linear(bias=MIS) == EALIGN
     assert linear(out=MIS) == EALIGN
+
+
+def test_gemm_rejects_k_beyond_tile_addressing():
+    assert gemm(K=1 << 24) == ESHAPE
+    assert linear(K=1 << 24) == ESHAPE
+
+
+def test_mx_workspace_query():
+    L = sol.mxfp4_linear_workspace_bytes
+    for M, K in [(1, 32), (128, 1152), (18432, 3072), (26574, 9728)]:
+        assert L(M, K) >= M * K // 2 + M * K // 32
+    assert L(0, 0) > 0
+    assert L(-1, 32) == 0 and L(3, 48) == 0
+
+
+def mxq(x=P, rows=4, K=64, codes=P2, scales=P3):
+    return sol.lib.mxfp4_quantize(x, rows, K, codes, scales, S)
+
+
+def test_mx_quantize_rejects_bad_arguments():
+    assert mxq(rows=-1) == EINVAL
+    assert mxq(K=-32) == EINVAL
+    assert mxq(K=48) == ESHAPE          # a multiple of 16 but not of 32
+    assert mxq(K=1 << 31) == ESHAPE
+    assert mxq(x=NULL) == EINVAL
+    assert mxq(codes=NULL) == EINVAL
+    assert mxq(scales=NULL) == EINVAL
+    assert mxq(x=MIS) == EALIGN
+    assert mxq(scales=MIS) == EALIGN
+    # nothing to encode: valid, and no HIP call is made
+    assert mxq(rows=0, x=NULL, codes=NULL, scales=NULL) == OK
+
+
+def mxgemm(ac=P, as_=P2, bc=P, bs=P2, bias=NULL, out=P3, M=8, N=8, K=64):
+    return sol.lib.mxfp4_gemm(ac, as_, bc, bs, bias, out, M, N, K, S)
+
+
+def test_mx_gemm_rejects_bad_arguments():
+    assert mxgemm(M=-1) == EINVAL
+    assert mxgemm(K=-32) == EINVAL
+    assert mxgemm(K=16) == ESHAPE
+    assert mxgemm(K=1 << 24) == ESHAPE
+    assert mxgemm(M=1 << 31) == ESHAPE
+    assert mxgemm(out=NULL) == EINVAL
+    assert mxgemm(bs=NULL) == EINVAL
+    assert mxgemm(ac=MIS) == EALIGN
+    assert mxgemm(bias=MIS) == EALIGN
+    assert mxgemm(M=0, out=NULL) == OK
+
+
+def mxlinear(x=P, wc=P2, ws_=P3, bias=NULL, out=P2, ws=P3, wsb=1 << 20, M=8, N=8, K=64):
+    return sol.lib.mxfp4_linear(x, wc, ws_, bias, out, ws, wsb, M, N, K, S)
+
+
+def test_mx_linear_rejects_bad_arguments():
+    assert mxlinear(M=-1) == EINVAL
+    assert mxlinear(K=80) == ESHAPE
+    assert mxlinear(ws=NULL) == EINVAL
+    assert mxlinear(ws=MIS) == EALIGN
+    assert mxlinear(wsb=16) == EWORKSPACE
+    assert mxlinear(x=NULL) == EINVAL
+    assert mxlinear(wc=NULL) == EINVAL
+    assert mxlinear(out=MIS) == EALIGN
