@@ -15,16 +15,18 @@
 // accumulators per lane in AGPRs).  K advances 128 elements (64 code bytes
 // per row) per stage.  Codes move global -> registers -> LDS -> registers,
 // through three LDS stage buffers whose rows are padded to 80 bytes (16-byte
-// row reads and writes of 16 consecutive rows are bank-conflict free).  Scale
-// bytes go straight from global memory to the lanes that use them: a lane
-// needs the scales of its own 8 rows only.
+// row reads and writes of 16 consecutive rows are bank-conflict free).
+// Scale bytes are fetched 16 per row (four stages) by one thread per tile
+// row with a single load, parked in LDS, and read by the lanes that use
+// them: a lane needs the scale words of its own 8 rows, which would
+// otherwise cost a 32-cache-line load per row and stage.
 //
 // Pipeline of stage s: the MFMAs read LDS buffer s%3; the codes of stage s+2,
 // fetched during stage s-1, are stored to buffer (s+2)%3; the codes of stage
-// s+3 and the scales of stage s+1 are fetched; the operands of the first
-// K-step of stage s+1 are read from LDS during the last K-step of stage s
-// (that buffer was completed before the previous barrier), so the one barrier
-// per stage does not expose LDS latency.
+// s+3 are fetched; the scales and operands of the first K-step of stage s+1
+// are read from LDS during the last K-step of stage s (that buffer was
+// completed before the previous barrier), so the one barrier per stage does
+// not expose LDS latency.
 #include <type_traits>
 
 #include "device_common.h"
@@ -42,14 +44,20 @@ constexpr int kMxFrags = kMxWaveTile / 32;     // 32 x 32 MFMA tiles per wave ed
 constexpr int kMxSteps = kMxBK / 64;           // MFMA K-steps per stage
 constexpr int kMxBufs = 3;
 constexpr int kMxRounds = kMxTile * kMxRowBytes / 16 / kMxThreads;   // 16-byte loads per operand
+constexpr int kMxGroup = 4;                    // stages per scale group (16 scale bytes per row)
+constexpr int kMxScaleStride = 5;              // words per row in LDS (4 + 1 pad: no bank conflicts)
 
 struct MxSmem {
   uint8_t a[kMxBufs][kMxTile * kMxLdsRow];
   uint8_t b[kMxBufs][kMxTile * kMxLdsRow];
+  uint32_t sc[2][2][kMxTile * kMxScaleStride];   // [group parity][operand][row, stage word]
+  uint16_t bias[kMxTile];
 };
 
 typedef int v4i_t __attribute__((ext_vector_type(4)));
 typedef int v8i_t __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float floatx2_t __attribute__((ext_vector_type(2)));
 
 // An FP4 matrix operand occupies the low 4 registers of the 8-register
 // operand; the rest are ignored for this format and left undefined.
@@ -58,20 +66,35 @@ __device__ __forceinline__ v8i_t fp4_operand(u32x4_t x) {
   return __builtin_shufflevector(y, y, 0, 1, 2, 3, -1, -1, -1, -1);
 }
 
-// Scale bytes of kgroups 4*stage .. 4*stage+3 of one row, as one word.
-// kFast: K % 128 == 0 (4-byte aligned, no stage reaches past K).  Otherwise
-// byte loads, with kgroups past K zeroed (a stray 0xFF byte would be NaN).
+// Two FP32 values to a BF16 pair (round to nearest even), first in the low half.
+__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((floatx2_t{lo, hi}), bf16x2_t));
+}
+
+// The 16 scale bytes of one row for stages 4 grp .. 4 grp + 3 (byte 4 j + i
+// is kgroup i of stage 4 grp + j).  kFast: K % 128 == 0, so the bytes of every
+// stage that is computed lie inside the row (a group reaching past K only
+// covers stages that are never computed).  Otherwise byte loads, with kgroups
+// past K zeroed (a stray 0xFF byte would be NaN).
 template <bool kFast>
-__device__ __forceinline__ uint32_t load_scale_word(__amdgpu_buffer_rsrc_t src, uint32_t off,
-                                                    int64_t kgroups, int stage) {
-  if (kFast) return __builtin_amdgcn_raw_buffer_load_b32(src, off, 0, 0);
-  uint32_t w = 0;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const uint32_t b = __builtin_amdgcn_raw_buffer_load_b8(src, off + i, 0, 0);
-    w |= ((int64_t)stage * 4 + i < kgroups ? b : 0u) << (8 * i);
+__device__ __forceinline__ u32x4_t load_scale_group(__amdgpu_buffer_rsrc_t src, uint32_t off,
+                                                    int64_t kgroups, int grp) {
+  if (kFast && kgroups % 16 == 0) return __builtin_amdgcn_raw_buffer_load_b128(src, off, 0, 0);
+  if (kFast) {
+    u32x4_t v;
+    v.x = __builtin_amdgcn_raw_buffer_load_b32(src, off, 0, 0);
+    v.y = __builtin_amdgcn_raw_buffer_load_b32(src, off + 4, 0, 0);
+    v.z = __builtin_amdgcn_raw_buffer_load_b32(src, off + 8, 0, 0);
+    v.w = __builtin_amdgcn_raw_buffer_load_b32(src, off + 12, 0, 0);
+    return v;
   }
-  return w;
+  uint32_t w[4] = {0, 0, 0, 0};
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const uint32_t b = __builtin_amdgcn_raw_buffer_load_b8(src, off + i, 0, 0);
+    w[i / 4] |= ((int64_t)grp * 16 + i < kgroups ? b : 0u) << (8 * (i % 4));
+  }
+  return u32x4_t{w[0], w[1], w[2], w[3]};
 }
 
 template <bool kFast, bool kVecOut>
@@ -113,15 +136,17 @@ __global__ __launch_bounds__(kMxThreads, 1) void mxfp4_gemm_kernel(
   const uint32_t code_off = (uint32_t)(srow * row_bytes + 16 * piece);
   const uint32_t round_stride = (uint32_t)(64 * row_bytes);
   const int st_off = (srow * kMxLdsRow) + 16 * piece;
-  // MFMA operand rows of this lane
-  uint32_t sa_off[kMxFrags], sb_off[kMxFrags];
-#pragma unroll
-  for (int f = 0; f < kMxFrags; ++f) {
-    sa_off[f] = (uint32_t)((wm * kMxWaveTile + f * 32 + li) * kgroups);
-    sb_off[f] = (uint32_t)((wn * kMxWaveTile + f * 32 + li) * kgroups);
-  }
+  // scale staging: thread t moves the scale group of tile row t of A and B
+  const uint32_t sg_off = (uint32_t)(t * kgroups);
+  // MFMA operand rows of this lane (LDS offsets)
   const int rd_a = (wm * kMxWaveTile + li) * kMxLdsRow + 16 * g;
   const int rd_b = (wn * kMxWaveTile + li) * kMxLdsRow + 16 * g;
+  const int rs_a = (wm * kMxWaveTile + li) * kMxScaleStride;
+  const int rs_b = (wn * kMxWaveTile + li) * kMxScaleStride;
+
+  // the tile's bias (+0 without one: the accumulators start at +0 and never
+  // hold -0, so adding +0 changes no result)
+  smem.bias[t] = bias && n0 + t < N ? bias[n0 + t] : (uint16_t)0;
 
   floatx16_t acc[kMxFrags][kMxFrags];
 #pragma unroll
@@ -130,6 +155,7 @@ __global__ __launch_bounds__(kMxThreads, 1) void mxfp4_gemm_kernel(
     for (int j = 0; j < kMxFrags; ++j) acc[i][j] = floatx16_t{};
 
   u32x4_t stg[2][2][kMxRounds];          // [set][operand][round]
+  u32x4_t gsa, gsb;                      // scale group in flight
   uint32_t sca[2][kMxFrags], scb[2][kMxFrags];
   u32x4_t fa[2][kMxFrags], fb[2][kMxFrags];
 
@@ -151,11 +177,23 @@ __global__ __launch_bounds__(kMxThreads, 1) void mxfp4_gemm_kernel(
       *reinterpret_cast<u32x4_t*>(&smem.b[buf][st_off + 64 * j * kMxLdsRow]) = src[1][j];
     }
   };
-  auto load_scales = [&](uint32_t (&da)[kMxFrags], uint32_t (&db)[kMxFrags], int stage) {
+  auto load_group = [&](int grp) {
+    gsa = load_scale_group<kFast>(rsa, sg_off + 16 * grp, kgroups, grp);
+    gsb = load_scale_group<kFast>(rsb, sg_off + 16 * grp, kgroups, grp);
+  };
+  auto store_group = [&](int set) {
+    uint32_t* da = &smem.sc[set][0][t * kMxScaleStride];
+    uint32_t* db = &smem.sc[set][1][t * kMxScaleStride];
+    da[0] = gsa.x; da[1] = gsa.y; da[2] = gsa.z; da[3] = gsa.w;
+    db[0] = gsb.x; db[1] = gsb.y; db[2] = gsb.z; db[3] = gsb.w;
+  };
+  // this lane's scale words of `stage` (its 4 A rows and 4 B rows)
+  auto read_scales = [&](uint32_t (&da)[kMxFrags], uint32_t (&db)[kMxFrags], int stage) {
+    const int set = (stage / kMxGroup) & 1, w = stage % kMxGroup;
 #pragma unroll
     for (int f = 0; f < kMxFrags; ++f) {
-      da[f] = load_scale_word<kFast>(rsa, sa_off[f] + 4 * stage, kgroups, stage);
-      db[f] = load_scale_word<kFast>(rsb, sb_off[f] + 4 * stage, kgroups, stage);
+      da[f] = smem.sc[set][0][rs_a + f * 32 * kMxScaleStride + w];
+      db[f] = smem.sc[set][1][rs_b + f * 32 * kMxScaleStride + w];
     }
   };
   auto read_frags = [&](u32x4_t (&da)[kMxFrags], u32x4_t (&db)[kMxFrags], int buf, int st) {
@@ -182,86 +220,136 @@ __global__ __launch_bounds__(kMxThreads, 1) void mxfp4_gemm_kernel(
 
   const int nstages = (int)((K + kMxBK - 1) / kMxBK);
   // prologue: stages 0 and 1 into LDS buffers 0 and 1, stage 2 in flight,
-  // scales of stage 0, operands of the first K-step
+  // scale group 0 in LDS, the scales and operands of the first K-step
+  load_group(0);
   load_codes(stg[0], 0);
   load_codes(stg[1], 1);
-  load_scales(sca[0], scb[0], 0);
+  store_group(0);
   store_codes(stg[0], 0);
   store_codes(stg[1], 1);
   load_codes(stg[0], 2);
   __syncthreads();
+  read_scales(sca[0], scb[0], 0);
   read_frags(fa[0], fb[0], 0, 0);
 
   using S0 = std::integral_constant<int, 0>;
   using S1 = std::integral_constant<int, 1>;
+  // Stage s with P = s % 4.  At P == 0 the scale group after the current one
+  // is fetched into registers, at P == 2 it is stored into the LDS set of
+  // its parity (last read two stages earlier); it is first read at P == 3,
+  // for the next stage.
   auto run_stage = [&](auto phase, int s, int cur, int nxt, int wbuf) {
     constexpr int P = decltype(phase)::value;
+    constexpr int C = P & 1;               // code and scale-word register set of stage s
     uint32_t ssa[kMxFrags], ssb[kMxFrags];
 #pragma unroll
     for (int f = 0; f < kMxFrags; ++f) {
-      ssa[f] = sca[P][f] >> (8 * g);
-      ssb[f] = scb[P][f] >> (8 * g);
+      ssa[f] = sca[C][f] >> (8 * g);
+      ssb[f] = scb[C][f] >> (8 * g);
     }
+    __builtin_amdgcn_sched_barrier(0);
+    // K-step 0: fetch scales and codes ahead, read the operands of K-step 1,
+    // store the codes of stage s+2
+    if (P == 0) load_group(s / kMxGroup + 1);
+    load_codes(stg[C ^ 1], s + 3);
     read_frags(fa[1], fb[1], cur, 1);
-    load_codes(stg[P ^ 1], s + 3);
-    load_scales(sca[P ^ 1], scb[P ^ 1], s + 1);
-    __builtin_amdgcn_sched_barrier(0);
     mfma_step(S0{}, fa[0], fb[0], ssa, ssb);
-    store_codes(stg[P], wbuf);
+    store_codes(stg[C], wbuf);
+    if (P == 2) store_group((s / kMxGroup + 1) & 1);
+#pragma unroll
+    for (int i = 0; i < kMxFrags * kMxFrags; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                 // MFMA
+      if (i < 8) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);      // DS read
+      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);                 // VMEM read
+      if (i < 8) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+      if (i >= 8) __builtin_amdgcn_sched_group_barrier(0x200, P == 2 ? 2 : 1, 0);   // DS write
+    }
     __builtin_amdgcn_sched_barrier(0);
+    // K-step 1, with the scales and operands of the next stage's first K-step
+    read_scales(sca[C ^ 1], scb[C ^ 1], s + 1);
     read_frags(fa[0], fb[0], nxt, 0);
     mfma_step(S1{}, fa[1], fb[1], ssa, ssb);
+#pragma unroll
+    for (int i = 0; i < kMxFrags * kMxFrags; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
     __syncthreads();
   };
 
+  using P0 = std::integral_constant<int, 0>;
+  using P1 = std::integral_constant<int, 1>;
+  using P2 = std::integral_constant<int, 2>;
+  using P3 = std::integral_constant<int, 3>;
+  // LDS buffers rotate mod 3: stage s + j uses buffer (cur + j) % 3
   int s = 0, cur = 0;
-  for (; s + 2 <= nstages; s += 2) {
-    const int c1 = cur == 2 ? 0 : cur + 1;
-    const int c2 = c1 == 2 ? 0 : c1 + 1;
-    run_stage(S0{}, s, cur, c1, c2);
-    run_stage(S1{}, s + 1, c1, c2, cur);
-    cur = c2;
+  auto next3 = [](int b) { return b == 2 ? 0 : b + 1; };
+  for (; s + 4 <= nstages; s += 4) {
+    const int c1 = next3(cur), c2 = next3(c1);
+    run_stage(P0{}, s, cur, c1, c2);
+    run_stage(P1{}, s + 1, c1, c2, cur);
+    run_stage(P2{}, s + 2, c2, cur, c1);
+    run_stage(P3{}, s + 3, cur, c1, c2);
+    cur = c1;   // (cur + 4) % 3
   }
-  if (s < nstages) {
-    const int c1 = cur == 2 ? 0 : cur + 1;
-    const int c2 = c1 == 2 ? 0 : c1 + 1;
-    run_stage(S0{}, s, cur, c1, c2);
+  {
+    const int rest = nstages - s;
+    const int c1 = next3(cur), c2 = next3(c1);
+    if (rest > 0) run_stage(P0{}, s, cur, c1, c2);
+    if (rest > 1) run_stage(P1{}, s + 1, c1, c2, cur);
+    if (rest > 2) run_stage(P2{}, s + 2, c2, cur, c1);
   }
 
-  // epilogue: out = bf16(fp32(acc + bias))
+  // epilogue: out = bf16(fp32(acc + bias)).  Lane (li, g) holds, per MFMA
+  // tile, row m = li and the column runs 8k + 4g .. 8k + 4g + 3 (k = 0..3);
+  // swapping halves with the lane 32 apart gives each lane two runs of 8
+  // consecutive columns (16-byte stores).  Stores go through a buffer
+  // resource covering the tile's valid rows, so rows past M are dropped by
+  // the hardware range check; columns past N get an offset beyond the range.
+  const __amdgpu_buffer_rsrc_t ro = uniform_rsrc(out + m0 * N, valid_a * N * 2);
+  constexpr uint32_t kDrop = 0x80000000u;   // beyond any output range (N < 2^22)
 #pragma unroll
   for (int fm = 0; fm < kMxFrags; ++fm) {
-    const int64_t m = m0 + wm * kMxWaveTile + fm * 32 + li;
-    if (m >= M) continue;
-    uint16_t* orow = out + m * N;
+    const uint32_t mrow = (uint32_t)((wm * kMxWaveTile + fm * 32 + li) * N);
 #pragma unroll
     for (int fn = 0; fn < kMxFrags; ++fn) {
+      const int nb = wn * kMxWaveTile + fn * 32;
+      float v[16];
+#pragma unroll
+      for (int q = 0; q < 16; ++q) v[q] = acc[fn][fm][q];
 #pragma unroll
       for (int k = 0; k < 4; ++k) {
-        const int64_t n = n0 + wn * kMxWaveTile + fn * 32 + 8 * k + 4 * g;
-        float v[4];
+        const uint2 b2 = *reinterpret_cast<const uint2*>(&smem.bias[nb + 8 * k + 4 * g]);
+        v[4 * k + 0] += __uint_as_float(b2.x << 16);
+        v[4 * k + 1] += __uint_as_float(b2.x & 0xFFFF0000u);
+        v[4 * k + 2] += __uint_as_float(b2.y << 16);
+        v[4 * k + 3] += __uint_as_float(b2.y & 0xFFFF0000u);
+      }
+      uint32_t p[4][2];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) v[q] = acc[fn][fm][4 * k + q];
-        if (kVecOut && n + 3 < N) {
-          float bv[4] = {0.f, 0.f, 0.f, 0.f};
-          if (bias) {
-            const uint2 b2 = *reinterpret_cast<const uint2*>(bias + n);
-            bv[0] = __uint_as_float(b2.x << 16);
-            bv[1] = __uint_as_float(b2.x & 0xFFFF0000u);
-            bv[2] = __uint_as_float(b2.y << 16);
-            bv[3] = __uint_as_float(b2.y & 0xFFFF0000u);
-          }
-          uint32_t o[4];
+      for (int k = 0; k < 4; ++k) {
+        p[k][0] = pack_bf16(v[4 * k], v[4 * k + 1]);
+        p[k][1] = pack_bf16(v[4 * k + 2], v[4 * k + 3]);
+      }
 #pragma unroll
-          for (int q = 0; q < 4; ++q) o[q] = f32_to_bf16_rne(v[q] + bv[q]);
-          *reinterpret_cast<uint2*>(orow + n) = make_uint2(o[0] | (o[1] << 16), o[2] | (o[3] << 16));
+      for (int h = 0; h < 2; ++h) {
+        uint32_t r[4];   // 8 columns starting at nb + 16 h + 8 g
+#pragma unroll
+        for (int d = 0; d < 2; ++d) {
+          const auto x = __builtin_amdgcn_permlane32_swap(p[2 * h][d], p[2 * h + 1][d], false, false);
+          r[d] = x[0];
+          r[2 + d] = x[1];
+        }
+        const int64_t n = n0 + nb + 16 * h + 8 * g;
+        if (kVecOut) {
+          const uint32_t off = n < N ? (mrow + (uint32_t)n) * 2 : kDrop;
+          __builtin_amdgcn_raw_buffer_store_b128(u32x4_t{r[0], r[1], r[2], r[3]}, ro, off, 0, 0);
         } else {
 #pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            if (n + q < N) {
-              const float bq = bias ? __uint_as_float((uint32_t)bias[n + q] << 16) : 0.f;
-              orow[n + q] = (uint16_t)f32_to_bf16_rne(v[q] + bq);
-            }
+          for (int q = 0; q < 8; ++q) {
+            const uint32_t off = n + q < N ? (mrow + (uint32_t)(n + q)) * 2 : kDrop;
+            __builtin_amdgcn_raw_buffer_store_b16((uint16_t)(r[q / 2] >> (16 * (q & 1))), ro, off, 0, 0);
           }
         }
       }
@@ -276,7 +364,7 @@ hipError_t launch_mx_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const
   const int64_t tiles = ((M + kMxTile - 1) / kMxTile) * ((N + kMxTile - 1) / kMxTile);
   const dim3 grid((unsigned)tiles), block(kMxThreads);
   const bool fast = K % kMxBK == 0;
-  const bool vec = N % 4 == 0;
+  const bool vec = N % 8 == 0;
   if (fast && vec)
     hipLaunchKernelGGL((mxfp4_gemm_kernel<true, true>), grid, block, 0, stream, a_codes, a_scales,
                        b_codes, b_scales, bias, out, M, N, K);

@@ -166,6 +166,8 @@ def test_mx_gemm_rejects_bad_arguments():
     assert mxgemm(K=16) == ESHAPE
     assert mxgemm(K=1 << 24) == ESHAPE
     assert mxgemm(M=1 << 31) == ESHAPE
+    assert mxgemm(N=1 << 22) == ESHAPE
+    assert mxlinear(N=1 << 22) == ESHAPE
     assert mxgemm(out=NULL) == EINVAL
     assert mxgemm(bs=NULL) == EINVAL
     assert mxgemm(ac=MIS) == EALIGN
