@@ -13,20 +13,25 @@
 // Tiling: a 256 x 256 output tile per workgroup of 4 waves (one per SIMD),
 // each wave owning 128 x 128 (4 x 4 MFMA tiles of 32 x 32, 256 FP32
 // accumulators per lane in AGPRs).  K advances 128 elements (64 code bytes
-// per row) per stage.  Codes move global -> registers -> LDS -> registers,
-// through three LDS stage buffers whose rows are padded to 80 bytes (16-byte
-// row reads and writes of 16 consecutive rows are bank-conflict free).
-// Scale bytes are fetched 16 per row (four stages) by one thread per tile
-// row with a single load, parked in LDS, and read by the lanes that use
-// them: a lane needs the scale words of its own 8 rows, which would
-// otherwise cost a 32-cache-line load per row and stage.
+// per row) per stage.  Codes go from global memory straight into LDS by
+// buffer loads with the LDS-destination bit (no register staging), into four
+// stage buffers: the loads for stage s+3 are issued while stage s computes,
+// so about two stages of time cover their latency.  A DMA instruction puts
+// lane l's 16 bytes at slot l of a 1 KB block, so each block holds 16 rows
+// as [piece][row] x 16 bytes: the same 16 lanes that read one 16-byte piece
+// of 16 consecutive rows for an MFMA operand read 256 contiguous bytes (no
+// bank conflicts, no padding).  Scale bytes are fetched 16 per row (four
+// stages) by one thread per tile row with a single load, parked in LDS, and
+// read by the lanes that use them: a lane needs the scale words of its own
+// 8 rows, which would otherwise cost a 32-cache-line load per row and stage.
 //
-// Pipeline of stage s: the MFMAs read LDS buffer s%3; the codes of stage s+2,
-// fetched during stage s-1, are stored to buffer (s+2)%3; the codes of stage
-// s+3 are fetched; the scales and operands of the first K-step of stage s+1
-// are read from LDS during the last K-step of stage s (that buffer was
-// completed before the previous barrier), so the one barrier per stage does
-// not expose LDS latency.
+// Pipeline of stage s (buffer s % 4): the DMA of stage s+3 goes to the buffer
+// read in stage s-1; the scales and operands of the first K-step of stage
+// s+1 are read during the last K-step of stage s; the barrier that ends
+// stage s first waits for this wave's DMA of stage s+2 (the barrier is a
+// plain s_barrier with explicit counter waits: a release fence would wait
+// for every DMA in flight).
+
 #include <type_traits>
 
 #include "device_common.h"
@@ -37,27 +42,20 @@ namespace solfp4 {
 constexpr int kMxTile = 256;                   // output tile edge (M and N)
 constexpr int kMxBK = 128;                     // K elements per stage
 constexpr int kMxRowBytes = kMxBK / 2;         // code bytes per row per stage
-constexpr int kMxLdsRow = kMxRowBytes + 16;    // padded LDS row
 constexpr int kMxThreads = 256;
 constexpr int kMxWaveTile = 128;
 constexpr int kMxFrags = kMxWaveTile / 32;     // 32 x 32 MFMA tiles per wave edge
-constexpr int kMxSteps = kMxBK / 64;           // MFMA K-steps per stage
-constexpr int kMxBufs = 3;
-constexpr int kMxRounds = kMxTile * kMxRowBytes / 16 / kMxThreads;   // 16-byte loads per operand
+constexpr int kMxBufs = 4;                     // LDS stage buffers (loads run 3 stages ahead)
+constexpr int kMxGroups = kMxTile / 16;        // 16-row groups per operand tile
+constexpr int kMxStageBytes = kMxTile * kMxRowBytes;   // one operand, one stage
 constexpr int kMxGroup = 4;                    // stages per scale group (16 scale bytes per row)
 constexpr int kMxScaleStride = 5;              // words per row in LDS (4 + 1 pad: no bank conflicts)
-
-struct MxSmem {
-  uint8_t a[kMxBufs][kMxTile * kMxLdsRow];
-  uint8_t b[kMxBufs][kMxTile * kMxLdsRow];
-  uint32_t sc[2][2][kMxTile * kMxScaleStride];   // [group parity][operand][row, stage word]
-  uint16_t bias[kMxTile];
-};
 
 typedef int v4i_t __attribute__((ext_vector_type(4)));
 typedef int v8i_t __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef float floatx2_t __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
 // An FP4 matrix operand occupies the low 4 registers of the 8-register
 // operand; the rest are ignored for this format and left undefined.
@@ -71,15 +69,22 @@ __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector((floatx2_t{lo, hi}), bf16x2_t));
 }
 
+// s_waitcnt with vmcnt(V) and lgkmcnt(L) (expcnt not waited on).
+template <int V, int L>
+__device__ __forceinline__ void wait_counts() {
+  static_assert(V >= 0 && V < 64 && L >= 0 && L < 16, "counter range");
+  __builtin_amdgcn_s_waitcnt((V & 15) | ((V >> 4) << 14) | (7 << 4) | (L << 8));
+}
+
 // The 16 scale bytes of one row for stages 4 grp .. 4 grp + 3 (byte 4 j + i
 // is kgroup i of stage 4 grp + j).  kFast: K % 128 == 0, so the bytes of every
 // stage that is computed lie inside the row (a group reaching past K only
 // covers stages that are never computed).  Otherwise byte loads, with kgroups
 // past K zeroed (a stray 0xFF byte would be NaN).
-template <bool kFast>
+template <bool kFast, bool kK512>
 __device__ __forceinline__ u32x4_t load_scale_group(__amdgpu_buffer_rsrc_t src, uint32_t off,
                                                     int64_t kgroups, int grp) {
-  if (kFast && kgroups % 16 == 0) return __builtin_amdgcn_raw_buffer_load_b128(src, off, 0, 0);
+  if (kFast && kK512) return __builtin_amdgcn_raw_buffer_load_b128(src, off, 0, 0);
   if (kFast) {
     u32x4_t v;
     v.x = __builtin_amdgcn_raw_buffer_load_b32(src, off, 0, 0);
@@ -97,13 +102,25 @@ __device__ __forceinline__ u32x4_t load_scale_group(__amdgpu_buffer_rsrc_t src, 
   return u32x4_t{w[0], w[1], w[2], w[3]};
 }
 
-template <bool kFast, bool kVecOut>
+// vector-memory instructions one scale-group fetch issues (both operands)
+constexpr int scale_group_loads(bool fast, bool k512) { return fast ? (k512 ? 2 : 8) : 32; }
+
+template <bool kFast, bool kVecOut, bool kK512>
 __global__ __launch_bounds__(kMxThreads, 1) void mxfp4_gemm_kernel(
     const uint8_t* __restrict__ a_codes, const uint8_t* __restrict__ a_scales,
     const uint8_t* __restrict__ b_codes, const uint8_t* __restrict__ b_scales,
     const uint16_t* __restrict__ bias, uint16_t* __restrict__ out, int64_t M, int64_t N,
     int64_t K) {
-  __shared__ MxSmem smem;
+  // one array per stage buffer and operand, so the compiler can tell the
+  // buffer being filled by DMA from the one being read
+  __shared__ __attribute__((aligned(1024))) uint8_t la0[kMxStageBytes], la1[kMxStageBytes],
+      la2[kMxStageBytes], la3[kMxStageBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t lb0[kMxStageBytes], lb1[kMxStageBytes],
+      lb2[kMxStageBytes], lb3[kMxStageBytes];
+  __shared__ uint32_t lsc[2][2][kMxTile * kMxScaleStride];   // [group parity][operand][row, word]
+  __shared__ uint16_t lbias[kMxTile];
+  uint8_t* const abuf[kMxBufs] = {la0, la1, la2, la3};
+  uint8_t* const bbuf[kMxBufs] = {lb0, lb1, lb2, lb3};
 
   const int tiles_m = (int)((M + kMxTile - 1) / kMxTile);
   const int tiles_n = (int)((N + kMxTile - 1) / kMxTile);
@@ -129,24 +146,27 @@ __global__ __launch_bounds__(kMxThreads, 1) void mxfp4_gemm_kernel(
   const __amdgpu_buffer_rsrc_t rsa = uniform_rsrc(a_scales + m0 * kgroups, valid_a * kgroups);
   const __amdgpu_buffer_rsrc_t rsb = uniform_rsrc(b_scales + n0 * kgroups, valid_b * kgroups);
 
-  // code staging: in round j this thread moves 16 bytes (piece `piece`) of
-  // tile row 64 j + srow; a wave covers 16 whole rows per round
-  const int srow = 16 * wave + (lane & 15);
+  // Code DMA: wave w fills 16-row groups 4 w .. 4 w + 3 of each operand; in
+  // one instruction lane l moves 16 bytes (piece l / 16) of row l % 16 of the
+  // group, and the hardware stores lane l's bytes at slot l of the group's
+  // 1 KB, so a group holds [piece][row] x 16 bytes.
   const int piece = lane >> 4;
-  const uint32_t code_off = (uint32_t)(srow * row_bytes + 16 * piece);
-  const uint32_t round_stride = (uint32_t)(64 * row_bytes);
-  const int st_off = (srow * kMxLdsRow) + 16 * piece;
+  const uint32_t dma_off = (uint32_t)((64 * wave + (lane & 15)) * row_bytes + 16 * piece);
+  const uint32_t group_stride = (uint32_t)(16 * row_bytes);
+  constexpr uint32_t kDrop = 0x80000000u;   // beyond any buffer range: loads read zero,
+                                            // stores are dropped (N < 2^22, K < 2^24)
   // scale staging: thread t moves the scale group of tile row t of A and B
   const uint32_t sg_off = (uint32_t)(t * kgroups);
-  // MFMA operand rows of this lane (LDS offsets)
-  const int rd_a = (wm * kMxWaveTile + li) * kMxLdsRow + 16 * g;
-  const int rd_b = (wn * kMxWaveTile + li) * kMxLdsRow + 16 * g;
+  // MFMA operand slots of this lane: row r of the tile lives in group r / 16
+  // at slot piece * 16 + r % 16; lane (li, g) of K-step st reads piece 2 st + g
+  const int rd_a = ((wm * kMxWaveTile + li) >> 4) * 1024 + ((li & 15) << 4) + 256 * g;
+  const int rd_b = ((wn * kMxWaveTile + li) >> 4) * 1024 + ((li & 15) << 4) + 256 * g;
   const int rs_a = (wm * kMxWaveTile + li) * kMxScaleStride;
   const int rs_b = (wn * kMxWaveTile + li) * kMxScaleStride;
 
   // the tile's bias (+0 without one: the accumulators start at +0 and never
   // hold -0, so adding +0 changes no result)
-  smem.bias[t] = bias && n0 + t < N ? bias[n0 + t] : (uint16_t)0;
+  lbias[t] = bias && n0 + t < N ? bias[n0 + t] : (uint16_t)0;
 
   floatx16_t acc[kMxFrags][kMxFrags];
 #pragma unroll
@@ -154,36 +174,30 @@ __global__ __launch_bounds__(kMxThreads, 1) void mxfp4_gemm_kernel(
 #pragma unroll
     for (int j = 0; j < kMxFrags; ++j) acc[i][j] = floatx16_t{};
 
-  u32x4_t stg[2][2][kMxRounds];          // [set][operand][round]
   u32x4_t gsa, gsb;                      // scale group in flight
   uint32_t sca[2][kMxFrags], scb[2][kMxFrags];
   u32x4_t fa[2][kMxFrags], fb[2][kMxFrags];
 
-  auto load_codes = [&](u32x4_t (&dst)[2][kMxRounds], int stage) {
+  // 8 DMA instructions per wave: stage `stage` into buffer `buf`
+  auto dma_stage = [&](int buf, int stage) {
     const bool ok = kFast || (int64_t)stage * kMxBK + 32 * piece < K;
+    const uint32_t base = dma_off + (uint32_t)stage * kMxRowBytes;
 #pragma unroll
-    for (int j = 0; j < kMxRounds; ++j) {
-      const uint32_t off = code_off + j * round_stride + (uint32_t)stage * kMxRowBytes;
-      const u32x4_t va = __builtin_amdgcn_raw_buffer_load_b128(rca, off, 0, 0);
-      const u32x4_t vb = __builtin_amdgcn_raw_buffer_load_b128(rcb, off, 0, 0);
-      dst[0][j] = ok ? va : u32x4_t{0, 0, 0, 0};
-      dst[1][j] = ok ? vb : u32x4_t{0, 0, 0, 0};
-    }
-  };
-  auto store_codes = [&](const u32x4_t (&src)[2][kMxRounds], int buf) {
-#pragma unroll
-    for (int j = 0; j < kMxRounds; ++j) {
-      *reinterpret_cast<u32x4_t*>(&smem.a[buf][st_off + 64 * j * kMxLdsRow]) = src[0][j];
-      *reinterpret_cast<u32x4_t*>(&smem.b[buf][st_off + 64 * j * kMxLdsRow]) = src[1][j];
+    for (int j = 0; j < 4; ++j) {
+      const uint32_t off = ok ? base + j * group_stride : kDrop;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          rca, (lds_ptr_t)(abuf[buf] + (4 * wave + j) * 1024), 16, off, 0, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          rcb, (lds_ptr_t)(bbuf[buf] + (4 * wave + j) * 1024), 16, off, 0, 0, 0);
     }
   };
   auto load_group = [&](int grp) {
-    gsa = load_scale_group<kFast>(rsa, sg_off + 16 * grp, kgroups, grp);
-    gsb = load_scale_group<kFast>(rsb, sg_off + 16 * grp, kgroups, grp);
+    gsa = load_scale_group<kFast, kK512>(rsa, sg_off + 16 * grp, kgroups, grp);
+    gsb = load_scale_group<kFast, kK512>(rsb, sg_off + 16 * grp, kgroups, grp);
   };
   auto store_group = [&](int set) {
-    uint32_t* da = &smem.sc[set][0][t * kMxScaleStride];
-    uint32_t* db = &smem.sc[set][1][t * kMxScaleStride];
+    uint32_t* da = &lsc[set][0][t * kMxScaleStride];
+    uint32_t* db = &lsc[set][1][t * kMxScaleStride];
     da[0] = gsa.x; da[1] = gsa.y; da[2] = gsa.z; da[3] = gsa.w;
     db[0] = gsb.x; db[1] = gsb.y; db[2] = gsb.z; db[3] = gsb.w;
   };
@@ -192,15 +206,15 @@ __global__ __launch_bounds__(kMxThreads, 1) void mxfp4_gemm_kernel(
     const int set = (stage / kMxGroup) & 1, w = stage % kMxGroup;
 #pragma unroll
     for (int f = 0; f < kMxFrags; ++f) {
-      da[f] = smem.sc[set][0][rs_a + f * 32 * kMxScaleStride + w];
-      db[f] = smem.sc[set][1][rs_b + f * 32 * kMxScaleStride + w];
+      da[f] = lsc[set][0][rs_a + f * 32 * kMxScaleStride + w];
+      db[f] = lsc[set][1][rs_b + f * 32 * kMxScaleStride + w];
     }
   };
   auto read_frags = [&](u32x4_t (&da)[kMxFrags], u32x4_t (&db)[kMxFrags], int buf, int st) {
 #pragma unroll
     for (int f = 0; f < kMxFrags; ++f) {
-      da[f] = *reinterpret_cast<const u32x4_t*>(&smem.a[buf][rd_a + f * 32 * kMxLdsRow + 32 * st]);
-      db[f] = *reinterpret_cast<const u32x4_t*>(&smem.b[buf][rd_b + f * 32 * kMxLdsRow + 32 * st]);
+      da[f] = *reinterpret_cast<const u32x4_t*>(abuf[buf] + rd_a + f * 2048 + 512 * st);
+      db[f] = *reinterpret_cast<const u32x4_t*>(bbuf[buf] + rd_b + f * 2048 + 512 * st);
     }
   };
   // one K-step: lane group g supplies kgroup 2 st + g of the stage, i.e.
@@ -218,29 +232,35 @@ __global__ __launch_bounds__(kMxThreads, 1) void mxfp4_gemm_kernel(
             (int)ssb[fn], 2 * st, (int)ssa[fm]);
   };
 
+  constexpr int kSL = scale_group_loads(kFast, kK512);
   const int nstages = (int)((K + kMxBK - 1) / kMxBK);
-  // prologue: stages 0 and 1 into LDS buffers 0 and 1, stage 2 in flight,
-  // scale group 0 in LDS, the scales and operands of the first K-step
+  // prologue: scale group 0, stages 0-2 in flight; once stages 0 and 1 have
+  // landed (stage 2 may still be in flight) the scales are parked and the
+  // first K-step's scales and operands read
   load_group(0);
-  load_codes(stg[0], 0);
-  load_codes(stg[1], 1);
+  dma_stage(0, 0);
+  dma_stage(1, 1);
+  dma_stage(2, 2);
+  wait_counts<8, 15>();
   store_group(0);
-  store_codes(stg[0], 0);
-  store_codes(stg[1], 1);
-  load_codes(stg[0], 2);
-  __syncthreads();
+  wait_counts<8, 0>();
+  __builtin_amdgcn_s_barrier();
   read_scales(sca[0], scb[0], 0);
   read_frags(fa[0], fb[0], 0, 0);
 
   using S0 = std::integral_constant<int, 0>;
   using S1 = std::integral_constant<int, 1>;
-  // Stage s with P = s % 4.  At P == 0 the scale group after the current one
-  // is fetched into registers, at P == 2 it is stored into the LDS set of
-  // its parity (last read two stages earlier); it is first read at P == 3,
-  // for the next stage.
-  auto run_stage = [&](auto phase, int s, int cur, int nxt, int wbuf) {
+  // Stage s with P = s % 4, computed from buffer P.  The DMA of stage s+3
+  // goes to buffer (P + 3) % 4, last read in stage s-1.  At P == 0 the scale
+  // group after the current one is fetched into registers (after the DMA,
+  // so waits for the DMA never wait for it), at P == 2 it is stored into the
+  // LDS set of its parity (last read two stages earlier); it is first read
+  // at P == 3, for the next stage.  The barrier ending stage s waits for this
+  // wave's DMA of stage s+2, so in stage s+1 both its own buffer and the
+  // next one (read ahead) are complete.
+  auto run_stage = [&](auto phase, int s) {
     constexpr int P = decltype(phase)::value;
-    constexpr int C = P & 1;               // code and scale-word register set of stage s
+    constexpr int C = P & 1;               // scale-word register set of stage s
     uint32_t ssa[kMxFrags], ssb[kMxFrags];
 #pragma unroll
     for (int f = 0; f < kMxFrags; ++f) {
@@ -248,26 +268,23 @@ __global__ __launch_bounds__(kMxThreads, 1) void mxfp4_gemm_kernel(
       ssb[f] = scb[C][f] >> (8 * g);
     }
     __builtin_amdgcn_sched_barrier(0);
-    // K-step 0: fetch scales and codes ahead, read the operands of K-step 1,
-    // store the codes of stage s+2
+    // K-step 0
+    dma_stage((P + 3) % kMxBufs, s + 3);
     if (P == 0) load_group(s / kMxGroup + 1);
-    load_codes(stg[C ^ 1], s + 3);
-    read_frags(fa[1], fb[1], cur, 1);
+    read_frags(fa[1], fb[1], P, 1);
     mfma_step(S0{}, fa[0], fb[0], ssa, ssb);
-    store_codes(stg[C], wbuf);
     if (P == 2) store_group((s / kMxGroup + 1) & 1);
 #pragma unroll
     for (int i = 0; i < kMxFrags * kMxFrags; ++i) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                 // MFMA
       if (i < 8) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);      // DS read
-      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);                 // VMEM read
-      if (i < 8) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
-      if (i >= 8) __builtin_amdgcn_sched_group_barrier(0x200, P == 2 ? 2 : 1, 0);   // DS write
+      __builtin_amdgcn_sched_group_barrier(0x020, P == 0 ? 3 : 1, 0);    // VMEM read
+      if (P == 2 && i >= 8) __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);   // DS write
     }
     __builtin_amdgcn_sched_barrier(0);
     // K-step 1, with the scales and operands of the next stage's first K-step
     read_scales(sca[C ^ 1], scb[C ^ 1], s + 1);
-    read_frags(fa[0], fb[0], nxt, 0);
+    read_frags(fa[0], fb[0], (P + 1) % kMxBufs, 0);
     mfma_step(S1{}, fa[1], fb[1], ssa, ssb);
 #pragma unroll
     for (int i = 0; i < kMxFrags * kMxFrags; ++i) {
@@ -275,31 +292,33 @@ __global__ __launch_bounds__(kMxThreads, 1) void mxfp4_gemm_kernel(
       __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
     }
     __builtin_amdgcn_sched_barrier(0);
-    __syncthreads();
+    // what this wave issued after its DMA of stage s+2 may stay in flight:
+    // at least this stage's 8 DMA instructions, plus at P == 0 the scale
+    // loads issued in this stage (never more than is certainly younger)
+    wait_counts<8 + (P == 0 ? kSL : 0), 0>();
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
   };
 
   using P0 = std::integral_constant<int, 0>;
   using P1 = std::integral_constant<int, 1>;
   using P2 = std::integral_constant<int, 2>;
   using P3 = std::integral_constant<int, 3>;
-  // LDS buffers rotate mod 3: stage s + j uses buffer (cur + j) % 3
-  int s = 0, cur = 0;
-  auto next3 = [](int b) { return b == 2 ? 0 : b + 1; };
+  int s = 0;
   for (; s + 4 <= nstages; s += 4) {
-    const int c1 = next3(cur), c2 = next3(c1);
-    run_stage(P0{}, s, cur, c1, c2);
-    run_stage(P1{}, s + 1, c1, c2, cur);
-    run_stage(P2{}, s + 2, c2, cur, c1);
-    run_stage(P3{}, s + 3, cur, c1, c2);
-    cur = c1;   // (cur + 4) % 3
+    run_stage(P0{}, s);
+    run_stage(P1{}, s + 1);
+    run_stage(P2{}, s + 2);
+    run_stage(P3{}, s + 3);
   }
   {
     const int rest = nstages - s;
-    const int c1 = next3(cur), c2 = next3(c1);
-    if (rest > 0) run_stage(P0{}, s, cur, c1, c2);
-    if (rest > 1) run_stage(P1{}, s + 1, c1, c2, cur);
-    if (rest > 2) run_stage(P2{}, s + 2, c2, cur, c1);
+    if (rest > 0) run_stage(P0{}, s);
+    if (rest > 1) run_stage(P1{}, s + 1);
+    if (rest > 2) run_stage(P2{}, s + 2);
   }
+  // no DMA may still be writing LDS when the workgroup ends
+  wait_counts<0, 0>();
 
   // epilogue: out = bf16(fp32(acc + bias)).  Lane (li, g) holds, per MFMA
   // tile, row m = li and the column runs 8k + 4g .. 8k + 4g + 3 (k = 0..3);
@@ -308,7 +327,6 @@ __global__ __launch_bounds__(kMxThreads, 1) void mxfp4_gemm_kernel(
   // resource covering the tile's valid rows, so rows past M are dropped by
   // the hardware range check; columns past N get an offset beyond the range.
   const __amdgpu_buffer_rsrc_t ro = uniform_rsrc(out + m0 * N, valid_a * N * 2);
-  constexpr uint32_t kDrop = 0x80000000u;   // beyond any output range (N < 2^22)
 #pragma unroll
   for (int fm = 0; fm < kMxFrags; ++fm) {
     const uint32_t mrow = (uint32_t)((wm * kMxWaveTile + fm * 32 + li) * N);
@@ -320,7 +338,7 @@ __global__ __launch_bounds__(kMxThreads, 1) void mxfp4_gemm_kernel(
       for (int q = 0; q < 16; ++q) v[q] = acc[fn][fm][q];
 #pragma unroll
       for (int k = 0; k < 4; ++k) {
-        const uint2 b2 = *reinterpret_cast<const uint2*>(&smem.bias[nb + 8 * k + 4 * g]);
+        const uint2 b2 = *reinterpret_cast<const uint2*>(&lbias[nb + 8 * k + 4 * g]);
         v[4 * k + 0] += __uint_as_float(b2.x << 16);
         v[4 * k + 1] += __uint_as_float(b2.x & 0xFFFF0000u);
         v[4 * k + 2] += __uint_as_float(b2.y << 16);
@@ -364,19 +382,22 @@ hipError_t launch_mx_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const
   const int64_t tiles = ((M + kMxTile - 1) / kMxTile) * ((N + kMxTile - 1) / kMxTile);
   const dim3 grid((unsigned)tiles), block(kMxThreads);
   const bool fast = K % kMxBK == 0;
+  const bool k512 = K % 512 == 0;
   const bool vec = N % 8 == 0;
-  if (fast && vec)
-    hipLaunchKernelGGL((mxfp4_gemm_kernel<true, true>), grid, block, 0, stream, a_codes, a_scales,
-                       b_codes, b_scales, bias, out, M, N, K);
-  else if (fast)
-    hipLaunchKernelGGL((mxfp4_gemm_kernel<true, false>), grid, block, 0, stream, a_codes, a_scales,
-                       b_codes, b_scales, bias, out, M, N, K);
-  else if (vec)
-    hipLaunchKernelGGL((mxfp4_gemm_kernel<false, true>), grid, block, 0, stream, a_codes, a_scales,
-                       b_codes, b_scales, bias, out, M, N, K);
-  else
-    hipLaunchKernelGGL((mxfp4_gemm_kernel<false, false>), grid, block, 0, stream, a_codes,
-                       a_scales, b_codes, b_scales, bias, out, M, N, K);
+#define SOLFP4_MX_LAUNCH(F, V, W)                                                           \
+  hipLaunchKernelGGL((mxfp4_gemm_kernel<F, V, W>), grid, block, 0, stream, a_codes, a_scales, \
+                     b_codes, b_scales, bias, out, M, N, K)
+  if (fast && k512) {
+    if (vec) SOLFP4_MX_LAUNCH(true, true, true);
+    else SOLFP4_MX_LAUNCH(true, false, true);
+  } else if (fast) {
+    if (vec) SOLFP4_MX_LAUNCH(true, true, false);
+    else SOLFP4_MX_LAUNCH(true, false, false);
+  } else {
+    if (vec) SOLFP4_MX_LAUNCH(false, true, false);
+    else SOLFP4_MX_LAUNCH(false, false, false);
+  }
+#undef SOLFP4_MX_LAUNCH
   return hipGetLastError();
 }
 
