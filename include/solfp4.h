@@ -57,8 +57,8 @@ extern "C" {
 #define SOLFP4_OK 0
 #define SOLFP4_EINVAL (-1)     /* null pointer where data is needed, negative size */
 #define SOLFP4_ESHAPE (-2)     /* K not a multiple of the block (16 NVFP4, 32 MXFP4), a size of
-                                  2^31 or more, a GEMM K of 2^24 or more, or an MXFP4 GEMM N
-                                  of 2^22 or more */
+                                  2^31 or more, or a GEMM with K of 2^24 or more or N of 2^22
+                                  or more */
 #define SOLFP4_EALIGN (-3)     /* a pointer is not 16-byte aligned */
 #define SOLFP4_EWORKSPACE (-4) /* workspace missing or smaller than the *_workspace_bytes query */
 #define SOLFP4_EHIP (-5)       /* a HIP launch reported an error */
@@ -114,7 +114,8 @@ SOLFP4_API int nvfp4_quantize(const uint16_t* x, int64_t rows, int64_t K,
  * is bf16_rne(fp32(fma(alpha, acc, bias[n]))): one FP32 fused multiply-add,
  * then rounding to BF16.  Results may differ from a float64 evaluation by
  * the FP32 summation and FMA roundings plus the BF16 rounding.  M, N or K
- * equal to 0 are valid (K == 0 writes the bias, or zeros).
+ * equal to 0 are valid (K == 0 writes the bias, or zeros).  K must be below
+ * 2^24 and N below 2^22.
  */
 SOLFP4_API int nvfp4_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_global_scale,
                const uint8_t* b_codes, const uint8_t* b_scales, const float* b_global_scale,
@@ -194,7 +195,7 @@ SOLFP4_API int mxfp4_quantize(const uint16_t* x, int64_t rows, int64_t K,
  * into FP32 accumulators in an unspecified order; the bias is added in FP32
  * (one rounding), then the sum is rounded to BF16.  Products or sums outside
  * the FP32 range are unspecified.  M, N or K equal to 0 are valid (K == 0
- * writes the bias, or zeros).  N must be below 2^22.
+ * writes the bias, or zeros).  K must be below 2^24 and N below 2^22.
  */
 SOLFP4_API int mxfp4_gemm(const uint8_t* a_codes, const uint8_t* a_scales,
                const uint8_t* b_codes, const uint8_t* b_scales,

@@ -9,7 +9,8 @@ constexpr size_t kAlign = 256;
 constexpr int64_t kMaxDim = (int64_t)1 << 31;
 // a GEMM addresses one 256-row operand tile through a 32-bit byte range
 constexpr int64_t kMaxGemmK = (int64_t)1 << 24;
-constexpr int64_t kMaxMxN = (int64_t)1 << 22;
+// the output of one 256-row tile is addressed through a 32-bit byte range
+constexpr int64_t kMaxN = (int64_t)1 << 22;
 
 size_t round_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 
@@ -60,7 +61,7 @@ int gemm_checks(const uint8_t* ac, const uint8_t* as, const float* ags, const ui
   if (rc) return rc;
   rc = check_dims(K, 0);
   if (rc) return rc;
-  if (K % 16 || K >= kMaxGemmK) return SOLFP4_ESHAPE;
+  if (K % 16 || K >= kMaxGemmK || N >= kMaxN) return SOLFP4_ESHAPE;
   // the grid is one workgroup per 256 x 256 output tile
   if (((M + 255) / 256) * ((N + 255) / 256) >= kMaxDim) return SOLFP4_ESHAPE;
   const bool any_out = M > 0 && N > 0;
@@ -105,9 +106,7 @@ int mx_gemm_checks(const uint8_t* ac, const uint8_t* as, const uint8_t* bc, cons
   if (rc) return rc;
   rc = check_dims(K, 0);
   if (rc) return rc;
-  if (K % 32 || K >= kMaxGemmK) return SOLFP4_ESHAPE;
-  // the output of one 256-row tile is addressed through a 32-bit byte range
-  if (N >= kMaxMxN) return SOLFP4_ESHAPE;
+  if (K % 32 || K >= kMaxGemmK || N >= kMaxN) return SOLFP4_ESHAPE;
   if (((M + 255) / 256) * ((N + 255) / 256) >= kMaxDim) return SOLFP4_ESHAPE;
   if (M == 0 || N == 0) return SOLFP4_OK;
   if (!out) return SOLFP4_EINVAL;
@@ -128,7 +127,7 @@ const char* solfp4_strerror(int status) {
     case SOLFP4_EINVAL: return "invalid argument (null pointer or negative size)";
     case SOLFP4_ESHAPE:
       return "unsupported shape (K must be a multiple of 16, or of 32 for MXFP4; sizes below 2^31; "
-             "GEMM K below 2^24; MXFP4 GEMM N below 2^22)";
+             "GEMM K below 2^24 and N below 2^22)";
     case SOLFP4_EALIGN: return "pointer not 16-byte aligned";
     case SOLFP4_EWORKSPACE: return "workspace missing or too small";
     case SOLFP4_EHIP: return "HIP kernel launch failed";
@@ -180,7 +179,7 @@ int nvfp4_linear(const uint16_t* x, const uint8_t* w_codes, const uint8_t* w_sca
   if (rc) return rc;
   rc = check_dims(K, 0);
   if (rc) return rc;
-  if (K % 16 || K >= kMaxGemmK) return SOLFP4_ESHAPE;
+  if (K % 16 || K >= kMaxGemmK || N >= kMaxN) return SOLFP4_ESHAPE;
   if (!workspace) return SOLFP4_EINVAL;
   if (!aligned16(workspace)) return SOLFP4_EALIGN;
   const LinearLayout l = linear_layout(M, K);
@@ -233,7 +232,7 @@ int mxfp4_linear(const uint16_t* x, const uint8_t* w_codes, const uint8_t* w_sca
   if (rc) return rc;
   rc = check_dims(K, 0);
   if (rc) return rc;
-  if (K % 32 || K >= kMaxGemmK || N >= kMaxMxN) return SOLFP4_ESHAPE;
+  if (K % 32 || K >= kMaxGemmK || N >= kMaxN) return SOLFP4_ESHAPE;
   if (!workspace) return SOLFP4_EINVAL;
   if (!aligned16(workspace)) return SOLFP4_EALIGN;
   const MxLinearLayout l = mx_linear_layout(M, K);

@@ -35,7 +35,8 @@
 // buffer, so each stage ends with a single barrier.  The two threads of a
 // row load its 32 code bytes (and 4 scale bytes) with one coalesced request.
 // The MFMA's first operand is the weight tile, so each lane's accumulators
-// hold 4 consecutive output columns of one row (8-byte BF16 stores).
+// hold runs of 4 consecutive output columns of one row; one lane swap with
+// the partner 32 lanes away turns them into 16-byte runs for the stores.
 #include <type_traits>
 
 #include "device_common.h"
@@ -58,7 +59,16 @@ constexpr int kSteps = kBK / 16;              // MFMA K-steps per stage
 struct Smem {
   _Float16 a[2][kBM * kRowHalves];
   _Float16 b[2][kBN * kRowHalves];
+  uint16_t bias[kBN];
 };
+
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float floatx2_t __attribute__((ext_vector_type(2)));
+
+// Two FP32 values to a BF16 pair (round to nearest even), first in the low half.
+__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((floatx2_t{lo, hi}), bf16x2_t));
+}
 
 // High bytes of the FP16 encodings of the E2M1 magnitudes 0, .5, 1, 1.5, 2,
 // 3, 4, 6 (their low bytes are 0), as the two source words of v_perm_b32.
@@ -246,6 +256,9 @@ __global__ __launch_bounds__(kGemmThreads, 1) void nvfp4_gemm_kernel(
   convert_block(ca[0], sa4[0].x >> sshift, 1, &smem.a[0][my]);
   convert_block(cb[0], sb4[0].x >> sshift, 0, &smem.b[0][my]);
   convert_block(cb[0], sb4[0].x >> sshift, 1, &smem.b[0][my]);
+  // the tile's bias (+0 without one: fma(alpha, acc, +0) == alpha * acc for
+  // every accumulator, which never holds -0)
+  if (t < kBN) smem.bias[t] = bias && n0 + t < N ? bias[n0 + t] : (uint16_t)0;
   __syncthreads();
 
   // One stage, branch free.  P = s % 8 selects the register sets: codes of
@@ -338,41 +351,55 @@ __global__ __launch_bounds__(kGemmThreads, 1) void nvfp4_gemm_kernel(
   if (rest > 5) run_stage(P5{}, s + 5);
   if (rest > 6) run_stage(P6{}, s + 6);
 
-  // epilogue: out = bf16(fp32(alpha * acc + bias)), alpha = aA * aB in FP32
+  // epilogue: out = bf16(fp32(fma(alpha, acc, bias))), alpha = aA * aB in
+  // FP32.  Lane (li, lg) holds, per MFMA tile, row m = li and the column runs
+  // 8k + 4lg .. 8k + 4lg + 3 (k = 0..3); swapping halves with the lane 32
+  // apart gives each lane two runs of 8 consecutive columns (16-byte
+  // stores).  Stores go through a buffer resource covering the tile's valid
+  // rows, so rows past M are dropped by the hardware range check; columns
+  // past N get an offset beyond the range.
   const float alpha = a_gs[0] * b_gs[0];
+  const __amdgpu_buffer_rsrc_t ro = uniform_rsrc(out + m0 * N, min<int64_t>(M - m0, kBM) * N * 2);
+  constexpr uint32_t kDrop = 0x80000000u;   // beyond any output range (N < 2^22)
 #pragma unroll
   for (int fm = 0; fm < kFragsM; ++fm) {
-    const int64_t m = m0 + wm * kWaveTileM + fm * 32 + li;
-    if (m >= M) continue;
-    uint16_t* orow = out + m * N;
+    const uint32_t mrow = (uint32_t)((wm * kWaveTileM + fm * 32 + li) * N);
 #pragma unroll
     for (int fn = 0; fn < kFragsN; ++fn) {
+      const int nb = wn * kWaveTileN + fn * 32;
+      float v[16];
 #pragma unroll
       for (int k = 0; k < 4; ++k) {
-        const int64_t n = n0 + wn * kWaveTileN + fn * 32 + 8 * k + 4 * lg;
-        float v[4];
+        const uint2 b2 = *reinterpret_cast<const uint2*>(&smem.bias[nb + 8 * k + 4 * lg]);
+        const float bv[4] = {__uint_as_float(b2.x << 16), __uint_as_float(b2.x & 0xFFFF0000u),
+                             __uint_as_float(b2.y << 16), __uint_as_float(b2.y & 0xFFFF0000u)};
 #pragma unroll
-        for (int q = 0; q < 4; ++q) v[q] = acc[fn][fm][4 * k + q];
-        if (kVecOut && n + 3 < N) {
-          float bv[4] = {0.f, 0.f, 0.f, 0.f};
-          if (bias) {
-            const uint2 b2 = *reinterpret_cast<const uint2*>(bias + n);
-            bv[0] = __uint_as_float(b2.x << 16);
-            bv[1] = __uint_as_float(b2.x & 0xFFFF0000u);
-            bv[2] = __uint_as_float(b2.y << 16);
-            bv[3] = __uint_as_float(b2.y & 0xFFFF0000u);
-          }
-          uint32_t o[4];
+        for (int q = 0; q < 4; ++q) v[4 * k + q] = __builtin_fmaf(alpha, acc[fn][fm][4 * k + q], bv[q]);
+      }
+      uint32_t p[4][2];
 #pragma unroll
-          for (int q = 0; q < 4; ++q) o[q] = f32_to_bf16_rne(__builtin_fmaf(alpha, v[q], bv[q]));
-          *reinterpret_cast<uint2*>(orow + n) = make_uint2(o[0] | (o[1] << 16), o[2] | (o[3] << 16));
+      for (int k = 0; k < 4; ++k) {
+        p[k][0] = pack_bf16(v[4 * k], v[4 * k + 1]);
+        p[k][1] = pack_bf16(v[4 * k + 2], v[4 * k + 3]);
+      }
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        uint32_t r[4];   // 8 columns starting at nb + 16 h + 8 lg
+#pragma unroll
+        for (int d = 0; d < 2; ++d) {
+          const auto x = __builtin_amdgcn_permlane32_swap(p[2 * h][d], p[2 * h + 1][d], false, false);
+          r[d] = x[0];
+          r[2 + d] = x[1];
+        }
+        const int64_t n = n0 + nb + 16 * h + 8 * lg;
+        if (kVecOut) {
+          const uint32_t off = n < N ? (mrow + (uint32_t)n) * 2 : kDrop;
+          __builtin_amdgcn_raw_buffer_store_b128(u32x4_t{r[0], r[1], r[2], r[3]}, ro, off, 0, 0);
         } else {
 #pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            if (n + q < N) {
-              const float bq = bias ? __uint_as_float((uint32_t)bias[n + q] << 16) : 0.f;
-              orow[n + q] = (uint16_t)f32_to_bf16_rne(__builtin_fmaf(alpha, v[q], bq));
-            }
+          for (int q = 0; q < 8; ++q) {
+            const uint32_t off = n + q < N ? (mrow + (uint32_t)(n + q)) * 2 : kDrop;
+            __builtin_amdgcn_raw_buffer_store_b16((uint16_t)(r[q / 2] >> (16 * (q & 1))), ro, off, 0, 0);
           }
         }
       }
@@ -388,7 +415,7 @@ hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const fl
   const int64_t tiles = ((M + kBM - 1) / kBM) * ((N + kBN - 1) / kBN);
   const dim3 grid((unsigned)tiles), block(kGemmThreads);
   const bool fast = K % kBK == 0;
-  const bool vec = N % 4 == 0;
+  const bool vec = N % 8 == 0;
   if (fast && vec)
     hipLaunchKernelGGL((nvfp4_gemm_kernel<true, true>), grid, block, 0, stream, a_codes, a_scales,
                        a_gs, b_codes, b_scales, b_gs, bias, out, M, N, K);

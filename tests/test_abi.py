@@ -125,9 +125,11 @@ def test_linear_rejects_bad_arguments():
     assert linear(out=MIS) == EALIGN
 
 
-def test_gemm_rejects_k_beyond_tile_addressing():
+def test_gemm_rejects_sizes_beyond_tile_addressing():
     assert gemm(K=1 << 24) == ESHAPE
     assert linear(K=1 << 24) == ESHAPE
+    assert gemm(N=1 << 22) == ESHAPE
+    assert linear(N=1 << 22) == ESHAPE
 
 
 def test_mx_workspace_query():
