@@ -9,7 +9,9 @@ out 3072->3072, MLP 3072->12288->3072), each as
     nvfp4_gemm(Xq, Wq, bias)     block-scaled FP4 GEMM, BF16 out
 which is exactly the launch sequence of nvfp4_quantize(W) + nvfp4_linear.
 Inputs are synthetic (seeded, from workloads/) and resident in HBM before the
-timed region.  Prints one JSON line.
+timed region.  The same layers and inputs then run through the MXFP4 variant
+(mxfp4_quantize of W and X, mxfp4_gemm on the scaled FP4 matrix
+instructions), reported in the "mxfp4" object.  Prints one JSON line.
 """
 from __future__ import annotations
 
@@ -27,6 +29,8 @@ PEAK_HBM_GBS = 8000.0
 PEAK_FP16_MFMA_TFLOPS = 2500.0
 PEAK_FP4_MFMA_TFLOPS = 10100.0
 METRIC = "NVFP4 GEMM TFLOPS & % of FP4 MFMA peak; quantize GB/s & % HBM peak"
+# MXFP4 quantize: 2 B read, 0.5 B codes + 1/32 B scales written per element
+MX_QUANT_BYTES = 2.53125
 
 
 def parse():
@@ -36,6 +40,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="flux-12b")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-mxfp4", action="store_true", help="skip the MXFP4 variant")
     ap.add_argument("--cpu-rows", type=int, default=256, help="oracle sample: activation rows")
     ap.add_argument("--cpu-wrows", type=int, default=1024, help="oracle sample: weight rows")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
@@ -66,6 +71,79 @@ def measured_traffic():
     if kv.get("gemm_source_sha256_16") != source_hash(GEMM_SOURCE):
         return None
     return float(kv["gemm_hbm_bytes_per_launch_avg"])
+
+
+def run_mxfp4(layers, steps, warmup):
+    """Time the MXFP4 variant of the step on the same resident inputs: per
+    layer mxfp4_quantize(W), mxfp4_quantize(X), mxfp4_gemm(+bias), each
+    bracketed by HIP events on the stream the kernels are launched on."""
+    import numpy as np
+    import torch
+
+    import paper_2604_06916_amd as sol
+    dev = layers[0]["x"].device
+    bufs = []
+    for L in layers:
+        M, N, K = L["M"], L["N"], L["K"]
+        bufs.append(dict(
+            wc=torch.empty((N, K // 2), dtype=torch.uint8, device=dev),
+            ws=torch.empty((N, K // 32), dtype=torch.uint8, device=dev),
+            xc=torch.empty((M, K // 2), dtype=torch.uint8, device=dev),
+            xs=torch.empty((M, K // 32), dtype=torch.uint8, device=dev)))
+
+    def step(events=None):
+        for i, (L, B) in enumerate(zip(layers, bufs)):
+            e = events[i] if events is not None else None
+            if e:
+                e[0].record()
+            sol.mxfp4_quantize(L["w"], B["wc"], B["ws"])
+            if e:
+                e[1].record()
+            sol.mxfp4_quantize(L["x"], B["xc"], B["xs"])
+            if e:
+                e[2].record()
+            sol.mxfp4_gemm(B["xc"], B["xs"], B["wc"], B["ws"], L["b"], L["out"])
+            if e:
+                e[3].record()
+
+    for _ in range(warmup):
+        step()
+    ev = [[[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in layers]
+          for _ in range(steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(steps):
+        step(ev[s])
+    torch.cuda.synchronize()
+    ms_per_step = (time.perf_counter() - t0) / steps * 1e3
+    gemm_ms = xq_ms = 0.0
+    per_layer = []
+    for i, L in enumerate(layers):
+        xq = np.mean([ev[s][i][1].elapsed_time(ev[s][i][2]) for s in range(steps)])
+        gm = np.mean([ev[s][i][2].elapsed_time(ev[s][i][3]) for s in range(steps)])
+        gemm_ms += gm
+        xq_ms += xq
+        fl = 2.0 * L["M"] * L["N"] * L["K"]
+        per_layer.append({"layer": L["name"], "gemm_us": round(gm * 1e3, 2),
+                          "gemm_tflops": round(fl / (gm * 1e-3) / 1e12, 1),
+                          "quantize_x_us": round(xq * 1e3, 2)})
+    flops = sum(2.0 * L["M"] * L["N"] * L["K"] for L in layers)
+    gemm_tflops = flops / (gemm_ms * 1e-3) / 1e12
+    xq_bytes = sum(MX_QUANT_BYTES * L["M"] * L["K"] for L in layers)
+    quant_gbs = xq_bytes / (xq_ms * 1e-3) / 1e9
+    return {
+        "operands": "MXFP4 (E2M1 + E8M0/32), v_mfma_scale_f32_32x32x64_f8f6f4, FP32 accumulate",
+        "step_tflops": round(flops / (ms_per_step * 1e-3) / 1e12, 1),
+        "ms_per_step": round(ms_per_step, 4),
+        "gemm": {"kernel": "mxfp4_gemm_kernel", "achieved": round(gemm_tflops, 1),
+                 "peak": PEAK_FP4_MFMA_TFLOPS, "unit": "TFLOP/s",
+                 "frac": round(gemm_tflops / PEAK_FP4_MFMA_TFLOPS, 4)},
+        "quantize": {"kernel": "mxfp4_quantize_kernel (activations)",
+                     "achieved_gbs": round(quant_gbs, 1), "bytes_per_element": MX_QUANT_BYTES,
+                     "peak_gbs": PEAK_HBM_GBS, "frac_hbm": round(quant_gbs / PEAK_HBM_GBS, 4)},
+        "time_split_ms": {"gemm": round(gemm_ms, 4), "quantize_x": round(xq_ms, 4)},
+        "layers": per_layer,
+    }
 
 
 def cpu_baseline(wl, rows, wrows):
@@ -241,8 +319,11 @@ def main():
         "time_split_ms": {"gemm": round(gemm_ms_tot, 4), "quantize_x": round(xq_ms_tot, 4),
                           "quantize_w": round(wq_ms_tot, 4)},
         "layers": per_layer,
+        "mxfp4": None,
         "cpu_baseline": None,
     }
+    if not args.no_mxfp4:
+        result["mxfp4"] = run_mxfp4(layers, args.steps, args.warmup)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, args.cpu_rows, args.cpu_wrows)
     if args.copy_calibration:
