@@ -9,9 +9,10 @@
 //      magnitude) per workgroup;
 //   2. nvfp4_encode_kernel  folds the partials into alpha, tabulates
 //      r(s) = 1 / (s * alpha) for the 126 nonzero finite E4M3 scales in LDS,
-//      then streams x again, one block per lane: block amax, E4M3 scale,
-//      table lookup of r, then E2M1 encoding of 16 elements by the hardware
-//      converter.
+//      then streams x again, one block per lane pair (8 elements per lane,
+//      so every load instruction covers whole cache lines): block amax
+//      across the pair, E4M3 scale, table lookup of r, then E2M1 encoding by
+//      the hardware converter.
 // Both passes are HBM-bound streaming reads (2 B/element each) plus the
 // 0.5625 B/element of codes and scales written by the second.
 //
@@ -30,7 +31,7 @@ constexpr int kQuantThreads = 256;
 __device__ __forceinline__ u32x4_t stream_load(const uint4* p) {
   return __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
 }
-constexpr int kEncodeUnroll = 4;   // blocks per lane per iteration
+constexpr int kEncodeUnroll = 8;   // pieces per lane per iteration
 
 __global__ __launch_bounds__(kQuantThreads) void amax_partial_kernel(
     const uint4* __restrict__ x, int64_t n_vec, uint32_t* __restrict__ partial) {
@@ -73,90 +74,61 @@ __global__ __launch_bounds__(kQuantThreads) void amax_partial_kernel(
   }
 }
 
-// Encode one 16-element block held in w[0..7] (two BF16 per word, element
-// 2j in the low half).  Writes the 8 code bytes into c0/c1 and returns the
-// E4M3 scale code.  rtab[c] = 1 / (value(c) * alpha) (0 for c == 0, so a
-// zero-scale block becomes signed zeros: x * 0 keeps the sign).
-__device__ __forceinline__ uint32_t encode_block(const uint32_t (&w)[8], float t,
-                                                 bool zero_tensor, const float* rtab,
-                                                 uint32_t& c0, uint32_t& c1) {
-  ushort2_t m = as_us2(w[0] & 0x7FFF7FFFu);
-#pragma unroll
-  for (int j = 1; j < 8; ++j) m = absmax_pair(m, w[j]);
-  const uint32_t ab = max((uint32_t)m.x, (uint32_t)m.y);
-  const float amax_b = __uint_as_float(ab << 16);
-  const float q = amax_b / t;
-  const uint32_t sc = e4m3_rne_sat(zero_tensor ? 0.0f : q);
-  const float r = rtab[sc];
-  float e[16];
-#pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    e[2 * j] = __uint_as_float(w[j] << 16) * r;
-    e[2 * j + 1] = __uint_as_float(w[j] & 0xFFFF0000u) * r;
-  }
-  // hardware E2M1 encode, two elements per byte (the first in the low nibble)
-  uint32_t lo = 0, hi = 0;
-  lo = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(lo, e[0], e[1], 1.0f, 0);
-  lo = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(lo, e[2], e[3], 1.0f, 1);
-  lo = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(lo, e[4], e[5], 1.0f, 2);
-  lo = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(lo, e[6], e[7], 1.0f, 3);
-  hi = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(hi, e[8], e[9], 1.0f, 0);
-  hi = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(hi, e[10], e[11], 1.0f, 1);
-  hi = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(hi, e[12], e[13], 1.0f, 2);
-  hi = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(hi, e[14], e[15], 1.0f, 3);
-  c0 = lo;
-  c1 = hi;
-  return sc;
+// max over the aligned lane pair (quad_perm DPP: lanes 1, 0, 3, 2)
+__device__ __forceinline__ uint32_t pair_max(uint32_t v) {
+  return max(v, (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0xB1, 0xF, 0xF, false));
 }
 
-// One grid-stride iteration: kEncodeUnroll blocks per lane starting at
-// `base`.  kGuard: the iteration reaches past the last block, so loads and
-// stores are guarded (uniform choice per iteration).
+// One grid-stride iteration: kEncodeUnroll 16-byte pieces (8 elements) per
+// lane starting at piece `base`; a lane pair owns one 16-element block, so
+// consecutive lanes read consecutive pieces and write consecutive 4-byte
+// code words.  rtab[c] = 1 / (value(c) * alpha) (0 for c == 0, so a
+// zero-scale block becomes signed zeros: x * 0 keeps the sign).  kGuard: the
+// iteration reaches past the last piece (uniform choice per iteration).
 template <bool kGuard>
-__device__ __forceinline__ void encode_iter(const uint4* __restrict__ x, int64_t nblocks,
+__device__ __forceinline__ void encode_iter(const u32x4_t* __restrict__ x, int64_t npieces,
                                             int64_t base, float t, bool zero_tensor,
-                                            const float* rtab, uint2* __restrict__ codes,
+                                            const float* rtab, uint32_t* __restrict__ codes,
                                             uint8_t* __restrict__ scales) {
   const int lane = threadIdx.x & (kWave - 1);
-  u32x4_t v[kEncodeUnroll][2];
+  u32x4_t v[kEncodeUnroll];
 #pragma unroll
   for (int u = 0; u < kEncodeUnroll; ++u) {
-    const int64_t blk = base + u * kQuantThreads + threadIdx.x;
-    if (!kGuard || blk < nblocks) {
-      v[u][0] = stream_load(&x[2 * blk]);
-      v[u][1] = stream_load(&x[2 * blk + 1]);
-    } else {
-      v[u][0] = u32x4_t{0, 0, 0, 0};
-      v[u][1] = u32x4_t{0, 0, 0, 0};
-    }
+    const int64_t p = base + u * kQuantThreads + threadIdx.x;
+    v[u] = (!kGuard || p < npieces) ? __builtin_nontemporal_load(&x[p]) : u32x4_t{0, 0, 0, 0};
   }
 #pragma unroll
   for (int u = 0; u < kEncodeUnroll; ++u) {
-    const int64_t blk = base + u * kQuantThreads + threadIdx.x;
-    const uint32_t w[8] = {v[u][0].x, v[u][0].y, v[u][0].z, v[u][0].w,
-                           v[u][1].x, v[u][1].y, v[u][1].z, v[u][1].w};
-    uint32_t c0, c1;
-    const uint32_t sc = encode_block(w, t, zero_tensor, rtab, c0, c1);
-    if (!kGuard || blk < nblocks) codes[blk] = make_uint2(c0, c1);
-    // gather the scale bytes of each aligned lane quad into its first lane
-    const uint32_t s1 = (uint32_t)__builtin_amdgcn_mov_dpp((int)sc, 0x55, 0xF, 0xF, false);
-    const uint32_t s2 = (uint32_t)__builtin_amdgcn_mov_dpp((int)sc, 0xAA, 0xF, 0xF, false);
-    const uint32_t s3 = (uint32_t)__builtin_amdgcn_mov_dpp((int)sc, 0xFF, 0xF, 0xF, false);
-    if ((lane & 3) == 0) {
-      if (!kGuard || blk + 3 < nblocks) {
-        *reinterpret_cast<uint32_t*>(scales + blk) = sc | (s1 << 8) | (s2 << 16) | (s3 << 24);
-      } else {
-        if (blk < nblocks) scales[blk] = (uint8_t)sc;
-        if (blk + 1 < nblocks) scales[blk + 1] = (uint8_t)s1;
-        if (blk + 2 < nblocks) scales[blk + 2] = (uint8_t)s2;
-      }
+    const int64_t p = base + u * kQuantThreads + threadIdx.x;
+    const uint32_t w[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+    ushort2_t m = as_us2(w[0] & 0x7FFF7FFFu);
+#pragma unroll
+    for (int j = 1; j < 4; ++j) m = absmax_pair(m, w[j]);
+    const uint32_t ab = pair_max(max((uint32_t)m.x, (uint32_t)m.y));
+    const float amax_b = __uint_as_float(ab << 16);
+    const float q = amax_b / t;
+    const uint32_t sc = e4m3_rne_sat(zero_tensor ? 0.0f : q);
+    const float r = rtab[sc];
+    // hardware E2M1 encode, two elements per byte (the first in the low nibble)
+    uint32_t c = 0;
+    c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c, __uint_as_float(w[0] << 16) * r,
+                                                 __uint_as_float(w[0] & 0xFFFF0000u) * r, 1.0f, 0);
+    c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c, __uint_as_float(w[1] << 16) * r,
+                                                 __uint_as_float(w[1] & 0xFFFF0000u) * r, 1.0f, 1);
+    c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c, __uint_as_float(w[2] << 16) * r,
+                                                 __uint_as_float(w[2] & 0xFFFF0000u) * r, 1.0f, 2);
+    c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c, __uint_as_float(w[3] << 16) * r,
+                                                 __uint_as_float(w[3] & 0xFFFF0000u) * r, 1.0f, 3);
+    if (!kGuard || p < npieces) {
+      codes[p] = c;
+      if ((lane & 1) == 0) scales[p >> 1] = (uint8_t)sc;
     }
   }
 }
 
 __global__ __launch_bounds__(kQuantThreads) void nvfp4_encode_kernel(
-    const uint4* __restrict__ x, int64_t nblocks, const uint32_t* __restrict__ partial,
-    int npartial, uint2* __restrict__ codes, uint8_t* __restrict__ scales,
+    const u32x4_t* __restrict__ x, int64_t npieces, const uint32_t* __restrict__ partial,
+    int npartial, uint32_t* __restrict__ codes, uint8_t* __restrict__ scales,
     float* __restrict__ global_scale) {
   // fold the first pass's partial maxima (every workgroup does it; a few KB
   // from L2)
@@ -186,12 +158,12 @@ __global__ __launch_bounds__(kQuantThreads) void nvfp4_encode_kernel(
   __syncthreads();
 
   const int64_t per_iter = (int64_t)kQuantThreads * kEncodeUnroll;
-  for (int64_t base = (int64_t)blockIdx.x * per_iter; base < nblocks;
+  for (int64_t base = (int64_t)blockIdx.x * per_iter; base < npieces;
        base += (int64_t)gridDim.x * per_iter) {
-    if (base + per_iter <= nblocks)
-      encode_iter<false>(x, nblocks, base, t, zero_tensor, rtab, codes, scales);
+    if (base + per_iter <= npieces)
+      encode_iter<false>(x, npieces, base, t, zero_tensor, rtab, codes, scales);
     else
-      encode_iter<true>(x, nblocks, base, t, zero_tensor, rtab, codes, scales);
+      encode_iter<true>(x, npieces, base, t, zero_tensor, rtab, codes, scales);
   }
 }
 
@@ -208,17 +180,17 @@ hipError_t launch_quantize(const uint16_t* x, int64_t rows, int64_t K, uint8_t* 
                            uint8_t* scales, float* global_scale, uint32_t* partial,
                            hipStream_t stream) {
   const int64_t n = rows * K;
-  const int64_t nblocks = n / 16;
+  const int64_t npieces = n / 8;           // 8 elements per lane, 2 lanes per block
   const int npartial = amax_partial_count(n);
   hipLaunchKernelGGL(amax_partial_kernel, dim3(npartial), dim3(kQuantThreads), 0, stream,
                      reinterpret_cast<const uint4*>(x), n / 8, partial);
   const int64_t per_wg = (int64_t)kQuantThreads * kEncodeUnroll;
-  int64_t grid = (nblocks + per_wg - 1) / per_wg;
+  int64_t grid = (npieces + per_wg - 1) / per_wg;
   if (grid > kEncodeMaxGrid) grid = kEncodeMaxGrid;
   if (grid < 1) grid = 1;
   hipLaunchKernelGGL(nvfp4_encode_kernel, dim3((unsigned)grid), dim3(kQuantThreads), 0, stream,
-                     reinterpret_cast<const uint4*>(x), nblocks, partial, npartial,
-                     reinterpret_cast<uint2*>(codes), scales, global_scale);
+                     reinterpret_cast<const u32x4_t*>(x), npieces, partial, npartial,
+                     reinterpret_cast<uint32_t*>(codes), scales, global_scale);
   return hipGetLastError();
 }
 
