@@ -41,16 +41,17 @@ def parse():
     ap.add_argument("--workload", default="flux-12b")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-mxfp4", action="store_true", help="skip the MXFP4 variant")
-    ap.add_argument("--cpu-rows", type=int, default=256, help="oracle sample: activation rows")
-    ap.add_argument("--cpu-wrows", type=int, default=1024, help="oracle sample: weight rows")
+    ap.add_argument("--cpu-rows", type=int, default=4096, help="oracle sample: activation rows")
+    ap.add_argument("--cpu-wrows", type=int, default=4096, help="oracle sample: weight rows")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="after the benchmark, run a plain device-to-device copy of BYTES "
                          "three times (reference for HBM traffic counters)")
     return ap.parse_args()
 
 
-GEMM_SOURCE = os.path.join(ROOT, "paper_2604_06916_amd", "csrc", "gemm.hip")
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "nvfp4_gemm_flux-12b_traffic.txt")
+CSRC = os.path.join(ROOT, "paper_2604_06916_amd", "csrc")
+PROFILES = os.path.join(ROOT, "profiles")
+PROFILED_WORKLOAD = "flux-12b"
 
 
 def source_hash(path):
@@ -59,21 +60,22 @@ def source_hash(path):
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def measured_traffic():
+def measured_traffic(summary, source):
     """HBM bytes per GEMM launch (FETCH_SIZE + WRITE_SIZE, scaled by a plain
-    copy's reading of the same counters) from the committed counter summary,
-    or None when the kernel source changed since the counters were taken."""
+    copy's reading of the same counters) from a committed counter summary of
+    the FLUX layers, or None when the kernel source changed since the
+    counters were taken."""
     try:
-        lines = open(TRAFFIC_FILE).read().splitlines()
+        lines = open(os.path.join(PROFILES, summary)).read().splitlines()
     except OSError:
         return None
     kv = dict(l.split("=", 1) for l in lines if "=" in l and not l.startswith("#"))
-    if kv.get("gemm_source_sha256_16") != source_hash(GEMM_SOURCE):
+    if kv.get("source_sha256_16") != source_hash(os.path.join(CSRC, source)):
         return None
-    return float(kv["gemm_hbm_bytes_per_launch_avg"])
+    return float(kv["hbm_bytes_per_launch_avg"])
 
 
-def run_mxfp4(layers, steps, warmup):
+def run_mxfp4(layers, steps, warmup, profiled):
     """Time the MXFP4 variant of the step on the same resident inputs: per
     layer mxfp4_quantize(W), mxfp4_quantize(X), mxfp4_gemm(+bias), each
     bracketed by HIP events on the stream the kernels are launched on."""
@@ -137,7 +139,10 @@ def run_mxfp4(layers, steps, warmup):
         "ms_per_step": round(ms_per_step, 4),
         "gemm": {"kernel": "mxfp4_gemm_kernel", "achieved": round(gemm_tflops, 1),
                  "peak": PEAK_FP4_MFMA_TFLOPS, "unit": "TFLOP/s",
-                 "frac": round(gemm_tflops / PEAK_FP4_MFMA_TFLOPS, 4)},
+                 "frac": round(gemm_tflops / PEAK_FP4_MFMA_TFLOPS, 4),
+                 "traffic": (measured_traffic("mxfp4_gemm_flux-12b_traffic.txt", "mx_gemm.hip")
+                             if profiled else None),
+                 "traffic_unit": "HBM bytes per launch (mean over the step's GEMMs)"},
         "quantize": {"kernel": "mxfp4_quantize_kernel (activations)",
                      "achieved_gbs": round(quant_gbs, 1), "bytes_per_element": MX_QUANT_BYTES,
                      "peak_gbs": PEAK_HBM_GBS, "frac_hbm": round(quant_gbs / PEAK_HBM_GBS, 4)},
@@ -304,7 +309,8 @@ def main():
             "peak": PEAK_FP16_MFMA_TFLOPS,
             "unit": "TFLOP/s",
             "frac": round(gemm_tflops / PEAK_FP16_MFMA_TFLOPS, 4),
-            "traffic": measured_traffic(),
+            "traffic": (measured_traffic("nvfp4_gemm_flux-12b_traffic.txt", "gemm.hip")
+                        if wl.name == PROFILED_WORKLOAD else None),
             "traffic_unit": "HBM bytes per launch (mean over the step's GEMMs)",
             "algorithmic_flops_per_launch": flops_step / len(layers),
         },
@@ -323,7 +329,8 @@ def main():
         "cpu_baseline": None,
     }
     if not args.no_mxfp4:
-        result["mxfp4"] = run_mxfp4(layers, args.steps, args.warmup)
+        result["mxfp4"] = run_mxfp4(layers, args.steps, args.warmup,
+                                    wl.name == PROFILED_WORKLOAD)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, args.cpu_rows, args.cpu_wrows)
     if args.copy_calibration:
