@@ -54,23 +54,27 @@ PROFILES = os.path.join(ROOT, "profiles")
 PROFILED_WORKLOAD = "flux-12b"
 
 
-def source_hash(path):
+def source_hash(*paths):
     import hashlib
-    with open(path, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for path in paths:
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 def measured_traffic(summary, source):
     """HBM bytes per GEMM launch (FETCH_SIZE + WRITE_SIZE, scaled by a plain
     copy's reading of the same counters) from a committed counter summary of
-    the FLUX layers, or None when the kernel source changed since the
-    counters were taken."""
+    the FLUX layers, or None when the kernel source (or the device header it
+    includes) changed since the counters were taken."""
     try:
         lines = open(os.path.join(PROFILES, summary)).read().splitlines()
     except OSError:
         return None
     kv = dict(l.split("=", 1) for l in lines if "=" in l and not l.startswith("#"))
-    if kv.get("source_sha256_16") != source_hash(os.path.join(CSRC, source)):
+    if kv.get("source_sha256_16") != source_hash(os.path.join(CSRC, source),
+                                                 os.path.join(CSRC, "device_common.h")):
         return None
     return float(kv["hbm_bytes_per_launch_avg"])
 

@@ -66,9 +66,17 @@ __device__ __forceinline__ uint32_t f32_to_bf16_rne(float f) {
 // descriptor handling.
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t uniform_rsrc(const void* base, int64_t bytes) {
   const uint64_t p = (uint64_t)base;
-  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)p);
-  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(p >> 32));
-  const int n = __builtin_amdgcn_readfirstlane((int)bytes);
+  uint32_t lo = (uint32_t)p, hi = (uint32_t)(p >> 32);
+  int n = (int)bytes;
+  // The empty asm hides that the words are already uniform, so the compiler
+  // cannot drop the readfirstlane: a uniform value that was computed by
+  // vector instructions (64-bit min and multiply) and left in vector
+  // registers would put a waterfall loop around every access through the
+  // descriptor.
+  asm volatile("" : "+v"(lo), "+v"(hi), "+v"(n));
+  lo = __builtin_amdgcn_readfirstlane(lo);
+  hi = __builtin_amdgcn_readfirstlane(hi);
+  n = __builtin_amdgcn_readfirstlane(n);
   return __builtin_amdgcn_make_buffer_rsrc((void*)(((uint64_t)hi << 32) | lo), (short)0, n,
                                            0x00020000);
 }
