@@ -11,7 +11,10 @@ which is exactly the launch sequence of nvfp4_quantize(W) + nvfp4_linear.
 Inputs are synthetic (seeded, from workloads/) and resident in HBM before the
 timed region.  The same layers and inputs then run through the MXFP4 variant
 (mxfp4_quantize of W and X, mxfp4_gemm on the scaled FP4 matrix
-instructions), reported in the "mxfp4" object.  Prints one JSON line.
+instructions), reported in the "mxfp4" object.  "graphs" times the weight
+re-quantization after a policy update and the per-step linears as captured
+HIP graphs replayed without re-capture; "small_linear" is the launch-bound
+128-token layer, eager and graph-batched.  Prints one JSON line.
 """
 from __future__ import annotations
 
@@ -41,6 +44,8 @@ def parse():
     ap.add_argument("--workload", default="flux-12b")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-mxfp4", action="store_true", help="skip the MXFP4 variant")
+    ap.add_argument("--no-graphs", action="store_true",
+                    help="skip the graph-replay and small-layer measurements")
     ap.add_argument("--cpu-rows", type=int, default=4096, help="oracle sample: activation rows")
     ap.add_argument("--cpu-wrows", type=int, default=4096, help="oracle sample: weight rows")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
@@ -153,6 +158,107 @@ def run_mxfp4(layers, steps, warmup, profiled):
         "time_split_ms": {"gemm": round(gemm_ms, 4), "quantize_x": round(xq_ms, 4)},
         "layers": per_layer,
     }
+
+
+def run_graphs(layers, reps):
+    """In-place weight re-quantization with graph replay on the bench layers:
+    one graph re-quantizes every weight into its existing buffers (what runs
+    after a policy update), one replays the per-step linears (activation
+    quantize + GEMM); both captured once.  Returns replay and eager times."""
+    import torch
+
+    import paper_2604_06916_amd as sol
+
+    def update():
+        for L in layers:
+            sol.nvfp4_quantize(L["w"], L["wc"], L["ws"], L["wa"], L["qws"])
+
+    def linears():
+        for L in layers:
+            sol.nvfp4_quantize(L["x"], L["xc"], L["xs"], L["xa"], L["qws"])
+            sol.nvfp4_gemm(L["xc"], L["xs"], L["xa"], L["wc"], L["ws"], L["wa"], L["b"], L["out"])
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    g_up, g_lin = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g_up):
+        update()
+    with torch.cuda.graph(g_lin):
+        linears()
+    torch.cuda.synchronize()
+    n_w = sum(L["N"] * L["K"] for L in layers)
+    up_ms = timed(g_up.replay)
+    return {
+        "requantize_graph_ms": round(up_ms, 4),
+        "requantize_eager_ms": round(timed(update), 4),
+        "requantize_gbs": round(4.5625 * n_w / (up_ms * 1e-3) / 1e9, 1),
+        "weights_requantized": n_w,
+        "linears_graph_ms": round(timed(g_lin.replay), 4),
+        "linears_eager_ms": round(timed(linears), 4),
+    }
+
+
+def run_small_linear(reps):
+    """The 128-token 1152 -> 1152 layer, launch-bound: nvfp4_linear per call,
+    eager launches against one graph holding `batch` linears."""
+    import numpy as np
+    import torch
+
+    import paper_2604_06916_amd as sol
+    from workloads import ROLE_BIAS, ROLE_W, ROLE_X, WORKLOADS, draw_activations, draw_bias, \
+        draw_weights, seed_for
+    wl = WORKLOADS["single-1152"]
+    layer = wl.layers[0]
+    M, N, K = wl.M, layer.N, layer.K
+    dev = torch.device("cuda:0")
+
+    def to_dev(bits):
+        return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).to(dev).view(torch.bfloat16)
+    x = to_dev(draw_activations(layer.x_dist, M, K, seed_for(wl.config_id, layer.index, ROLE_X)))
+    w = to_dev(draw_weights(N, K, wl.w_sigma, seed_for(wl.config_id, layer.index, ROLE_W)))
+    b = to_dev(draw_bias(N, wl.w_sigma, seed_for(wl.config_id, layer.index, ROLE_BIAS)))
+    wc, ws, wa = sol.nvfp4_quantize(w)
+    out = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+    lws = torch.empty(sol.nvfp4_linear_workspace_bytes(M, K), dtype=torch.uint8, device=dev)
+    batch = 50
+
+    def lin():
+        sol.nvfp4_linear(x, wc, ws, wa, b, out, lws)
+    for _ in range(10):
+        lin()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps * batch):
+        lin()
+    e1.record()
+    torch.cuda.synchronize()
+    eager_us = e0.elapsed_time(e1) / (reps * batch) * 1e3
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for _ in range(batch):
+            lin()
+    g.replay()
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(reps):
+        g.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    graph_us = e0.elapsed_time(e1) / (reps * batch) * 1e3
+    fl = 2.0 * M * N * K
+    return {"layer": f"M={M} {K}->{N} nvfp4_linear (+bias)", "eager_us": round(eager_us, 2),
+            "graph_us": round(graph_us, 2),
+            "graph_tflops": round(fl / (graph_us * 1e-6) / 1e12, 2)}
 
 
 def cpu_baseline(wl, rows, wrows):
@@ -330,8 +436,13 @@ def main():
                           "quantize_w": round(wq_ms_tot, 4)},
         "layers": per_layer,
         "mxfp4": None,
+        "graphs": None,
+        "small_linear": None,
         "cpu_baseline": None,
     }
+    if not args.no_graphs:
+        result["graphs"] = run_graphs(layers, max(args.steps, 5))
+        result["small_linear"] = run_small_linear(max(args.steps, 5))
     if not args.no_mxfp4:
         result["mxfp4"] = run_mxfp4(layers, args.steps, args.warmup,
                                     wl.name == PROFILED_WORKLOAD)

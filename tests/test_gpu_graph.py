@@ -1,0 +1,163 @@
+"""In-place weight re-quantization with HIP-graph replay (the analogue of
+copying updated weights into the compiled rollout model without
+recompiling; appendix "Rollout Pipeline Details" of the paper).
+
+Two chained linear layers are captured once into a graph.  After every
+simulated policy update (a LoRA-style merge W = W0 + (alpha/r) B A of rank
+r = 32, alpha = 64, done in plain torch as the update step is not the hot
+path) the new BF16 weights are written into the same buffer, a second
+captured graph re-quantizes them into the same code/scale buffers, and the
+linear graph is replayed without re-capture.  Every replay must equal eager
+calls on the same data bit for bit; the re-quantized weights must equal the
+oracle's encoding of the merged weights bit for bit; and the output matches
+the oracle's linear within the GEMM tolerance.  Replays are interleaved with
+eager work and synchronisations."""
+import numpy as np
+import pytest
+import torch
+
+import oracle.nvfp4 as O
+import paper_2604_06916_amd as sol
+from gpu_util import bf16_from_dev, bf16_to_dev, device, rel_fro, say, u8_from_dev
+from workloads import draw_activations, draw_weights
+
+pytestmark = pytest.mark.gpu
+
+TOL = 2e-3
+RANK, LORA_ALPHA = 32, 64
+
+
+def lora_merge(w0, a, b, step):
+    """W0 + (alpha / r) * step * (B @ A), rounded to BF16 (torch, FP32)."""
+    delta = (b.float() @ a.float()) * (LORA_ALPHA / RANK) * step
+    return (w0.float() + delta).to(torch.bfloat16)
+
+
+def setup(fmt, M, dims, seed):
+    dev = device()
+    x = bf16_to_dev(draw_activations("normal", M, dims[0], seed))
+    layers = []
+    for i, (K, N) in enumerate(zip(dims[:-1], dims[1:])):
+        w0 = bf16_to_dev(draw_weights(N, K, 0.02, seed + 10 * i + 1))
+        a = bf16_to_dev(draw_weights(RANK, K, 0.02, seed + 10 * i + 2))
+        b = bf16_to_dev(draw_weights(N, RANK, 0.02, seed + 10 * i + 3))
+        L = dict(K=K, N=N, w0=w0, a=a, b=b, w=w0.clone(),
+                 wc=torch.empty((N, K // 2), dtype=torch.uint8, device=dev),
+                 y=torch.empty((M, N), dtype=torch.bfloat16, device=dev),
+                 ye=torch.empty((M, N), dtype=torch.bfloat16, device=dev))
+        if fmt == "nvfp4":
+            L["ws"] = torch.empty((N, K // 16), dtype=torch.uint8, device=dev)
+            L["wa"] = torch.empty(1, dtype=torch.float32, device=dev)
+            L["qws"] = torch.empty(max(sol.nvfp4_quantize_workspace_bytes(N, K), 256),
+                                   dtype=torch.uint8, device=dev)
+            L["lws"] = torch.empty(sol.nvfp4_linear_workspace_bytes(M, K), dtype=torch.uint8,
+                                   device=dev)
+        else:
+            L["ws"] = torch.empty((N, K // 32), dtype=torch.uint8, device=dev)
+            L["lws"] = torch.empty(sol.mxfp4_linear_workspace_bytes(M, K), dtype=torch.uint8,
+                                   device=dev)
+        layers.append(L)
+    return x, layers
+
+
+def requantize(fmt, layers):
+    for L in layers:
+        if fmt == "nvfp4":
+            sol.nvfp4_quantize(L["w"], L["wc"], L["ws"], L["wa"], L["qws"])
+        else:
+            sol.mxfp4_quantize(L["w"], L["wc"], L["ws"])
+
+
+def forward(fmt, x, layers, key):
+    h = x
+    for L in layers:
+        if fmt == "nvfp4":
+            sol.nvfp4_linear(h, L["wc"], L["ws"], L["wa"], None, L[key], L["lws"])
+        else:
+            sol.mxfp4_linear(h, L["wc"], L["ws"], None, L[key], L["lws"])
+        h = L[key]
+    return h
+
+
+def oracle_check(fmt, x, layers, got):
+    """Weights re-quantized bit-exactly; last layer within tolerance of the
+    oracle's linear on the (device) input of that layer."""
+    for L in layers:
+        wb = bf16_from_dev(L["w"])
+        if fmt == "nvfp4":
+            rc, rs, ra = O.nvfp4_quantize_ref(wb)
+            assert np.array_equal(u8_from_dev(L["wc"]), rc)
+            assert np.array_equal(u8_from_dev(L["ws"]), rs)
+            assert np.float32(L["wa"].item()) == ra
+        else:
+            rc, rs = O.mxfp4_quantize_ref(wb)
+            assert np.array_equal(u8_from_dev(L["wc"]), rc)
+            assert np.array_equal(u8_from_dev(L["ws"]), rs)
+    last, prev_in = layers[-1], (layers[-2]["y"] if len(layers) > 1 else x)
+    xin = bf16_from_dev(prev_in)
+    wq = (u8_from_dev(last["wc"]), u8_from_dev(last["ws"]))
+    if fmt == "nvfp4":
+        ref, _ = O.nvfp4_linear_ref(xin, *wq, np.float32(last["wa"].item()))
+    else:
+        ref, _ = O.mxfp4_linear_ref(xin, *wq)
+    err = rel_fro(bf16_from_dev(got), ref)
+    assert err <= TOL, err
+    return err
+
+
+@pytest.mark.parametrize("fmt", ["nvfp4", "mxfp4"])
+def test_graph_replay_after_in_place_requantization(fmt):
+    M, dims = 300, [256, 288, 160]
+    x, layers = setup(fmt, M, dims, 77)
+    requantize(fmt, layers)
+    forward(fmt, x, layers, "y")             # eager warm-up (loads the code objects)
+    torch.cuda.synchronize()
+
+    g_lin, g_req = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g_req):
+        requantize(fmt, layers)
+    with torch.cuda.graph(g_lin):
+        forward(fmt, x, layers, "y")
+    torch.cuda.synchronize()
+
+    for step in range(4):
+        if step:
+            for L in layers:
+                L["w"].copy_(lora_merge(L["w0"], L["a"], L["b"], step))   # in place
+            g_req.replay()
+        g_lin.replay()
+        torch.cuda.synchronize()
+        got = layers[-1]["y"].clone()
+        # eager calls on the same (re-quantized) weights, into other buffers
+        forward(fmt, x, layers, "ye")
+        torch.cuda.synchronize()
+        for L in layers:
+            assert torch.equal(L["y"].view(torch.int16), L["ye"].view(torch.int16)), step
+        err = oracle_check(fmt, x, layers, got)
+        say(f"{fmt} update {step}: replay == eager, rel_fro vs oracle {err:.3e}")
+
+
+@pytest.mark.parametrize("fmt", ["nvfp4", "mxfp4"])
+def test_requantize_graph_tracks_weight_buffer(fmt):
+    """The captured re-quantization reads whatever the weight buffer holds at
+    replay time: after each in-place update the codes equal an eager
+    quantization of the new weights."""
+    M, dims = 64, [512, 384]
+    x, layers = setup(fmt, M, dims, 91)
+    requantize(fmt, layers)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        requantize(fmt, layers)
+    L = layers[0]
+    for step in range(1, 4):
+        L["w"].copy_(lora_merge(L["w0"], L["a"], L["b"], -step))
+        g.replay()
+        torch.cuda.synchronize()
+        wc, ws = L["wc"].clone(), L["ws"].clone()
+        wa = L["wa"].clone() if fmt == "nvfp4" else None
+        requantize(fmt, layers)
+        torch.cuda.synchronize()
+        assert torch.equal(wc, L["wc"]) and torch.equal(ws, L["ws"])
+        if wa is not None:
+            assert torch.equal(wa, L["wa"])
