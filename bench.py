@@ -14,7 +14,9 @@ timed region.  The same layers and inputs then run through the MXFP4 variant
 instructions), reported in the "mxfp4" object.  "graphs" times the weight
 re-quantization after a policy update and the per-step linears as captured
 HIP graphs replayed without re-capture; "small_linear" is the launch-bound
-128-token layer, eager and graph-batched.  Prints one JSON line.
+128-token layer, eager and graph-batched; "stage1" runs the synthetic
+Stage-1 rollout loop (paper_2604_06916_amd/stage1.py) with BF16, NVFP4 and
+MXFP4 linears.  Prints one JSON line.
 """
 from __future__ import annotations
 
@@ -46,6 +48,7 @@ def parse():
     ap.add_argument("--no-mxfp4", action="store_true", help="skip the MXFP4 variant")
     ap.add_argument("--no-graphs", action="store_true",
                     help="skip the graph-replay and small-layer measurements")
+    ap.add_argument("--no-stage1", action="store_true", help="skip the synthetic Stage-1 rollouts")
     ap.add_argument("--cpu-rows", type=int, default=4096, help="oracle sample: activation rows")
     ap.add_argument("--cpu-wrows", type=int, default=4096, help="oracle sample: weight rows")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
@@ -261,6 +264,50 @@ def run_small_linear(reps):
             "graph_tflops": round(fl / (graph_us * 1e-6) / 1e12, 2)}
 
 
+def run_stage1():
+    """Synthetic Stage-1 rollouts (8 blocks of the FLUX-like width, 8 rollouts
+    x 4608 tokens, 6 Euler steps, reward, top/bottom selection) with every
+    linear on each backend: rollout time, the linears' share of it (HIP
+    events around every linear) and the speed-up over BF16 linears."""
+    import torch
+
+    from paper_2604_06916_amd import stage1 as G
+    cfg = G.Stage1Config()
+    dev = torch.device("cuda:0")
+    model = G.make_weights(cfg, dev)
+    x0 = G.initial_latents(cfg, dev)
+    u = G.reward_direction(cfg)
+    out = {"config": {"blocks": cfg.blocks, "hidden": cfg.hidden, "heads": cfg.heads,
+                      "mlp": cfg.mlp, "rollouts": cfg.rollouts, "tokens": cfg.tokens,
+                      "euler_steps": cfg.steps, "keep": cfg.keep,
+                      "attention": "BF16, torch fused attention"}}
+    for backend in G.BACKENDS:
+        runner = G.Runner(cfg, model, backend, dev)
+        warm = G.Stage1Config(**{**cfg.__dict__, "steps": 1})
+        runner.cfg = warm
+        runner.rollout(x0)
+        runner.cfg = cfg
+        torch.cuda.synchronize()
+        runner.linear_events = []
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        x = runner.rollout(x0)
+        r = G.rewards(cfg, x, u)
+        e1.record()
+        torch.cuda.synchronize()
+        total = e0.elapsed_time(e1)
+        lin = sum(a.elapsed_time(b) for a, b in runner.linear_events)
+        top, bottom = G.select_rollouts(r.cpu().numpy(), cfg.keep)
+        out[backend] = {"rollout_ms": round(total, 2), "linear_ms": round(lin, 2),
+                        "linear_share": round(lin / total, 4),
+                        "top": [int(i) for i in top], "bottom": [int(i) for i in bottom]}
+        del runner
+        torch.cuda.empty_cache()
+    for backend in ("nvfp4", "mxfp4"):
+        out[backend]["speedup_vs_bf16"] = round(out["bf16"]["rollout_ms"] / out[backend]["rollout_ms"], 3)
+    return out
+
+
 def cpu_baseline(wl, rows, wrows):
     """The CPU oracle on a bounded sample of the same step: per layer, `rows`
     activation rows and `wrows` weight rows at full K, quantize both and the
@@ -438,11 +485,14 @@ def main():
         "mxfp4": None,
         "graphs": None,
         "small_linear": None,
+        "stage1": None,
         "cpu_baseline": None,
     }
     if not args.no_graphs:
         result["graphs"] = run_graphs(layers, max(args.steps, 5))
         result["small_linear"] = run_small_linear(max(args.steps, 5))
+    if not args.no_stage1:
+        result["stage1"] = run_stage1()
     if not args.no_mxfp4:
         result["mxfp4"] = run_mxfp4(layers, args.steps, args.warmup,
                                     wl.name == PROFILED_WORKLOAD)

@@ -1,0 +1,203 @@
+"""Synthetic Stage-1 rollout loop around the FP4 linears.
+
+Stage 1 of the paper's two-stage framework (Sec. 3.4) samples a large pool
+of rollouts with the quantized exploration model, scores each with a reward,
+and keeps the highest- and lowest-rewarded ones for the BF16 policy update.
+Here a stack of diffusion-transformer blocks with random weights stands in
+for the denoiser, an Euler integrator for the sampler and a fixed linear
+functional for the reward; no model weights, prompts or reward models are
+involved.  Every linear layer runs through one backend:
+
+    "nvfp4"  nvfp4_linear (activations quantized on the fly, NVFP4 weights)
+    "mxfp4"  mxfp4_linear
+    "bf16"   a plain BF16 matmul (the unquantized baseline)
+
+Attention is BF16 through torch's fused attention kernels only (no fallback
+to the unfused path).  Norms, GELU, residual adds and the Euler update are
+elementwise BF16/FP32 torch ops around the linears.
+
+Block (pre-norm, no modulation):
+    h = rmsnorm(x); qkv = linear(h); a = attention(q, k, v); x = x + linear(a)
+    h = rmsnorm(x); u = gelu_tanh(linear(h)); x = x + linear(u)
+Euler step with T steps: x <- x + (1/T) * (blocks(x) - x).
+Reward of rollout i: mean over its tokens of <x_final[token], u> for a fixed
+direction u.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+
+import numpy as np
+import torch
+import torch.nn.functional as F
+from torch.nn.attention import SDPBackend, sdpa_kernel
+
+from . import _binding as sol
+
+BACKENDS = ("bf16", "nvfp4", "mxfp4")
+EPS = 1e-6
+
+
+@dataclass(frozen=True)
+class Stage1Config:
+    blocks: int = 8
+    hidden: int = 3072
+    heads: int = 24
+    mlp: int = 12288
+    rollouts: int = 8
+    tokens: int = 4608
+    steps: int = 6
+    keep: int = 4            # K: K/2 highest- and K/2 lowest-rewarded rollouts
+    w_sigma: float = 0.015
+    seed: int = 5000
+
+    @property
+    def head_dim(self):
+        return self.hidden // self.heads
+
+
+def layer_shapes(cfg):
+    """(name, N, K) of one block's linears."""
+    return [("qkv", 3 * cfg.hidden, cfg.hidden), ("out", cfg.hidden, cfg.hidden),
+            ("up", cfg.mlp, cfg.hidden), ("down", cfg.hidden, cfg.mlp)]
+
+
+def select_rollouts(rewards, keep):
+    """Indices of the keep/2 highest and keep/2 lowest rewards (host logic):
+    descending rewards for the top, ascending for the bottom, ties broken by
+    the lower index."""
+    r = np.asarray(rewards, dtype=np.float64)
+    if keep % 2 or keep > r.size:
+        raise ValueError("keep must be even and at most the number of rollouts")
+    order = np.lexsort((np.arange(r.size), -r))          # descending, stable by index
+    top = order[: keep // 2]
+    rest = order[keep // 2:]
+    bottom = rest[np.lexsort((rest, r[rest]))][: keep // 2]
+    return top, bottom
+
+
+def make_weights(cfg, device):
+    """BF16 weights and biases of every block, seeded (workloads generator)."""
+    from workloads import draw_bias, draw_weights
+    model = []
+    for b in range(cfg.blocks):
+        blk = {}
+        for j, (name, N, K) in enumerate(layer_shapes(cfg)):
+            seed = cfg.seed + 100 * b + 10 * j
+            w = draw_weights(N, K, cfg.w_sigma, seed)
+            bias = draw_bias(N, cfg.w_sigma, seed + 1)
+            blk[name] = (_bf16_dev(w, device), _bf16_dev(bias, device))
+        model.append(blk)
+    return model
+
+
+def _bf16_dev(bits, device):
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).to(device).view(torch.bfloat16)
+
+
+class Runner:
+    """Holds the backend's weights (quantized once, as after a policy update)
+    and the activation and workspace buffers of the whole loop."""
+
+    def __init__(self, cfg, model, backend, device):
+        if backend not in BACKENDS:
+            raise ValueError(backend)
+        self.cfg, self.backend, self.device = cfg, backend, device
+        M = cfg.rollouts * cfg.tokens
+        self.M = M
+        self.layers = []
+        for blk in model:
+            L = {}
+            for name, N, K in layer_shapes(cfg):
+                w, b = blk[name]
+                if backend == "nvfp4":
+                    q = sol.nvfp4_quantize(w)
+                elif backend == "mxfp4":
+                    q = sol.mxfp4_quantize(w)
+                else:
+                    q = (w.t().contiguous(),)        # [K, N] for a plain matmul
+                L[name] = (q, b, N, K)
+            self.layers.append(L)
+        kmax = max(K for _, _, K in layer_shapes(cfg))
+        if backend == "nvfp4":
+            self.ws = torch.empty(sol.nvfp4_linear_workspace_bytes(M, kmax), dtype=torch.uint8, device=device)
+        elif backend == "mxfp4":
+            self.ws = torch.empty(sol.mxfp4_linear_workspace_bytes(M, kmax), dtype=torch.uint8, device=device)
+        H, D = cfg.hidden, cfg.mlp
+        self.buf = {n: torch.empty((M, c), dtype=torch.bfloat16, device=device)
+                    for n, c in [("h", H), ("qkv", 3 * H), ("a", H), ("o", H), ("u", D), ("d", H)]}
+        self.linear_events = None
+        self.trace = None        # list: (stage name, tensor copy) of every block stage
+
+    def _t(self, name, t):
+        if self.trace is not None:
+            self.trace.append((name, t.clone()))
+        return t
+
+    def linear(self, x, layer, out):
+        q, b, N, K = layer
+        ev = None
+        if self.linear_events is not None:
+            ev = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+            ev[0].record()
+        if self.backend == "nvfp4":
+            sol.nvfp4_linear(x, q[0], q[1], q[2], b, out, self.ws)
+        elif self.backend == "mxfp4":
+            sol.mxfp4_linear(x, q[0], q[1], b, out, self.ws)
+        else:
+            torch.addmm(b, x, q[0], out=out)
+        if ev is not None:
+            ev[1].record()
+            self.linear_events.append(ev)
+        return out
+
+    def blocks(self, x):
+        cfg, B = self.cfg, self.buf
+        R, T, Hh, hd = cfg.rollouts, cfg.tokens, cfg.heads, cfg.head_dim
+        for L in self.layers:
+            self._t("x", x)
+            h = self._t("h1", _rmsnorm(x, B["h"]))
+            qkv = self._t("qkv", self.linear(h, L["qkv"], B["qkv"])).view(R, T, 3, Hh, hd)
+            q, k, v = (qkv[:, :, i].transpose(1, 2) for i in range(3))   # [R, heads, T, hd] views
+            with sdpa_kernel([SDPBackend.FLASH_ATTENTION, SDPBackend.EFFICIENT_ATTENTION]):
+                a = F.scaled_dot_product_attention(q, k, v)
+            B["a"].copy_(a.transpose(1, 2).reshape(R * T, cfg.hidden))
+            self._t("a", B["a"])
+            x = self._t("x2", x + self._t("o", self.linear(B["a"], L["out"], B["o"])))
+            h = self._t("h2", _rmsnorm(x, B["h"]))
+            u = self._t("up", self.linear(h, L["up"], B["u"]))
+            B["u"].copy_(F.gelu(u, approximate="tanh"))
+            self._t("g", B["u"])
+            x = self._t("x3", x + self._t("d", self.linear(B["u"], L["down"], B["d"])))
+        return x
+
+    def rollout(self, x0):
+        """T Euler steps from x0 [rollouts * tokens, hidden] (BF16)."""
+        x = x0
+        dt = 1.0 / self.cfg.steps
+        for _ in range(self.cfg.steps):
+            y = self.blocks(x)
+            x = (x.float() + dt * (y.float() - x.float())).to(torch.bfloat16)
+        return x
+
+
+def _rmsnorm(x, out):
+    xf = x.float()
+    out.copy_(xf * torch.rsqrt(xf.pow(2).mean(dim=-1, keepdim=True) + EPS))
+    return out
+
+
+def initial_latents(cfg, device):
+    from workloads import draw_activations
+    return _bf16_dev(draw_activations("normal", cfg.rollouts * cfg.tokens, cfg.hidden, cfg.seed + 7), device)
+
+
+def reward_direction(cfg):
+    g = np.random.Generator(np.random.PCG64(cfg.seed + 9))
+    return (g.standard_normal(cfg.hidden) / np.sqrt(cfg.hidden)).astype(np.float32)
+
+
+def rewards(cfg, x_final, u):
+    """Per-rollout mean over tokens of <x, u> (FP32)."""
+    xf = x_final.float().view(cfg.rollouts, cfg.tokens, cfg.hidden)
+    return (xf @ torch.from_numpy(u).to(xf.device)).mean(dim=1)
