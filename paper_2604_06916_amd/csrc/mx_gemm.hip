@@ -17,13 +17,18 @@
 // buffer loads with the LDS-destination bit (no register staging), into four
 // stage buffers: the loads for stage s+3 are issued while stage s computes,
 // so about two stages of time cover their latency.  A DMA instruction puts
-// lane l's 16 bytes at slot l of a 1 KB block, so each block holds 16 rows
-// as [piece][row] x 16 bytes: the same 16 lanes that read one 16-byte piece
-// of 16 consecutive rows for an MFMA operand read 256 contiguous bytes (no
-// bank conflicts, no padding).  Scale bytes are fetched 16 per row (four
-// stages) by one thread per tile row with a single load, parked in LDS, and
-// read by the lanes that use them: a lane needs the scale words of its own
-// 8 rows, which would otherwise cost a 32-cache-line load per row and stage.
+// lane l's 16 bytes at slot l of a 1 KB block; each lane quad reads the 64
+// contiguous bytes of one row, so the request coalesces (with the 16 rows in
+// adjacent lanes instead, the memory pipeline spent most of its time on 64
+// separate 16-byte accesses per instruction).  A block holds 16 rows as
+// [row][piece] x 16 bytes, the piece order of row r swizzled by (r >> 2) & 3,
+// so that the 16 lanes reading one piece of 16 consecutive rows for an MFMA
+// operand hit every bank once (no bank conflicts, no padding).  The loads
+// skip allocation in the per-CU vector cache (sc0): every line is used once
+// from there.  Scale bytes are fetched 16 per row (four stages) by one
+// thread per tile row with a single load, parked in LDS, and read by the
+// lanes that use them: a lane needs the scale words of its own 8 rows,
+// which would otherwise cost a 32-cache-line load per row and stage.
 //
 // Pipeline of stage s (buffer s % 4): the DMA of stage s+3 goes to the buffer
 // read in stage s-1; the scales and operands of the first K-step of stage
@@ -146,21 +151,28 @@ __global__ __launch_bounds__(kMxThreads, 1) void mxfp4_gemm_kernel(
   const __amdgpu_buffer_rsrc_t rsa = uniform_rsrc(a_scales + m0 * kgroups, valid_a * kgroups);
   const __amdgpu_buffer_rsrc_t rsb = uniform_rsrc(b_scales + n0 * kgroups, valid_b * kgroups);
 
-  // Code DMA: wave w fills 16-row groups 4 w .. 4 w + 3 of each operand; in
-  // one instruction lane l moves 16 bytes (piece l / 16) of row l % 16 of the
-  // group, and the hardware stores lane l's bytes at slot l of the group's
-  // 1 KB, so a group holds [piece][row] x 16 bytes.
-  const int piece = lane >> 4;
-  const uint32_t dma_off = (uint32_t)((64 * wave + (lane & 15)) * row_bytes + 16 * piece);
+  // Code DMA: wave w fills 16-row groups 4 w .. 4 w + 3 of each operand.  In
+  // one instruction lane quad l/4 reads the 64 contiguous bytes of row l/4 of
+  // the group (so the request coalesces), and the hardware stores lane l's 16
+  // bytes at slot l of the group's 1 KB: the group holds [row][piece] x 16
+  // bytes, with the piece order of row r swizzled to piece ^ ((r >> 2) & 3) so
+  // that 16 lanes reading one piece of 16 consecutive rows for an MFMA
+  // operand hit all 64 banks once.
+  const int dma_r = lane >> 2;
+  const int piece = (lane & 3) ^ ((dma_r >> 2) & 3);
+  const uint32_t dma_off = (uint32_t)((64 * wave + dma_r) * row_bytes + 16 * piece);
   const uint32_t group_stride = (uint32_t)(16 * row_bytes);
   constexpr uint32_t kDrop = 0x80000000u;   // beyond any buffer range: loads read zero,
                                             // stores are dropped (N < 2^22, K < 2^24)
   // scale staging: thread t moves the scale group of tile row t of A and B
   const uint32_t sg_off = (uint32_t)(t * kgroups);
   // MFMA operand slots of this lane: row r of the tile lives in group r / 16
-  // at slot piece * 16 + r % 16; lane (li, g) of K-step st reads piece 2 st + g
-  const int rd_a = ((wm * kMxWaveTile + li) >> 4) * 1024 + ((li & 15) << 4) + 256 * g;
-  const int rd_b = ((wn * kMxWaveTile + li) >> 4) * 1024 + ((li & 15) << 4) + 256 * g;
+  // at byte (r % 16) * 64 + 16 * (piece ^ ((r % 16) >> 2)); lane (li, g) of
+  // K-step st reads piece 2 st + g
+  const int swz = ((li & 15) >> 2) & 3;
+  const int rd_a = ((wm * kMxWaveTile + li) >> 4) * 1024 + (li & 15) * 64;
+  const int rd_b = ((wn * kMxWaveTile + li) >> 4) * 1024 + (li & 15) * 64;
+  const int q_off[2] = {16 * (g ^ swz), 16 * ((2 + g) ^ swz)};
   const int rs_a = (wm * kMxWaveTile + li) * kMxScaleStride;
   const int rs_b = (wn * kMxWaveTile + li) * kMxScaleStride;
 
@@ -186,9 +198,9 @@ __global__ __launch_bounds__(kMxThreads, 1) void mxfp4_gemm_kernel(
     for (int j = 0; j < 4; ++j) {
       const uint32_t off = ok ? base + j * group_stride : kDrop;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(
-          rca, (lds_ptr_t)(abuf[buf] + (4 * wave + j) * 1024), 16, off, 0, 0, 0);
+          rca, (lds_ptr_t)(abuf[buf] + (4 * wave + j) * 1024), 16, off, 0, 0, 1);
       __builtin_amdgcn_raw_ptr_buffer_load_lds(
-          rcb, (lds_ptr_t)(bbuf[buf] + (4 * wave + j) * 1024), 16, off, 0, 0, 0);
+          rcb, (lds_ptr_t)(bbuf[buf] + (4 * wave + j) * 1024), 16, off, 0, 0, 1);
     }
   };
   auto load_group = [&](int grp) {
@@ -213,8 +225,8 @@ __global__ __launch_bounds__(kMxThreads, 1) void mxfp4_gemm_kernel(
   auto read_frags = [&](u32x4_t (&da)[kMxFrags], u32x4_t (&db)[kMxFrags], int buf, int st) {
 #pragma unroll
     for (int f = 0; f < kMxFrags; ++f) {
-      da[f] = *reinterpret_cast<const u32x4_t*>(abuf[buf] + rd_a + f * 2048 + 512 * st);
-      db[f] = *reinterpret_cast<const u32x4_t*>(bbuf[buf] + rd_b + f * 2048 + 512 * st);
+      da[f] = *reinterpret_cast<const u32x4_t*>(abuf[buf] + rd_a + f * 2048 + q_off[st]);
+      db[f] = *reinterpret_cast<const u32x4_t*>(bbuf[buf] + rd_b + f * 2048 + q_off[st]);
     }
   };
   // one K-step: lane group g supplies kgroup 2 st + g of the stage, i.e.
