@@ -87,6 +87,42 @@ def measured_traffic(summary, source):
     return float(kv["hbm_bytes_per_launch_avg"])
 
 
+def vendor_mxfp4(layers, bufs, steps):
+    """The vendor library's MXFP4 GEMM (torch._scaled_mm on the ROCm stack)
+    on the same quantized operands, for reference: its time per layer and
+    the relative Frobenius difference of its output from mxfp4_gemm's.
+    None when this torch build has no MXFP4 scaled matmul."""
+    import torch
+
+    import paper_2604_06916_amd as sol
+    if not (hasattr(torch, "float4_e2m1fn_x2") and hasattr(torch, "float8_e8m0fnu")):
+        return None
+    res = []
+    try:
+        for L, B in zip(layers, bufs):
+            a = B["xc"].view(torch.float4_e2m1fn_x2)
+            b = B["wc"].view(torch.float4_e2m1fn_x2)
+            sa = B["xs"].view(torch.float8_e8m0fnu)
+            sb = B["ws"].view(torch.float8_e8m0fnu)
+            ref = torch._scaled_mm(a, b.t(), scale_a=sa, scale_b=sb, out_dtype=torch.bfloat16)
+            ours = sol.mxfp4_gemm(B["xc"], B["xs"], B["wc"], B["ws"])
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(steps):
+                torch._scaled_mm(a, b.t(), scale_a=sa, scale_b=sb, out_dtype=torch.bfloat16)
+            e1.record()
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1) / steps
+            diff = ((ref.float() - ours.float()).norm() / ours.float().norm()).item()
+            res.append({"vendor_gemm_us": round(ms * 1e3, 2),
+                        "vendor_gemm_tflops": round(2.0 * L["M"] * L["N"] * L["K"] / (ms * 1e-3) / 1e12, 1),
+                        "vendor_rel_diff": float(f"{diff:.3e}")})
+            del ref, ours
+    except (RuntimeError, TypeError) as e:      # no MXFP4 path in this build
+        return [{"vendor_error": str(e)[:120]}]
+    return res
+
+
 def run_mxfp4(layers, steps, warmup, profiled):
     """Time the MXFP4 variant of the step on the same resident inputs: per
     layer mxfp4_quantize(W), mxfp4_quantize(X), mxfp4_gemm(+bias), each
@@ -143,6 +179,9 @@ def run_mxfp4(layers, steps, warmup, profiled):
                           "quantize_x_us": round(xq * 1e3, 2)})
     flops = sum(2.0 * L["M"] * L["N"] * L["K"] for L in layers)
     gemm_tflops = flops / (gemm_ms * 1e-3) / 1e12
+    vendor = vendor_mxfp4(layers, bufs, steps)
+    for row, v in zip(per_layer, vendor or []):
+        row.update(v)
     xq_bytes = sum(MX_QUANT_BYTES * L["M"] * L["K"] for L in layers)
     quant_gbs = xq_bytes / (xq_ms * 1e-3) / 1e9
     return {
