@@ -49,6 +49,8 @@ def parse():
     ap.add_argument("--no-graphs", action="store_true",
                     help="skip the graph-replay and small-layer measurements")
     ap.add_argument("--no-stage1", action="store_true", help="skip the synthetic Stage-1 rollouts")
+    ap.add_argument("--no-vendor", action="store_true",
+                    help="skip the vendor MXFP4 GEMM reference (it launches mxfp4_gemm once more per layer)")
     ap.add_argument("--cpu-rows", type=int, default=4096, help="oracle sample: activation rows")
     ap.add_argument("--cpu-wrows", type=int, default=4096, help="oracle sample: weight rows")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
@@ -123,7 +125,7 @@ def vendor_mxfp4(layers, bufs, steps):
     return res
 
 
-def run_mxfp4(layers, steps, warmup, profiled):
+def run_mxfp4(layers, steps, warmup, profiled, vendor=True):
     """Time the MXFP4 variant of the step on the same resident inputs: per
     layer mxfp4_quantize(W), mxfp4_quantize(X), mxfp4_gemm(+bias), each
     bracketed by HIP events on the stream the kernels are launched on."""
@@ -179,7 +181,7 @@ def run_mxfp4(layers, steps, warmup, profiled):
                           "quantize_x_us": round(xq * 1e3, 2)})
     flops = sum(2.0 * L["M"] * L["N"] * L["K"] for L in layers)
     gemm_tflops = flops / (gemm_ms * 1e-3) / 1e12
-    vendor = vendor_mxfp4(layers, bufs, steps)
+    vendor = vendor_mxfp4(layers, bufs, steps) if vendor else None
     for row, v in zip(per_layer, vendor or []):
         row.update(v)
     xq_bytes = sum(MX_QUANT_BYTES * L["M"] * L["K"] for L in layers)
@@ -534,7 +536,7 @@ def main():
         result["stage1"] = run_stage1()
     if not args.no_mxfp4:
         result["mxfp4"] = run_mxfp4(layers, args.steps, args.warmup,
-                                    wl.name == PROFILED_WORKLOAD)
+                                    wl.name == PROFILED_WORKLOAD, not args.no_vendor)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, args.cpu_rows, args.cpu_wrows)
     if args.copy_calibration:
