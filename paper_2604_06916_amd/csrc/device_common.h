@@ -16,6 +16,16 @@ typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kWave = 64;
 
+// An LDS address, as the LDS-destination buffer loads take it.
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+
+// s_waitcnt with vmcnt(V) and lgkmcnt(L) (expcnt not waited on).
+template <int V, int L>
+__device__ __forceinline__ void wait_counts() {
+  static_assert(V >= 0 && V < 64 && L >= 0 && L < 16, "counter range");
+  __builtin_amdgcn_s_waitcnt((V & 15) | ((V >> 4) << 14) | (7 << 4) | (L << 8));
+}
+
 // Per-tensor scale divisor: largest E2M1 magnitude times largest E4M3 value.
 constexpr float kAlphaDivisor = 6.0f * 448.0f;
 

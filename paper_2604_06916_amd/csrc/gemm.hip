@@ -14,35 +14,53 @@
 // rounding round.  The per-tensor scales and the bias are applied once, in
 // the epilogue.
 //
-// Dequantization is shared by the whole workgroup: per K stage each pair of
-// threads owns one row of the A tile and one row of the B tile, each thread
-// converting 32 codes of each to FP16 and storing them to LDS, where all
-// eight waves read their MFMA operands.  Each element is converted once per
-// 256 x 256 output tile.
-// The conversion avoids the (half-rate) FP4 convert instructions: E2M1 values
-// have at most 2 significant bits, so the low byte of their FP16 encoding is
-// zero and the high byte comes from an 8-entry byte table indexed with
-// v_perm_b32 (sign bits are copied in by mask); one packed FP16 multiply then
-// applies the E4M3 block scale.
+// The dequantization is two instructions per pair of elements: the hardware
+// FP4 converter (which applies only the exponent of its scale operand) with
+// scale 2^8 gives 256 q exactly in FP16, and one packed FP16 multiply by the
+// E4M3 byte shifted into an FP16 bit pattern (which reads as s * 2^-8, the
+// two formats' mantissa fields being aligned and E4M3 subnormals landing on
+// FP16 subnormals) gives q * s exactly.
 //
-// Tiling: 256 x 256 output tile per workgroup of 8 waves (2 x 4, two per
-// SIMD so one wave's waits are covered by the other's MFMAs), each wave
-// owning 128 x 64 (4 x 2 MFMA tiles of 32 x 32, accumulators in AGPRs); K
-// advances 64 elements (4 NVFP4 blocks) per stage.  LDS holds two stages of
-// FP16 A and B tiles (rows padded to 144 bytes: conflict-free 16-byte row
-// accesses).  Packed codes for stage s+2 are fetched into registers while
-// stage s runs its MFMAs and stage s+1 is converted into the other LDS
-// buffer, so each stage ends with a single barrier.  The two threads of a
-// row load its 32 code bytes (and 4 scale bytes) with one coalesced request.
-// The MFMA's first operand is the weight tile, so each lane's accumulators
-// hold runs of 4 consecutive output columns of one row; one lane swap with
-// the partner 32 lanes away turns them into 16-byte runs for the stores.
+// Two kernels:
+//   nvfp4_gemm_lane_kernel (K % 128 == 0, every model layer): codes travel
+//     from HBM into LDS by DMA and each wave dequantizes its own MFMA operands
+//     in registers, so LDS carries 0.5 B/element of codes instead of 2 B of
+//     FP16 per operand read;
+//   nvfp4_gemm_kernel (any K % 16 == 0): the workgroup converts each stage
+//     once into FP16 tiles in LDS, which all waves read.
 #include <type_traits>
 
 #include "device_common.h"
 #include "kernels.h"
 
 namespace solfp4 {
+
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float floatx2_t __attribute__((ext_vector_type(2)));
+
+// Two FP32 values to a BF16 pair (round to nearest even), first in the low half.
+__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((floatx2_t{lo, hi}), bf16x2_t));
+}
+
+// ---------------------------------------------------------------------------
+// nvfp4_gemm_kernel: workgroup-shared dequantization, any K % 16 == 0.
+//
+// Per K stage each pair of threads owns one row of the A tile and one row of
+// the B tile, each thread converting 32 codes of each to FP16 and storing
+// them to LDS, where all eight waves read their MFMA operands: each element
+// is converted once per 256 x 256 output tile.  Tiling: 8 waves (2 x 4, two
+// per SIMD so one wave's waits are covered by the other's MFMAs), each wave
+// owning 128 x 64 (4 x 2 MFMA tiles of 32 x 32); K advances 64 elements
+// (4 NVFP4 blocks) per stage.  LDS holds two stages of FP16 A and B tiles
+// (rows padded to 144 bytes: conflict-free 16-byte row accesses).  Packed
+// codes for stage s+2 are fetched into registers while stage s runs its
+// MFMAs and stage s+1 is converted into the other LDS buffer, so each stage
+// ends with a single barrier.  The two threads of a row load its 32 code
+// bytes (and 4 scale bytes) with one coalesced request.  The MFMA's first
+// operand is the weight tile, so each lane's accumulators hold runs of 4
+// consecutive output columns of one row; one lane swap with the partner 32
+// lanes away turns them into 16-byte runs for the stores.
 
 constexpr int kBM = 256;
 constexpr int kBN = 256;
@@ -62,34 +80,15 @@ struct Smem {
   uint16_t bias[kBN];
 };
 
-typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
-typedef float floatx2_t __attribute__((ext_vector_type(2)));
-
-// Two FP32 values to a BF16 pair (round to nearest even), first in the low half.
-__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
-  return __builtin_bit_cast(uint32_t, __builtin_convertvector((floatx2_t{lo, hi}), bf16x2_t));
-}
-
-// High bytes of the FP16 encodings of the E2M1 magnitudes 0, .5, 1, 1.5, 2,
-// 3, 4, 6 (their low bytes are 0), as the two source words of v_perm_b32.
-constexpr uint32_t kLutLo = 0x3E3C3800u;
-constexpr uint32_t kLutHi = 0x46444240u;
-
 // 8 E2M1 codes (element 2j in the low nibble of byte j) times the block
-// scale s2 = (s, s) in FP16, as 4 words of FP16 pairs (elements 2j, 2j+1).
+// scale, as 4 words of FP16 pairs (elements 2j, 2j+1); s2 holds s * 2^-8 in
+// both halves.
 __device__ __forceinline__ void dequant8(uint32_t w, uint32_t s2, uint32_t (&d)[4]) {
-  // high bytes of the even elements (0, 2, 4, 6), signs in bit 7
-  const uint32_t ev = __builtin_amdgcn_perm(kLutHi, kLutLo, w & 0x07070707u) |
-                      ((w << 4) & 0x80808080u);
-  // and of the odd elements (1, 3, 5, 7)
-  const uint32_t od = __builtin_amdgcn_perm(kLutHi, kLutLo, (w >> 4) & 0x07070707u) |
-                      (w & 0x80808080u);
-  // interleave into FP16 pairs: [0, ev.byte j, 0, od.byte j]
   const half2_t s = as_h2(s2);
-  d[0] = h2_as_u32(as_h2(__builtin_amdgcn_perm(od, ev, 0x040C000Cu)) * s);
-  d[1] = h2_as_u32(as_h2(__builtin_amdgcn_perm(od, ev, 0x050C010Cu)) * s);
-  d[2] = h2_as_u32(as_h2(__builtin_amdgcn_perm(od, ev, 0x060C020Cu)) * s);
-  d[3] = h2_as_u32(as_h2(__builtin_amdgcn_perm(od, ev, 0x070C030Cu)) * s);
+  d[0] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 256.0f, 0) * s);
+  d[1] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 256.0f, 1) * s);
+  d[2] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 256.0f, 2) * s);
+  d[3] = h2_as_u32(__builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 256.0f, 3) * s);
 }
 
 // One thread's share of a stage: half a row of one operand, 32 codes (16
@@ -176,9 +175,8 @@ __device__ __forceinline__ u32x4_t load_scales(const TileSrc& src, int64_t K, in
 // subnormals); one exact multiply by 2^8 restores s.
 __device__ __forceinline__ void convert_block(const HalfRow& r, uint32_t sc2, int j,
                                               _Float16* dst) {
-  const half2_t k256 = {(_Float16)256.0f, (_Float16)256.0f};
   const uint32_t c = (sc2 >> (8 * j)) & 0xFFu;
-  const uint32_t s2 = h2_as_u32(as_h2((c << 7) | (c << 23)) * k256);
+  const uint32_t s2 = (c << 7) | (c << 23);   // s * 2^-8 in both FP16 halves
   const uint32_t w0 = j == 0 ? r.c.x : r.c.z;
   const uint32_t w1 = j == 0 ? r.c.y : r.c.w;
   uint32_t d[4], e[4];
@@ -407,15 +405,408 @@ __global__ __launch_bounds__(kGemmThreads, 1) void nvfp4_gemm_kernel(
   }
 }
 
+// ---------------------------------------------------------------------------
+// nvfp4_gemm_lane_kernel: lane-side dequantization, K % 128 == 0.
+//
+// Tiling and data movement follow the MXFP4 GEMM: a 256 x 256 output tile
+// per workgroup of 4 waves (one per SIMD), each wave owning 128 x 128 (4 x 4
+// MFMA tiles of 32 x 32, 256 FP32 accumulators per lane); K advances 128
+// elements (64 code bytes per row) per stage; codes go from global memory
+// straight into four LDS stage buffers by DMA, three stages ahead, each lane
+// quad reading the 64 contiguous bytes of one row, stored as [row][piece] x
+// 16 bytes with the piece order of row r swizzled by (r >> 2) & 3 (no bank
+// conflicts on the operand reads).
+//
+// Each wave turns its own operands into FP16 in registers.  The order of K
+// inside a stage is free as long as both operands use the same one, so lane
+// group g (lanes 32g .. 32g+31) of K-step j supplies the 8 elements
+// 32 p + 8 (j % 4) .. +7 with p = g for j < 4 and p = 2 + g after: one
+// 16-byte LDS read of a row's piece p feeds four K-steps, and the 8 elements
+// of a K-step always sit in one NVFP4 block.  Scales are staged through LDS
+// already as FP16 patterns (s * 2^-8, two blocks per word), so a lane reads
+// the word of its row and piece and a packed multiply with the half selected
+// by op_sel applies the block scale.  Per K-step a wave converts 8 fragments
+// (64 VALU instructions) under 16 MFMAs.
+
+constexpr int kLTile = 256;                     // output tile edge (M and N)
+constexpr int kLBK = 128;                       // K elements per stage
+constexpr int kLRowBytes = kLBK / 2;            // code bytes per row per stage
+constexpr int kLThreads = 256;
+constexpr int kLWaveTile = 128;
+constexpr int kLFrags = kLWaveTile / 32;        // 32 x 32 MFMA tiles per wave edge
+constexpr int kLBufs = 4;                       // LDS stage buffers (loads run 3 stages ahead)
+constexpr int kLStageBytes = kLTile * kLRowBytes;   // one operand, one stage
+constexpr int kLScaleStride = 5;                // words per row in LDS (4 + 1 pad)
+
+// The 8 elements of one K-step (codes of word w, element j in nibble j)
+// times the scale pattern s (s * 2^-8 in both halves): 256 q from the
+// converter, then one exact packed multiply per pair.
+__device__ __forceinline__ half8_t dequant_step(uint32_t w, half2_t s) {
+  const half2_t d0 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 256.0f, 0) * s;
+  const half2_t d1 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 256.0f, 1) * s;
+  const half2_t d2 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 256.0f, 2) * s;
+  const half2_t d3 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 256.0f, 3) * s;
+  typedef _Float16 half4_t __attribute__((ext_vector_type(4)));
+  const half4_t lo = __builtin_shufflevector(d0, d1, 0, 1, 2, 3);
+  const half4_t hi = __builtin_shufflevector(d2, d3, 0, 1, 2, 3);
+  return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
+// Scale bytes b0 (low) and b1 of a word's byte pair, as the FP16 patterns
+// b << 7 (s * 2^-8) in the low and high half.
+__device__ __forceinline__ uint32_t scale_patterns(uint32_t w, bool high_pair) {
+  return __builtin_amdgcn_perm(0u, w, high_pair ? 0x0C030C02u : 0x0C010C00u) << 7;
+}
+
+template <bool kVecOut>
+__global__ __launch_bounds__(kLThreads, 1) void nvfp4_gemm_lane_kernel(
+    const uint8_t* __restrict__ a_codes, const uint8_t* __restrict__ a_scales,
+    const float* __restrict__ a_gs, const uint8_t* __restrict__ b_codes,
+    const uint8_t* __restrict__ b_scales, const float* __restrict__ b_gs,
+    const uint16_t* __restrict__ bias, uint16_t* __restrict__ out, int64_t M, int64_t N,
+    int64_t K) {
+  // one array per stage buffer and operand, so the compiler can tell the
+  // buffer being filled by DMA from the one being read
+  __shared__ __attribute__((aligned(1024))) uint8_t la0[kLStageBytes], la1[kLStageBytes],
+      la2[kLStageBytes], la3[kLStageBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t lb0[kLStageBytes], lb1[kLStageBytes],
+      lb2[kLStageBytes], lb3[kLStageBytes];
+  __shared__ uint32_t lsc[2][2][kLTile * kLScaleStride];   // [stage parity][operand][row, word]
+  __shared__ uint16_t lbias[kLTile];
+  uint8_t* const abuf[kLBufs] = {la0, la1, la2, la3};
+  uint8_t* const bbuf[kLBufs] = {lb0, lb1, lb2, lb3};
+
+  const int tiles_m = (int)((M + kLTile - 1) / kLTile);
+  const int tiles_n = (int)((N + kLTile - 1) / kLTile);
+  int tm, tn;
+  tile_coords(tiles_m, tiles_n, tm, tn);
+  const int64_t m0 = (int64_t)tm * kLTile;
+  const int64_t n0 = (int64_t)tn * kLTile;
+
+  const int t = threadIdx.x;
+  const int lane = t & (kWave - 1);
+  const int wave = t / kWave;
+  const int wm = wave >> 1;
+  const int wn = wave & 1;
+  const int li = lane & 31;
+  const int g = lane >> 5;
+
+  const int64_t row_bytes = K / 2;
+  const int64_t scale_row = K / 16;
+  const int64_t valid_a = min<int64_t>(M - m0, kLTile);
+  const int64_t valid_b = min<int64_t>(N - n0, kLTile);
+  const __amdgpu_buffer_rsrc_t rca = uniform_rsrc(a_codes + m0 * row_bytes, valid_a * row_bytes);
+  const __amdgpu_buffer_rsrc_t rcb = uniform_rsrc(b_codes + n0 * row_bytes, valid_b * row_bytes);
+  const __amdgpu_buffer_rsrc_t rsa = uniform_rsrc(a_scales + m0 * scale_row, valid_a * scale_row);
+  const __amdgpu_buffer_rsrc_t rsb = uniform_rsrc(b_scales + n0 * scale_row, valid_b * scale_row);
+
+  // code DMA: wave w fills 16-row groups 4 w .. 4 w + 3 of each operand; lane
+  // quad l/4 reads the 64 bytes of row l/4 of the group, lane l's 16 bytes
+  // land in slot l of the group's 1 KB
+  const int dma_r = lane >> 2;
+  const int piece = (lane & 3) ^ ((dma_r >> 2) & 3);
+  const uint32_t dma_off = (uint32_t)((64 * wave + dma_r) * row_bytes + 16 * piece);
+  const uint32_t group_stride = (uint32_t)(16 * row_bytes);
+  // scale staging: thread t moves the 8 scale bytes of tile row t of A and B
+  const uint32_t sg_off = (uint32_t)(t * scale_row);
+  // operand slots of this lane: row r of the tile lives in group r / 16 at
+  // byte (r % 16) * 64 + 16 * (piece ^ ((r % 16) >> 2)); lane group g reads
+  // piece g in K-steps 0-3 and piece 2 + g in K-steps 4-7
+  const int swz = ((li & 15) >> 2) & 3;
+  const int rd_a = ((wm * kLWaveTile + li) >> 4) * 1024 + (li & 15) * 64;
+  const int rd_b = ((wn * kLWaveTile + li) >> 4) * 1024 + (li & 15) * 64;
+  const int q_off[2] = {16 * (g ^ swz), 16 * ((2 + g) ^ swz)};
+  // and its scale words: word p of a row holds the patterns of blocks 2p, 2p+1
+  const int rs_a = (wm * kLWaveTile + li) * kLScaleStride + g;
+  const int rs_b = (wn * kLWaveTile + li) * kLScaleStride + g;
+
+  // the tile's bias (+0 without one: fma(alpha, acc, +0) == alpha * acc for
+  // every accumulator, which never holds -0)
+  lbias[t] = bias && n0 + t < N ? bias[n0 + t] : (uint16_t)0;
+
+  floatx16_t acc[kLFrags][kLFrags];
+#pragma unroll
+  for (int i = 0; i < kLFrags; ++i)
+#pragma unroll
+    for (int j = 0; j < kLFrags; ++j) acc[i][j] = floatx16_t{};
+
+  u32x2_t gsa, gsb;                                  // scale bytes of one stage in flight
+  uint32_t sca[2][kLFrags][2], scb[2][kLFrags][2];   // [stage parity][frag][half stage]
+  u32x4_t ca[2][kLFrags], cb[2][kLFrags];            // code pieces, [half stage][frag]
+  half8_t oa[2][kLFrags], ob[2][kLFrags];            // FP16 operands, [K-step parity][frag]
+
+  // 8 DMA instructions per wave: stage `stage` into buffer `buf`.  Stages
+  // past K read bytes of later rows or zeros into buffers never computed.
+  auto dma_stage = [&](int buf, int stage) {
+    const uint32_t base = dma_off + (uint32_t)stage * kLRowBytes;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint32_t off = base + j * group_stride;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          rca, (lds_ptr_t)(abuf[buf] + (4 * wave + j) * 1024), 16, off, 0, 0, 1);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          rcb, (lds_ptr_t)(bbuf[buf] + (4 * wave + j) * 1024), 16, off, 0, 0, 1);
+    }
+  };
+  auto fetch_scales = [&](int stage) {
+    gsa = __builtin_amdgcn_raw_buffer_load_b64(rsa, sg_off + 8 * stage, 0, 0);
+    gsb = __builtin_amdgcn_raw_buffer_load_b64(rsb, sg_off + 8 * stage, 0, 0);
+  };
+  auto store_scales = [&](int set) {
+    uint32_t* da = &lsc[set][0][t * kLScaleStride];
+    uint32_t* db = &lsc[set][1][t * kLScaleStride];
+    da[0] = scale_patterns(gsa.x, false);
+    da[1] = scale_patterns(gsa.x, true);
+    da[2] = scale_patterns(gsa.y, false);
+    da[3] = scale_patterns(gsa.y, true);
+    db[0] = scale_patterns(gsb.x, false);
+    db[1] = scale_patterns(gsb.x, true);
+    db[2] = scale_patterns(gsb.y, false);
+    db[3] = scale_patterns(gsb.y, true);
+  };
+  // this lane's scale words of `stage` (its 4 A rows and 4 B rows, both pieces)
+  auto read_scales = [&](uint32_t (&da)[kLFrags][2], uint32_t (&db)[kLFrags][2], int stage) {
+    const int set = stage & 1;
+#pragma unroll
+    for (int f = 0; f < kLFrags; ++f) {
+      da[f][0] = lsc[set][0][rs_a + f * 32 * kLScaleStride];
+      da[f][1] = lsc[set][0][rs_a + f * 32 * kLScaleStride + 2];
+      db[f][0] = lsc[set][1][rs_b + f * 32 * kLScaleStride];
+      db[f][1] = lsc[set][1][rs_b + f * 32 * kLScaleStride + 2];
+    }
+  };
+  auto read_codes = [&](int half, int buf) {
+#pragma unroll
+    for (int f = 0; f < kLFrags; ++f) {
+      ca[half][f] = *reinterpret_cast<const u32x4_t*>(abuf[buf] + rd_a + f * 2048 + q_off[half]);
+      cb[half][f] = *reinterpret_cast<const u32x4_t*>(bbuf[buf] + rd_b + f * 2048 + q_off[half]);
+    }
+  };
+  // K-step j of a stage (scale words ss) into operand set d
+  auto convert = [&](auto step, const uint32_t (&ssa)[kLFrags][2],
+                     const uint32_t (&ssb)[kLFrags][2], int d) {
+    constexpr int j = decltype(step)::value;
+    constexpr int h = j >> 2, w = j & 3;
+#pragma unroll
+    for (int f = 0; f < kLFrags; ++f) {
+      const half2_t xa = as_h2(ssa[f][h]), xb = as_h2(ssb[f][h]);
+      const half2_t sa = (w & 2) ? __builtin_shufflevector(xa, xa, 1, 1) : __builtin_shufflevector(xa, xa, 0, 0);
+      const half2_t sb = (w & 2) ? __builtin_shufflevector(xb, xb, 1, 1) : __builtin_shufflevector(xb, xb, 0, 0);
+      oa[d][f] = dequant_step(ca[h][f][w], sa);
+      ob[d][f] = dequant_step(cb[h][f][w], sb);
+    }
+  };
+  auto mfma_step = [&](int d) {
+#pragma unroll
+    for (int fn = 0; fn < kLFrags; ++fn)
+#pragma unroll
+      for (int fm = 0; fm < kLFrags; ++fm)
+        acc[fn][fm] = __builtin_amdgcn_mfma_f32_32x32x16_f16(ob[d][fn], oa[d][fm], acc[fn][fm], 0, 0, 0);
+  };
+  // 16 MFMAs, each followed by up to 4 VALU instructions of the next
+  // K-step's conversion and kR / kV / kW of the step's LDS reads, memory
+  // loads and LDS writes
+  auto interleave = [&](auto reads, auto vmem, auto writes) {
+    constexpr int kR = decltype(reads)::value, kV = decltype(vmem)::value,
+                  kW = decltype(writes)::value;
+#pragma unroll
+    for (int i = 0; i < kLFrags * kLFrags; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                          // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);                          // VALU
+      if (i < kR) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);              // DS read
+      if (i < kV) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);              // VMEM read
+      if (i < kW) __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);              // DS write
+    }
+  };
+
+  using I0 = std::integral_constant<int, 0>;
+  using I4 = std::integral_constant<int, 4>;
+  using I8 = std::integral_constant<int, 8>;
+  using I10 = std::integral_constant<int, 10>;
+  using I12 = std::integral_constant<int, 12>;
+  using J0 = std::integral_constant<int, 0>;
+  using J1 = std::integral_constant<int, 1>;
+  using J2 = std::integral_constant<int, 2>;
+  using J3 = std::integral_constant<int, 3>;
+  using J4 = std::integral_constant<int, 4>;
+  using J5 = std::integral_constant<int, 5>;
+  using J6 = std::integral_constant<int, 6>;
+  using J7 = std::integral_constant<int, 7>;
+
+  const int nstages = (int)(K / kLBK);
+  // prologue: scales of stages 0 and 1 parked in LDS, stage 2's in
+  // registers, codes of stages 0-2 in flight; once stages 0 and 1 have
+  // landed, the first half stage's codes and the scales of stage 0 are read
+  // and K-step 0 converted.  The second barrier keeps stage 0 from parking
+  // stage 2's scales over set 0 before every wave has read it.
+  fetch_scales(0);
+  store_scales(0);
+  fetch_scales(1);
+  store_scales(1);
+  dma_stage(0, 0);
+  dma_stage(1, 1);
+  dma_stage(2, 2);
+  fetch_scales(2);
+  wait_counts<10, 0>();
+  __builtin_amdgcn_s_barrier();
+  read_scales(sca[0], scb[0], 0);
+  read_codes(0, 0);
+  wait_counts<63, 0>();
+  __builtin_amdgcn_s_barrier();
+  convert(J0{}, sca[0], scb[0], 0);
+
+  // Stage s with P = s % 4 (buffer P, scale parity C = P % 2).  K-step 0
+  // issues the DMA of stage s+3 into buffer (P + 3) % 4 (last read in stage
+  // s-1), parks the scales of stage s+2 in set C (last read in stage s-1,
+  // next read in stage s+1) and fetches those of stage s+3, and reads this
+  // stage's second code half; K-step 4 reads the next stage's first code
+  // half and scales; K-step 7 converts the next stage's K-step 0.  The
+  // barrier that ends stage s waits for this wave's DMA of stage s+2, so in
+  // stage s+1 both its own buffer and the next one are complete.
+  auto run_stage = [&](auto phase, int s) {
+    constexpr int P = decltype(phase)::value;
+    constexpr int C = P & 1;
+    __builtin_amdgcn_sched_barrier(0);
+    dma_stage((P + 3) % kLBufs, s + 3);
+    store_scales(C);
+    fetch_scales(s + 3);
+    read_codes(1, P);
+    mfma_step(0);
+    convert(J1{}, sca[C], scb[C], 1);
+    interleave(I4{}, I10{}, I8{});
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_step(1);
+    convert(J2{}, sca[C], scb[C], 0);
+    interleave(I0{}, I0{}, I0{});
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_step(0);
+    convert(J3{}, sca[C], scb[C], 1);
+    interleave(I0{}, I0{}, I0{});
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_step(1);
+    convert(J4{}, sca[C], scb[C], 0);
+    interleave(I0{}, I0{}, I0{});
+    __builtin_amdgcn_sched_barrier(0);
+    read_codes(0, (P + 1) % kLBufs);
+    read_scales(sca[C ^ 1], scb[C ^ 1], s + 1);
+    mfma_step(0);
+    convert(J5{}, sca[C], scb[C], 1);
+    interleave(I12{}, I0{}, I0{});
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_step(1);
+    convert(J6{}, sca[C], scb[C], 0);
+    interleave(I0{}, I0{}, I0{});
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_step(0);
+    convert(J7{}, sca[C], scb[C], 1);
+    interleave(I0{}, I0{}, I0{});
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_step(1);
+    convert(J0{}, sca[C ^ 1], scb[C ^ 1], 0);
+    interleave(I0{}, I0{}, I0{});
+    __builtin_amdgcn_sched_barrier(0);
+    // what this wave issued after its DMA of stage s+2 may stay in flight:
+    // this stage's 8 DMA instructions and 2 scale loads
+    wait_counts<10, 0>();
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
+  using P0 = std::integral_constant<int, 0>;
+  using P1 = std::integral_constant<int, 1>;
+  using P2 = std::integral_constant<int, 2>;
+  using P3 = std::integral_constant<int, 3>;
+  int s = 0;
+  for (; s + 4 <= nstages; s += 4) {
+    run_stage(P0{}, s);
+    run_stage(P1{}, s + 1);
+    run_stage(P2{}, s + 2);
+    run_stage(P3{}, s + 3);
+  }
+  {
+    const int rest = nstages - s;
+    if (rest > 0) run_stage(P0{}, s);
+    if (rest > 1) run_stage(P1{}, s + 1);
+    if (rest > 2) run_stage(P2{}, s + 2);
+  }
+  // no DMA may still be writing LDS when the workgroup ends
+  wait_counts<0, 0>();
+
+  // epilogue: out = bf16(fp32(fma(alpha, acc, bias))), alpha = aA * aB in
+  // FP32.  Lane (li, g) holds, per MFMA tile, row m = li and the column runs
+  // 8k + 4g .. 8k + 4g + 3 (k = 0..3); swapping halves with the lane 32 apart
+  // gives each lane two runs of 8 consecutive columns (16-byte stores).
+  // Stores go through a buffer resource covering the tile's valid rows, so
+  // rows past M are dropped by the hardware range check; columns past N get
+  // an offset beyond the range.
+  const float alpha = a_gs[0] * b_gs[0];
+  const __amdgpu_buffer_rsrc_t ro = uniform_rsrc(out + m0 * N, valid_a * N * 2);
+  constexpr uint32_t kDrop = 0x80000000u;   // beyond any output range (N < 2^22)
+#pragma unroll
+  for (int fm = 0; fm < kLFrags; ++fm) {
+    const uint32_t mrow = (uint32_t)((wm * kLWaveTile + fm * 32 + li) * N);
+#pragma unroll
+    for (int fn = 0; fn < kLFrags; ++fn) {
+      const int nb = wn * kLWaveTile + fn * 32;
+      float v[16];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const uint2 b2 = *reinterpret_cast<const uint2*>(&lbias[nb + 8 * k + 4 * g]);
+        const float bv[4] = {__uint_as_float(b2.x << 16), __uint_as_float(b2.x & 0xFFFF0000u),
+                             __uint_as_float(b2.y << 16), __uint_as_float(b2.y & 0xFFFF0000u)};
+#pragma unroll
+        for (int q = 0; q < 4; ++q) v[4 * k + q] = __builtin_fmaf(alpha, acc[fn][fm][4 * k + q], bv[q]);
+      }
+      uint32_t p[4][2];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        p[k][0] = pack_bf16(v[4 * k], v[4 * k + 1]);
+        p[k][1] = pack_bf16(v[4 * k + 2], v[4 * k + 3]);
+      }
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        uint32_t r[4];   // 8 columns starting at nb + 16 h + 8 g
+#pragma unroll
+        for (int d = 0; d < 2; ++d) {
+          const auto x = __builtin_amdgcn_permlane32_swap(p[2 * h][d], p[2 * h + 1][d], false, false);
+          r[d] = x[0];
+          r[2 + d] = x[1];
+        }
+        const int64_t n = n0 + nb + 16 * h + 8 * g;
+        if (kVecOut) {
+          const uint32_t off = n < N ? (mrow + (uint32_t)n) * 2 : kDrop;
+          __builtin_amdgcn_raw_buffer_store_b128(u32x4_t{r[0], r[1], r[2], r[3]}, ro, off, 0, 0);
+        } else {
+#pragma unroll
+          for (int q = 0; q < 8; ++q) {
+            const uint32_t off = n + q < N ? (mrow + (uint32_t)(n + q)) * 2 : kDrop;
+            __builtin_amdgcn_raw_buffer_store_b16((uint16_t)(r[q / 2] >> (16 * (q & 1))), ro, off, 0, 0);
+          }
+        }
+      }
+    }
+  }
+}
+
 hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_gs,
                        const uint8_t* b_codes, const uint8_t* b_scales, const float* b_gs,
                        const uint16_t* bias, uint16_t* out, int64_t M, int64_t N, int64_t K,
                        hipStream_t stream) {
   if (M == 0 || N == 0) return hipSuccess;
   const int64_t tiles = ((M + kBM - 1) / kBM) * ((N + kBN - 1) / kBN);
-  const dim3 grid((unsigned)tiles), block(kGemmThreads);
-  const bool fast = K % kBK == 0;
+  const dim3 grid((unsigned)tiles);
   const bool vec = N % 8 == 0;
+  if (K % kLBK == 0) {
+    if (vec)
+      hipLaunchKernelGGL((nvfp4_gemm_lane_kernel<true>), grid, dim3(kLThreads), 0, stream, a_codes,
+                         a_scales, a_gs, b_codes, b_scales, b_gs, bias, out, M, N, K);
+    else
+      hipLaunchKernelGGL((nvfp4_gemm_lane_kernel<false>), grid, dim3(kLThreads), 0, stream, a_codes,
+                         a_scales, a_gs, b_codes, b_scales, b_gs, bias, out, M, N, K);
+    return hipGetLastError();
+  }
+  const dim3 block(kGemmThreads);
+  const bool fast = K % kBK == 0;
   if (fast && vec)
     hipLaunchKernelGGL((nvfp4_gemm_kernel<true, true>), grid, block, 0, stream, a_codes, a_scales,
                        a_gs, b_codes, b_scales, b_gs, bias, out, M, N, K);

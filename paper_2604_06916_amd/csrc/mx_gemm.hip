@@ -60,7 +60,6 @@ typedef int v4i_t __attribute__((ext_vector_type(4)));
 typedef int v8i_t __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef float floatx2_t __attribute__((ext_vector_type(2)));
-typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
 // An FP4 matrix operand occupies the low 4 registers of the 8-register
 // operand; the rest are ignored for this format and left undefined.
@@ -72,13 +71,6 @@ __device__ __forceinline__ v8i_t fp4_operand(u32x4_t x) {
 // Two FP32 values to a BF16 pair (round to nearest even), first in the low half.
 __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector((floatx2_t{lo, hi}), bf16x2_t));
-}
-
-// s_waitcnt with vmcnt(V) and lgkmcnt(L) (expcnt not waited on).
-template <int V, int L>
-__device__ __forceinline__ void wait_counts() {
-  static_assert(V >= 0 && V < 64 && L >= 0 && L < 16, "counter range");
-  __builtin_amdgcn_s_waitcnt((V & 15) | ((V >> 4) << 14) | (7 << 4) | (L << 8));
 }
 
 // The 16 scale bytes of one row for stages 4 grp .. 4 grp + 3 (byte 4 j + i

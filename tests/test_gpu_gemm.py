@@ -44,8 +44,11 @@ def test_golden_gemms():
         assert int(got[0, 0]) == c["bf16"], name
 
 
+# K % 128 == 0 runs the lane-dequantizing kernel, any other K the
+# workgroup-shared one; each list covers both.
 @pytest.mark.parametrize("M,N,K", [(1, 1, 16), (3, 5, 32), (37, 70, 64), (300, 260, 48),
-                                   (257, 513, 16), (64, 96, 128)])
+                                   (257, 513, 16), (64, 96, 128), (300, 260, 256),
+                                   (513, 700, 384), (64, 1000, 1280)])
 def test_exact_sums_are_bit_exact(M, N, K):
     """Scales 1.0 and power-of-two alphas: every partial sum is a multiple of
     1/4 below 2^12, exact in FP32, so the only rounding is the final BF16."""
@@ -60,12 +63,13 @@ def test_exact_sums_are_bit_exact(M, N, K):
     assert np.array_equal(got, O.bf16_output(ref))
 
 
-def test_one_hot_weight_returns_activation_columns():
+@pytest.mark.parametrize("K", [272, 384])
+def test_one_hot_weight_returns_activation_columns(K):
     """B row n = code 0x2 (value 1) at k = n: the FP32 sum is the single
     product (s q)_A[m, n], exact, so out[m, n] = bf16(fp32(aA * (s q)_A[m, n]))
     bit for bit (the epilogue rounds alpha * acc + bias to FP32, then to
     BF16); pins nibble order, the [N, K] layout of B, scales and tails."""
-    M, N, K = 300, 200, 272
+    M, N = 300, 200
     ac, as_, aa = quantized("normal", M, K, 3)
     b4 = np.zeros((N, K), np.uint8)
     b4[np.arange(N), np.arange(N)] = 0x2
@@ -81,13 +85,14 @@ def test_one_hot_weight_returns_activation_columns():
     assert np.array_equal(got, want)
 
 
+@pytest.mark.parametrize("K", [272, 384])
 @pytest.mark.parametrize("side", ["A", "B"])
-def test_every_scale_code_bit_exact(side):
+def test_every_scale_code_bit_exact(side, K):
     """One operand cycles its block scales through all 127 finite E4M3 codes
     (subnormals included) with random codes; the other is one-hot (value 1 at
     k = row, scale 1.0).  Each output is a single exact product, so it must
     equal bf16(fp32(alpha * s * q)) bit for bit, on either operand side."""
-    R, K = 300, 272
+    R = 300
     g = np.random.Generator(np.random.PCG64(31 if side == "A" else 32))
     c = g.integers(0, 256, size=(R, K // 2), dtype=np.uint8)
     sc = (np.arange(R * (K // 16)).reshape(R, K // 16) % 0x7F).astype(np.uint8)
@@ -133,7 +138,7 @@ def test_wide_dynamic_range_vs_oracle(kind):
 
 SHAPES = [(1, 1, 16), (5, 7, 32), (64, 64, 128), (255, 257, 48), (300, 520, 272),
           (257, 129, 2240), (128, 1152, 1152), (513, 260, 5600), (96, 300, 3072),
-          (260, 2049, 256)]
+          (260, 2049, 256), (513, 777, 640), (1, 9, 128)]
 
 
 @pytest.mark.parametrize("M,N,K", SHAPES)
