@@ -51,8 +51,8 @@ def parse():
     ap.add_argument("--no-stage1", action="store_true", help="skip the synthetic Stage-1 rollouts")
     ap.add_argument("--no-vendor", action="store_true",
                     help="skip the vendor MXFP4 GEMM reference (it launches mxfp4_gemm once more per layer)")
-    ap.add_argument("--cpu-rows", type=int, default=4096, help="oracle sample: activation rows")
-    ap.add_argument("--cpu-wrows", type=int, default=4096, help="oracle sample: weight rows")
+    ap.add_argument("--cpu-rows", type=int, default=3072, help="oracle sample: activation rows")
+    ap.add_argument("--cpu-wrows", type=int, default=3072, help="oracle sample: weight rows")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="after the benchmark, run a plain device-to-device copy of BYTES "
                          "three times (reference for HBM traffic counters)")
@@ -351,7 +351,8 @@ def run_stage1():
 
 def cpu_baseline(wl, rows, wrows):
     """The CPU oracle on a bounded sample of the same step: per layer, `rows`
-    activation rows and `wrows` weight rows at full K, quantize both and the
+    activation rows and `wrows` weight rows at full K (each clipped to the
+    layer's size), quantize both and the
     float64 GEMM; throughput in the metric's unit (TFLOP/s of 2 m n K)."""
     import numpy as np
     from threadpoolctl import threadpool_info
@@ -360,25 +361,27 @@ def cpu_baseline(wl, rows, wrows):
     from workloads import ROLE_BIAS, ROLE_W, ROLE_X, draw_activations, draw_bias, draw_weights, seed_for
     flops, secs = 0.0, 0.0
     for layer in wl.layers:
+        m, n = min(rows, wl.M), min(wrows, layer.N)
         xb = draw_activations(layer.x_dist, wl.M, layer.K, seed_for(wl.config_id, layer.index, ROLE_X),
-                              row_range=(0, rows))
+                              row_range=(0, m))
         wb = draw_weights(layer.N, layer.K, wl.w_sigma, seed_for(wl.config_id, layer.index, ROLE_W),
-                          row_range=(0, wrows))
-        bias = draw_bias(layer.N, wl.w_sigma, seed_for(wl.config_id, layer.index, ROLE_BIAS))[:wrows]
+                          row_range=(0, n))
+        bias = draw_bias(layer.N, wl.w_sigma, seed_for(wl.config_id, layer.index, ROLE_BIAS))[:n]
         t0 = time.perf_counter()
         wq = O.nvfp4_quantize_ref(wb)
         xq = O.nvfp4_quantize_ref(xb)
         out = O.bf16_output(O.nvfp4_gemm_ref(*xq, *wq, bias))
         secs += time.perf_counter() - t0
-        flops += 2.0 * rows * wb.shape[0] * layer.K
-        assert out.shape == (rows, wb.shape[0])
+        flops += 2.0 * m * n * layer.K
+        assert out.shape == (m, n)
     blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     return {
         "value": flops / secs / 1e12,
         "unit": "TFLOP/s",
         "cores": int(blas_threads),
         "kind": "oracle",
-        "sample": (f"per layer {rows} activation rows x {wrows} weight rows at full K: oracle "
+        "sample": (f"per layer min({rows}, M) activation rows x min({wrows}, N) weight rows at "
+                   f"full K: oracle "
                    f"quantize of both (numpy float32, 1 thread) + float64 GEMM (BLAS, "
                    f"{blas_threads} threads); {secs:.1f} s"),
     }

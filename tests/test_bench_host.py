@@ -26,4 +26,24 @@ def test_cpu_baseline_leg_on_a_tiny_sample():
     cb = bench.cpu_baseline(WORKLOADS["single-1152"], rows=8, wrows=16)
     assert cb["kind"] == "oracle" and cb["unit"] == "TFLOP/s"
     assert cb["value"] > 0 and cb["cores"] >= 1
-    assert "8 activation rows x 16 weight rows" in cb["sample"]
+    assert "min(8, M) activation rows x min(16, N) weight rows" in cb["sample"]
+
+
+def test_cpu_baseline_clips_the_sample_to_the_layer():
+    # a weight sample larger than a layer's N (the default sample against the
+    # 3072-row FLUX out-projection) is clipped, not drawn past the tensor
+    pytest.importorskip("threadpoolctl")
+    sys.path.insert(0, ROOT)
+    import bench
+    from workloads import WORKLOADS
+    cb = bench.cpu_baseline(WORKLOADS["single-1152"], rows=4, wrows=1300)
+    assert cb["value"] > 0
+
+
+def test_row_range_outside_the_tensor_is_rejected():
+    sys.path.insert(0, ROOT)
+    from workloads import draw_activations, draw_weights
+    with pytest.raises(ValueError):
+        draw_weights(300, 32, 0.02, seed=1, row_range=(0, 400))
+    with pytest.raises(ValueError):
+        draw_activations("normal", 300, 32, seed=1, row_range=(10, 5))

@@ -123,6 +123,8 @@ def draw_activations(dist: str, rows: int, K: int, seed: int, row_range=None) ->
     """BF16 bit patterns [rows, K] of the named activation distribution; with
     ``row_range=(r0, r1)`` only those rows of the same tensor."""
     r0, r1 = (0, rows) if row_range is None else row_range
+    if not 0 <= r0 <= r1 <= rows:
+        raise ValueError(f"row_range {(r0, r1)} outside [0, {rows}]")
     n_chunks = max(1, -(-rows // CHUNK_ROWS))
     seeds = np.random.SeedSequence(seed).spawn(n_chunks)
     cols = rng(seed).choice(K, size=min(4, K), replace=False) if dist == "outlier4x20" else None
@@ -146,6 +148,8 @@ def draw_activations(dist: str, rows: int, K: int, seed: int, row_range=None) ->
 def draw_weights(N: int, K: int, sigma: float, seed: int, row_range=None) -> np.ndarray:
     """BF16 bit patterns of an [N, K] weight ~ N(0, sigma^2)."""
     r0, r1 = (0, N) if row_range is None else row_range
+    if not 0 <= r0 <= r1 <= N:
+        raise ValueError(f"row_range {(r0, r1)} outside [0, {N}]")
     n_chunks = max(1, -(-N // CHUNK_ROWS))
     seeds = np.random.SeedSequence(seed).spawn(n_chunks)
     out = np.empty((r1 - r0, K), dtype=np.uint16)
