@@ -505,7 +505,8 @@ def main():
         },
         "roofline": {
             "bound": "mfma",
-            "kernel": "nvfp4_gemm_kernel",
+            "kernel": ("nvfp4_gemm_lane_kernel" if all(L["K"] % 128 == 0 for L in layers)
+                       else "nvfp4_gemm_kernel (and nvfp4_gemm_lane_kernel where K % 128 == 0)"),
             "achieved": round(gemm_tflops, 1),
             "peak": PEAK_FP16_MFMA_TFLOPS,
             "unit": "TFLOP/s",
