@@ -8,8 +8,11 @@ namespace solfp4 {
 
 // First quantize pass: at most this many partial maxima (workspace words).
 constexpr int kMaxPartials = 1024;
-// Encode pass: grid-stride loop over at most this many workgroups.
-constexpr int64_t kEncodeMaxGrid = 8192;
+// Encode pass: grid-stride loop over at most this many workgroups (eight
+// per compute unit: more only adds per-workgroup set-up and an uneven tail).
+constexpr int64_t kEncodeMaxGrid = 2048;
+// MXFP4 quantize: grid-stride loop over at most this many workgroups.
+constexpr int64_t kMxQuantMaxGrid = 8192;
 
 int amax_partial_count(int64_t n_elems);
 

@@ -168,9 +168,12 @@ __global__ __launch_bounds__(kQuantThreads) void nvfp4_encode_kernel(
 }
 
 int amax_partial_count(int64_t n_elems) {
-  // one workgroup per 64 Ki elements, at most kMaxPartials
+  // one workgroup per 64 Ki elements, rounded up to a whole number of
+  // workgroups per compute unit (256 of them) so that every CU streams the
+  // same amount, at most kMaxPartials
   const int64_t per_wg = 64 * 1024;
   int64_t p = (n_elems + per_wg - 1) / per_wg;
+  if (p > 256) p = (p + 255) / 256 * 256;
   if (p < 1) p = 1;
   if (p > kMaxPartials) p = kMaxPartials;
   return (int)p;

@@ -154,8 +154,12 @@ def test_golden_gemm():
         assert int(got[0, 0]) == c["bf16"], name
 
 
+# (4200, 4360, 1024) and (6000, 6152, 1024): more 256 x 256 tiles than the
+# chip has compute units with K % 512 == 0 and N % 8 == 0, so the persistent
+# kernel runs (one and two to three tiles per workgroup, ragged M and N)
 @pytest.mark.parametrize("M,N,K", [(1, 1, 32), (3, 5, 64), (37, 70, 128), (300, 260, 96),
-                                   (257, 513, 32), (64, 96, 512), (260, 300, 1152)])
+                                   (257, 513, 32), (64, 96, 512), (260, 300, 1152),
+                                   (4200, 4360, 1024), (6000, 6152, 1024)])
 def test_exact_sums_are_bit_exact(M, N, K):
     """Scales 2^-2 and 2^3: every partial sum is a multiple of 1/2 below
     2^17, exact in FP32, so the only rounding is the final BF16."""
@@ -195,7 +199,9 @@ def test_every_scale_code_bit_exact(side):
 
 SHAPES = [(1, 1, 32), (5, 7, 64), (64, 64, 128), (255, 257, 96), (300, 520, 288),
           (257, 129, 2240), (128, 1152, 1152), (513, 260, 5600), (96, 300, 3072),
-          (260, 2049, 256), (600, 700, 2432)]
+          (260, 2049, 256), (600, 700, 2432),
+          # persistent kernel (more tiles than compute units, K % 512 == 0)
+          (4200, 4360, 1024), (2100, 9000, 3072)]
 
 
 @pytest.mark.parametrize("M,N,K", SHAPES)
