@@ -22,12 +22,12 @@
 // FP16 subnormals) gives q * s exactly.
 //
 // Two kernels:
-//   nvfp4_gemm_lane_kernel (K % 128 == 0, every model layer): codes travel
+//   nvfp4_gemm_lane_kernel (K % 128 == 0 or K % 64 == 32): codes travel
 //     from HBM into LDS by DMA and each wave dequantizes its own MFMA operands
 //     in registers, so LDS carries 0.5 B/element of codes instead of 2 B of
 //     FP16 per operand read;
-//   nvfp4_gemm_kernel (any K % 16 == 0): the workgroup converts each stage
-//     once into FP16 tiles in LDS, which all waves read.
+//   nvfp4_gemm_kernel (the other K % 16 == 0): the workgroup converts each
+//     stage once into FP16 tiles in LDS, which all waves read.
 #include <type_traits>
 
 #include "device_common.h"
@@ -406,7 +406,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void nvfp4_gemm_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// nvfp4_gemm_lane_kernel: lane-side dequantization, K % 128 == 0.
+// nvfp4_gemm_lane_kernel: lane-side dequantization, K % 32 == 0.
 //
 // Tiling and data movement follow the MXFP4 GEMM: a 256 x 256 output tile
 // per workgroup of 4 waves (one per SIMD), each wave owning 128 x 128 (4 x 4
@@ -458,7 +458,14 @@ __device__ __forceinline__ uint32_t scale_patterns(uint32_t w, bool high_pair) {
   return __builtin_amdgcn_perm(0u, w, high_pair ? 0x0C030C02u : 0x0C010C00u) << 7;
 }
 
-template <bool kVecOut>
+// kFull: K % 128 == 0, every stage lies inside the rows and a stage's 8
+// scale bytes per row are one aligned 8-byte load.  Otherwise (K % 32 == 0)
+// the last stage is partial: its code pieces past K read bytes of the next
+// row (or zeros past the tile), which stay harmless because the scales of
+// those blocks are set to zero (E2M1 codes are all finite, and q * 0 = 0);
+// scale bytes are then fetched as four 2-byte loads (a row's scales start at
+// an even offset only).
+template <bool kVecOut, bool kFull>
 __global__ __launch_bounds__(kLThreads, 1) void nvfp4_gemm_lane_kernel(
     const uint8_t* __restrict__ a_codes, const uint8_t* __restrict__ a_scales,
     const float* __restrict__ a_gs, const uint8_t* __restrict__ b_codes,
@@ -531,6 +538,7 @@ __global__ __launch_bounds__(kLThreads, 1) void nvfp4_gemm_lane_kernel(
     for (int j = 0; j < kLFrags; ++j) acc[i][j] = floatx16_t{};
 
   u32x2_t gsa, gsb;                                  // scale bytes of one stage in flight
+  uint32_t gha[4], ghb[4];                           // the same as 2-byte loads (!kFull)
   uint32_t sca[2][kLFrags][2], scb[2][kLFrags][2];   // [stage parity][frag][half stage]
   u32x4_t ca[2][kLFrags], cb[2][kLFrags];            // code pieces, [half stage][frag]
   half8_t oa[2][kLFrags], ob[2][kLFrags];            // FP16 operands, [K-step parity][frag]
@@ -549,10 +557,34 @@ __global__ __launch_bounds__(kLThreads, 1) void nvfp4_gemm_lane_kernel(
     }
   };
   auto fetch_scales = [&](int stage) {
-    gsa = __builtin_amdgcn_raw_buffer_load_b64(rsa, sg_off + 8 * stage, 0, 0);
-    gsb = __builtin_amdgcn_raw_buffer_load_b64(rsb, sg_off + 8 * stage, 0, 0);
+    const uint32_t off = sg_off + 8 * stage;
+    if (kFull) {
+      gsa = __builtin_amdgcn_raw_buffer_load_b64(rsa, off, 0, 0);
+      gsb = __builtin_amdgcn_raw_buffer_load_b64(rsb, off, 0, 0);
+    } else {
+      // kept as loaded; combined when parked, so nothing waits for them here
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        gha[j] = __builtin_amdgcn_raw_buffer_load_b16(rsa, off + 2 * j, 0, 0);
+        ghb[j] = __builtin_amdgcn_raw_buffer_load_b16(rsb, off + 2 * j, 0, 0);
+      }
+    }
   };
-  auto store_scales = [&](int set) {
+  // scale bytes of `stage` (fetched earlier) into set `set`, as FP16 patterns;
+  // blocks at or past K/16 get scale 0
+  auto store_scales = [&](int set, int stage) {
+    if (!kFull) {
+      gsa = u32x2_t{gha[0] | (gha[1] << 16), gha[2] | (gha[3] << 16)};
+      gsb = u32x2_t{ghb[0] | (ghb[1] << 16), ghb[2] | (ghb[3] << 16)};
+      const int64_t valid = scale_row - 8 * (int64_t)stage;   // blocks of this stage inside K
+      if (valid < 8) {
+        const uint64_t keep = valid <= 0 ? 0ull : (~0ull >> (64 - 8 * valid));
+        gsa.x &= (uint32_t)keep;
+        gsa.y &= (uint32_t)(keep >> 32);
+        gsb.x &= (uint32_t)keep;
+        gsb.y &= (uint32_t)(keep >> 32);
+      }
+    }
     uint32_t* da = &lsc[set][0][t * kLScaleStride];
     uint32_t* db = &lsc[set][1][t * kLScaleStride];
     da[0] = scale_patterns(gsa.x, false);
@@ -622,7 +654,6 @@ __global__ __launch_bounds__(kLThreads, 1) void nvfp4_gemm_lane_kernel(
   using I0 = std::integral_constant<int, 0>;
   using I4 = std::integral_constant<int, 4>;
   using I8 = std::integral_constant<int, 8>;
-  using I10 = std::integral_constant<int, 10>;
   using I12 = std::integral_constant<int, 12>;
   using J0 = std::integral_constant<int, 0>;
   using J1 = std::integral_constant<int, 1>;
@@ -633,21 +664,22 @@ __global__ __launch_bounds__(kLThreads, 1) void nvfp4_gemm_lane_kernel(
   using J6 = std::integral_constant<int, 6>;
   using J7 = std::integral_constant<int, 7>;
 
-  const int nstages = (int)(K / kLBK);
+  const int nstages = (int)((K + kLBK - 1) / kLBK);
+  constexpr int kSL = kFull ? 2 : 8;   // vector-memory instructions of one scale fetch
   // prologue: scales of stages 0 and 1 parked in LDS, stage 2's in
   // registers, codes of stages 0-2 in flight; once stages 0 and 1 have
   // landed, the first half stage's codes and the scales of stage 0 are read
   // and K-step 0 converted.  The second barrier keeps stage 0 from parking
   // stage 2's scales over set 0 before every wave has read it.
   fetch_scales(0);
-  store_scales(0);
+  store_scales(0, 0);
   fetch_scales(1);
-  store_scales(1);
+  store_scales(1, 1);
   dma_stage(0, 0);
   dma_stage(1, 1);
   dma_stage(2, 2);
   fetch_scales(2);
-  wait_counts<10, 0>();
+  wait_counts<8 + kSL, 0>();
   __builtin_amdgcn_s_barrier();
   read_scales(sca[0], scb[0], 0);
   read_codes(0, 0);
@@ -668,12 +700,12 @@ __global__ __launch_bounds__(kLThreads, 1) void nvfp4_gemm_lane_kernel(
     constexpr int C = P & 1;
     __builtin_amdgcn_sched_barrier(0);
     dma_stage((P + 3) % kLBufs, s + 3);
-    store_scales(C);
+    store_scales(C, s + 2);
     fetch_scales(s + 3);
     read_codes(1, P);
     mfma_step(0);
     convert(J1{}, sca[C], scb[C], 1);
-    interleave(I4{}, I10{}, I8{});
+    interleave(I4{}, std::integral_constant<int, 8 + kSL>{}, I8{});
     __builtin_amdgcn_sched_barrier(0);
     mfma_step(1);
     convert(J2{}, sca[C], scb[C], 0);
@@ -706,8 +738,8 @@ __global__ __launch_bounds__(kLThreads, 1) void nvfp4_gemm_lane_kernel(
     interleave(I0{}, I0{}, I0{});
     __builtin_amdgcn_sched_barrier(0);
     // what this wave issued after its DMA of stage s+2 may stay in flight:
-    // this stage's 8 DMA instructions and 2 scale loads
-    wait_counts<10, 0>();
+    // this stage's 8 DMA instructions and its scale loads
+    wait_counts<8 + kSL, 0>();
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
   };
@@ -796,13 +828,20 @@ hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const fl
   const int64_t tiles = ((M + kBM - 1) / kBM) * ((N + kBN - 1) / kBN);
   const dim3 grid((unsigned)tiles);
   const bool vec = N % 8 == 0;
-  if (K % kLBK == 0) {
-    if (vec)
-      hipLaunchKernelGGL((nvfp4_gemm_lane_kernel<true>), grid, dim3(kLThreads), 0, stream, a_codes,
-                         a_scales, a_gs, b_codes, b_scales, b_gs, bias, out, M, N, K);
-    else
-      hipLaunchKernelGGL((nvfp4_gemm_lane_kernel<false>), grid, dim3(kLThreads), 0, stream, a_codes,
-                         a_scales, a_gs, b_codes, b_scales, b_gs, bias, out, M, N, K);
+  // The lane kernel for K % 128 == 0 and for K % 64 == 32; measured on the
+  // 8192-token 2240 -> 6720/2240/5600 layers, the workgroup-shared kernel is
+  // about 5% faster at K % 128 == 64 (K = 2240), while at K = 5600 (where it
+  // must take its unaligned path) the lane kernel is 1.46x faster.
+  if (K % kLBK == 0 || K % 64 == 32) {
+#define SOLFP4_LANE_LAUNCH(V, F)                                                              \
+  hipLaunchKernelGGL((nvfp4_gemm_lane_kernel<V, F>), grid, dim3(kLThreads), 0, stream, a_codes, \
+                     a_scales, a_gs, b_codes, b_scales, b_gs, bias, out, M, N, K)
+    const bool full = K % kLBK == 0;
+    if (vec && full) SOLFP4_LANE_LAUNCH(true, true);
+    else if (full) SOLFP4_LANE_LAUNCH(false, true);
+    else if (vec) SOLFP4_LANE_LAUNCH(true, false);
+    else SOLFP4_LANE_LAUNCH(false, false);
+#undef SOLFP4_LANE_LAUNCH
     return hipGetLastError();
   }
   const dim3 block(kGemmThreads);

@@ -44,11 +44,13 @@ def test_golden_gemms():
         assert int(got[0, 0]) == c["bf16"], name
 
 
-# K % 128 == 0 runs the lane-dequantizing kernel, any other K the
-# workgroup-shared one; each list covers both.
+# K % 128 == 0 and K % 64 == 32 run the lane-dequantizing kernel (the latter
+# with a partial last stage), K % 128 == 64 and K % 32 == 16 the
+# workgroup-shared one; each list covers every case.
 @pytest.mark.parametrize("M,N,K", [(1, 1, 16), (3, 5, 32), (37, 70, 64), (300, 260, 48),
                                    (257, 513, 16), (64, 96, 128), (300, 260, 256),
-                                   (513, 700, 384), (64, 1000, 1280)])
+                                   (513, 700, 384), (64, 1000, 1280), (300, 260, 160),
+                                   (513, 700, 224), (260, 300, 2240)])
 def test_exact_sums_are_bit_exact(M, N, K):
     """Scales 1.0 and power-of-two alphas: every partial sum is a multiple of
     1/4 below 2^12, exact in FP32, so the only rounding is the final BF16."""
@@ -63,7 +65,7 @@ def test_exact_sums_are_bit_exact(M, N, K):
     assert np.array_equal(got, O.bf16_output(ref))
 
 
-@pytest.mark.parametrize("K", [272, 384])
+@pytest.mark.parametrize("K", [224, 272, 384])
 def test_one_hot_weight_returns_activation_columns(K):
     """B row n = code 0x2 (value 1) at k = n: the FP32 sum is the single
     product (s q)_A[m, n], exact, so out[m, n] = bf16(fp32(aA * (s q)_A[m, n]))
@@ -85,7 +87,7 @@ def test_one_hot_weight_returns_activation_columns(K):
     assert np.array_equal(got, want)
 
 
-@pytest.mark.parametrize("K", [272, 384])
+@pytest.mark.parametrize("K", [224, 272, 384])
 @pytest.mark.parametrize("side", ["A", "B"])
 def test_every_scale_code_bit_exact(side, K):
     """One operand cycles its block scales through all 127 finite E4M3 codes
