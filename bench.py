@@ -89,6 +89,12 @@ def measured_traffic(summary, source):
     return float(kv["hbm_bytes_per_launch_avg"])
 
 
+def nvfp4_gemm_kernel_name(K):
+    """The kernel nvfp4_gemm launches for this K (the library's dispatch:
+    lane-side dequantization for K % 128 == 0 and K % 64 == 32)."""
+    return "nvfp4_gemm_lane_kernel" if K % 128 == 0 or K % 64 == 32 else "nvfp4_gemm_kernel"
+
+
 def vendor_mxfp4(layers, bufs, steps):
     """The vendor library's MXFP4 GEMM (torch._scaled_mm on the ROCm stack)
     on the same quantized operands, for reference: its time per layer and
@@ -505,8 +511,7 @@ def main():
         },
         "roofline": {
             "bound": "mfma",
-            "kernel": ("nvfp4_gemm_lane_kernel" if all(L["K"] % 128 == 0 for L in layers)
-                       else "nvfp4_gemm_kernel (and nvfp4_gemm_lane_kernel where K % 128 == 0)"),
+            "kernel": " + ".join(sorted({nvfp4_gemm_kernel_name(L["K"]) for L in layers})),
             "achieved": round(gemm_tflops, 1),
             "peak": PEAK_FP16_MFMA_TFLOPS,
             "unit": "TFLOP/s",
