@@ -51,8 +51,8 @@ def parse():
     ap.add_argument("--no-stage1", action="store_true", help="skip the synthetic Stage-1 rollouts")
     ap.add_argument("--no-vendor", action="store_true",
                     help="skip the vendor MXFP4 GEMM reference (it launches mxfp4_gemm once more per layer)")
-    ap.add_argument("--cpu-rows", type=int, default=4096, help="oracle sample: activation rows")
-    ap.add_argument("--cpu-wrows", type=int, default=4096, help="oracle sample: weight rows")
+    ap.add_argument("--cpu-rows", type=int, default=5120, help="oracle sample: activation rows")
+    ap.add_argument("--cpu-wrows", type=int, default=5120, help="oracle sample: weight rows")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="after the benchmark, run a plain device-to-device copy of BYTES "
                          "three times (reference for HBM traffic counters)")
