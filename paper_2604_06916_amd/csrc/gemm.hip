@@ -528,8 +528,9 @@ __global__ __launch_bounds__(kLThreads, 1) void nvfp4_gemm_lane_kernel(
   const int rs_b = (wn * kLWaveTile + li) * kLScaleStride + g;
 
   // the tile's bias (+0 without one: fma(alpha, acc, +0) == alpha * acc for
-  // every accumulator, which never holds -0)
-  lbias[t] = bias && n0 + t < N ? bias[n0 + t] : (uint16_t)0;
+  // every accumulator, which never holds -0); parked in LDS once the
+  // prologue's loads are out, so its latency overlaps theirs
+  const uint16_t bias_v = bias && n0 + t < N ? bias[n0 + t] : (uint16_t)0;
 
   floatx16_t acc[kLFrags][kLFrags];
 #pragma unroll
@@ -537,8 +538,6 @@ __global__ __launch_bounds__(kLThreads, 1) void nvfp4_gemm_lane_kernel(
 #pragma unroll
     for (int j = 0; j < kLFrags; ++j) acc[i][j] = floatx16_t{};
 
-  u32x2_t gsa, gsb;                                  // scale bytes of one stage in flight
-  uint32_t gha[4], ghb[4];                           // the same as 2-byte loads (!kFull)
   uint32_t sca[2][kLFrags][2], scb[2][kLFrags][2];   // [stage parity][frag][half stage]
   u32x4_t ca[2][kLFrags], cb[2][kLFrags];            // code pieces, [half stage][frag]
   half8_t oa[2][kLFrags], ob[2][kLFrags];            // FP16 operands, [K-step parity][frag]
@@ -556,45 +555,50 @@ __global__ __launch_bounds__(kLThreads, 1) void nvfp4_gemm_lane_kernel(
           rcb, (lds_ptr_t)(bbuf[buf] + (4 * wave + j) * 1024), 16, off, 0, 0, 1);
     }
   };
-  auto fetch_scales = [&](int stage) {
+  // one stage's scale bytes of this thread's A and B rows, in flight
+  struct ScaleFetch {
+    u32x2_t a, b;            // kFull: one 8-byte load each
+    uint32_t ha[4], hb[4];   // otherwise four 2-byte loads each, combined when parked
+  };
+  auto fetch_scales = [&](ScaleFetch& f, int stage) {
     const uint32_t off = sg_off + 8 * stage;
     if (kFull) {
-      gsa = __builtin_amdgcn_raw_buffer_load_b64(rsa, off, 0, 0);
-      gsb = __builtin_amdgcn_raw_buffer_load_b64(rsb, off, 0, 0);
+      f.a = __builtin_amdgcn_raw_buffer_load_b64(rsa, off, 0, 0);
+      f.b = __builtin_amdgcn_raw_buffer_load_b64(rsb, off, 0, 0);
     } else {
-      // kept as loaded; combined when parked, so nothing waits for them here
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        gha[j] = __builtin_amdgcn_raw_buffer_load_b16(rsa, off + 2 * j, 0, 0);
-        ghb[j] = __builtin_amdgcn_raw_buffer_load_b16(rsb, off + 2 * j, 0, 0);
+        f.ha[j] = __builtin_amdgcn_raw_buffer_load_b16(rsa, off + 2 * j, 0, 0);
+        f.hb[j] = __builtin_amdgcn_raw_buffer_load_b16(rsb, off + 2 * j, 0, 0);
       }
     }
   };
-  // scale bytes of `stage` (fetched earlier) into set `set`, as FP16 patterns;
-  // blocks at or past K/16 get scale 0
-  auto store_scales = [&](int set, int stage) {
+  // scale bytes of `stage` (fetched earlier into f) into set `set`, as FP16
+  // patterns; blocks at or past K/16 get scale 0
+  auto store_scales = [&](ScaleFetch& f, int set, int stage) {
+    u32x2_t ga = f.a, gb = f.b;
     if (!kFull) {
-      gsa = u32x2_t{gha[0] | (gha[1] << 16), gha[2] | (gha[3] << 16)};
-      gsb = u32x2_t{ghb[0] | (ghb[1] << 16), ghb[2] | (ghb[3] << 16)};
+      ga = u32x2_t{f.ha[0] | (f.ha[1] << 16), f.ha[2] | (f.ha[3] << 16)};
+      gb = u32x2_t{f.hb[0] | (f.hb[1] << 16), f.hb[2] | (f.hb[3] << 16)};
       const int64_t valid = scale_row - 8 * (int64_t)stage;   // blocks of this stage inside K
       if (valid < 8) {
         const uint64_t keep = valid <= 0 ? 0ull : (~0ull >> (64 - 8 * valid));
-        gsa.x &= (uint32_t)keep;
-        gsa.y &= (uint32_t)(keep >> 32);
-        gsb.x &= (uint32_t)keep;
-        gsb.y &= (uint32_t)(keep >> 32);
+        ga.x &= (uint32_t)keep;
+        ga.y &= (uint32_t)(keep >> 32);
+        gb.x &= (uint32_t)keep;
+        gb.y &= (uint32_t)(keep >> 32);
       }
     }
     uint32_t* da = &lsc[set][0][t * kLScaleStride];
     uint32_t* db = &lsc[set][1][t * kLScaleStride];
-    da[0] = scale_patterns(gsa.x, false);
-    da[1] = scale_patterns(gsa.x, true);
-    da[2] = scale_patterns(gsa.y, false);
-    da[3] = scale_patterns(gsa.y, true);
-    db[0] = scale_patterns(gsb.x, false);
-    db[1] = scale_patterns(gsb.x, true);
-    db[2] = scale_patterns(gsb.y, false);
-    db[3] = scale_patterns(gsb.y, true);
+    da[0] = scale_patterns(ga.x, false);
+    da[1] = scale_patterns(ga.x, true);
+    da[2] = scale_patterns(ga.y, false);
+    da[3] = scale_patterns(ga.y, true);
+    db[0] = scale_patterns(gb.x, false);
+    db[1] = scale_patterns(gb.x, true);
+    db[2] = scale_patterns(gb.y, false);
+    db[3] = scale_patterns(gb.y, true);
   };
   // this lane's scale words of `stage` (its 4 A rows and 4 B rows, both pieces)
   auto read_scales = [&](uint32_t (&da)[kLFrags][2], uint32_t (&db)[kLFrags][2], int stage) {
@@ -666,19 +670,23 @@ __global__ __launch_bounds__(kLThreads, 1) void nvfp4_gemm_lane_kernel(
 
   const int nstages = (int)((K + kLBK - 1) / kLBK);
   constexpr int kSL = kFull ? 2 : 8;   // vector-memory instructions of one scale fetch
-  // prologue: scales of stages 0 and 1 parked in LDS, stage 2's in
-  // registers, codes of stages 0-2 in flight; once stages 0 and 1 have
-  // landed, the first half stage's codes and the scales of stage 0 are read
-  // and K-step 0 converted.  The second barrier keeps stage 0 from parking
-  // stage 2's scales over set 0 before every wave has read it.
-  fetch_scales(0);
-  store_scales(0, 0);
-  fetch_scales(1);
-  store_scales(1, 1);
+  // prologue: the scales of stages 0-2 and the codes of stages 0-2 all go
+  // out first; the scales of stages 0 and 1 are parked in LDS as they land
+  // (each store waits only for its own, older loads), stage 2's stay in
+  // registers; once stages 0 and 1 have landed, the first half stage's codes
+  // and the scales of stage 0 are read and K-step 0 converted.  The second
+  // barrier keeps stage 0 from parking stage 2's scales over set 0 before
+  // every wave has read it.
+  ScaleFetch sf, sf0, sf1;   // sf: the stage in flight during the main loop
+  fetch_scales(sf0, 0);
+  fetch_scales(sf1, 1);
   dma_stage(0, 0);
   dma_stage(1, 1);
   dma_stage(2, 2);
-  fetch_scales(2);
+  fetch_scales(sf, 2);
+  lbias[t] = bias_v;
+  store_scales(sf0, 0, 0);
+  store_scales(sf1, 1, 1);
   wait_counts<8 + kSL, 0>();
   __builtin_amdgcn_s_barrier();
   read_scales(sca[0], scb[0], 0);
@@ -700,8 +708,8 @@ __global__ __launch_bounds__(kLThreads, 1) void nvfp4_gemm_lane_kernel(
     constexpr int C = P & 1;
     __builtin_amdgcn_sched_barrier(0);
     dma_stage((P + 3) % kLBufs, s + 3);
-    store_scales(C, s + 2);
-    fetch_scales(s + 3);
+    store_scales(sf, C, s + 2);
+    fetch_scales(sf, s + 3);
     read_codes(1, P);
     mfma_step(0);
     convert(J1{}, sca[C], scb[C], 1);

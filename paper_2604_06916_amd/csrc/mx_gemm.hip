@@ -169,8 +169,9 @@ __global__ __launch_bounds__(kMxThreads, 1) void mxfp4_gemm_kernel(
   const int rs_b = (wn * kMxWaveTile + li) * kMxScaleStride;
 
   // the tile's bias (+0 without one: the accumulators start at +0 and never
-  // hold -0, so adding +0 changes no result)
-  lbias[t] = bias && n0 + t < N ? bias[n0 + t] : (uint16_t)0;
+  // hold -0, so adding +0 changes no result); parked in LDS once the
+  // prologue's loads are out, so its latency overlaps theirs
+  const uint16_t bias_v = bias && n0 + t < N ? bias[n0 + t] : (uint16_t)0;
 
   floatx16_t acc[kMxFrags][kMxFrags];
 #pragma unroll
@@ -245,6 +246,7 @@ __global__ __launch_bounds__(kMxThreads, 1) void mxfp4_gemm_kernel(
   dma_stage(0, 0);
   dma_stage(1, 1);
   dma_stage(2, 2);
+  lbias[t] = bias_v;
   wait_counts<8, 15>();
   store_group(0);
   wait_counts<8, 0>();
