@@ -47,3 +47,14 @@ def test_row_range_outside_the_tensor_is_rejected():
         draw_weights(300, 32, 0.02, seed=1, row_range=(0, 400))
     with pytest.raises(ValueError):
         draw_activations("normal", 300, 32, seed=1, row_range=(10, 5))
+
+
+def test_paper_context_is_marked_not_comparable():
+    sys.path.insert(0, ROOT)
+    import bench
+    ctx = bench.PAPER_CONTEXT
+    assert ctx["comparable"] is False and "B200" in ctx["hardware"]
+    for model, (naive, ours) in ctx["rollout_s"].items():
+        assert abs(naive / ours - ctx["rollout_speedup"][model]) < 0.01
+    for model, (naive, ours) in ctx["end_to_end_s"].items():
+        assert abs(naive / ours - ctx["end_to_end_speedup"][model]) < 0.01
