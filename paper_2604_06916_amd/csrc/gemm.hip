@@ -408,9 +408,11 @@ __global__ __launch_bounds__(kGemmThreads, 1) void nvfp4_gemm_kernel(
 // ---------------------------------------------------------------------------
 // nvfp4_gemm_lane_kernel: lane-side dequantization, K % 32 == 0.
 //
-// Tiling and data movement follow the MXFP4 GEMM: a 256 x 256 output tile
-// per workgroup of 4 waves (one per SIMD), each wave owning 128 x 128 (4 x 4
-// MFMA tiles of 32 x 32, 256 FP32 accumulators per lane); K advances 128
+// Tiling and data movement follow the MXFP4 GEMM: a 2 kWT x 2 kWT output
+// tile per workgroup of 4 waves (one per SIMD), each wave owning kWT x kWT
+// (kWT = 128: 4 x 4 MFMA tiles of 32 x 32, 256 FP32 accumulators per lane;
+// kWT = 64, for GEMMs with too few 256 x 256 tiles to fill the chip: 2 x 2
+// tiles, a quarter of the work per workgroup); K advances 128
 // elements (64 code bytes per row) per stage; codes go from global memory
 // straight into four LDS stage buffers by DMA, three stages ahead, each lane
 // quad reading the 64 contiguous bytes of one row, stored as [row][piece] x
@@ -425,17 +427,13 @@ __global__ __launch_bounds__(kGemmThreads, 1) void nvfp4_gemm_kernel(
 // of a K-step always sit in one NVFP4 block.  Scales are staged through LDS
 // already as FP16 patterns (s * 2^-8, two blocks per word), so a lane reads
 // the word of its row and piece and a packed multiply with the half selected
-// by op_sel applies the block scale.  Per K-step a wave converts 8 fragments
-// (64 VALU instructions) under 16 MFMAs.
+// by op_sel applies the block scale.  Per K-step a kWT = 128 wave converts 8
+// fragments (64 VALU instructions) under 16 MFMAs.
 
-constexpr int kLTile = 256;                     // output tile edge (M and N)
 constexpr int kLBK = 128;                       // K elements per stage
 constexpr int kLRowBytes = kLBK / 2;            // code bytes per row per stage
 constexpr int kLThreads = 256;
-constexpr int kLWaveTile = 128;
-constexpr int kLFrags = kLWaveTile / 32;        // 32 x 32 MFMA tiles per wave edge
 constexpr int kLBufs = 4;                       // LDS stage buffers (loads run 3 stages ahead)
-constexpr int kLStageBytes = kLTile * kLRowBytes;   // one operand, one stage
 constexpr int kLScaleStride = 5;                // words per row in LDS (4 + 1 pad)
 
 // The 8 elements of one K-step (codes of word w, element j in nibble j)
@@ -465,30 +463,36 @@ __device__ __forceinline__ uint32_t scale_patterns(uint32_t w, bool high_pair) {
 // those blocks are set to zero (E2M1 codes are all finite, and q * 0 = 0);
 // scale bytes are then fetched as four 2-byte loads (a row's scales start at
 // an even offset only).
-template <bool kVecOut, bool kFull>
+template <bool kVecOut, bool kFull, int kWT>
 __global__ __launch_bounds__(kLThreads, 1) void nvfp4_gemm_lane_kernel(
     const uint8_t* __restrict__ a_codes, const uint8_t* __restrict__ a_scales,
     const float* __restrict__ a_gs, const uint8_t* __restrict__ b_codes,
     const uint8_t* __restrict__ b_scales, const float* __restrict__ b_gs,
     const uint16_t* __restrict__ bias, uint16_t* __restrict__ out, int64_t M, int64_t N,
     int64_t K) {
+  static_assert(kWT == 128 || kWT == 64, "wave tile edge");
+  constexpr int kT = 2 * kWT;                // output tile edge (M and N)
+  constexpr int kFr = kWT / 32;              // 32 x 32 MFMA tiles per wave edge
+  constexpr int kStage = kT * kLRowBytes;    // one operand, one stage
+  constexpr int kGw = kT / 64;               // 16-row DMA groups per wave and operand
+  constexpr int kDma = 2 * kGw;              // DMA instructions per wave and stage
   // one array per stage buffer and operand, so the compiler can tell the
   // buffer being filled by DMA from the one being read
-  __shared__ __attribute__((aligned(1024))) uint8_t la0[kLStageBytes], la1[kLStageBytes],
-      la2[kLStageBytes], la3[kLStageBytes];
-  __shared__ __attribute__((aligned(1024))) uint8_t lb0[kLStageBytes], lb1[kLStageBytes],
-      lb2[kLStageBytes], lb3[kLStageBytes];
-  __shared__ uint32_t lsc[2][2][kLTile * kLScaleStride];   // [stage parity][operand][row, word]
-  __shared__ uint16_t lbias[kLTile];
+  __shared__ __attribute__((aligned(1024))) uint8_t la0[kStage], la1[kStage],
+      la2[kStage], la3[kStage];
+  __shared__ __attribute__((aligned(1024))) uint8_t lb0[kStage], lb1[kStage],
+      lb2[kStage], lb3[kStage];
+  __shared__ uint32_t lsc[2][2][kT * kLScaleStride];   // [stage parity][operand][row, word]
+  __shared__ uint16_t lbias[kT];
   uint8_t* const abuf[kLBufs] = {la0, la1, la2, la3};
   uint8_t* const bbuf[kLBufs] = {lb0, lb1, lb2, lb3};
 
-  const int tiles_m = (int)((M + kLTile - 1) / kLTile);
-  const int tiles_n = (int)((N + kLTile - 1) / kLTile);
+  const int tiles_m = (int)((M + kT - 1) / kT);
+  const int tiles_n = (int)((N + kT - 1) / kT);
   int tm, tn;
   tile_coords(tiles_m, tiles_n, tm, tn);
-  const int64_t m0 = (int64_t)tm * kLTile;
-  const int64_t n0 = (int64_t)tn * kLTile;
+  const int64_t m0 = (int64_t)tm * kT;
+  const int64_t n0 = (int64_t)tn * kT;
 
   const int t = threadIdx.x;
   const int lane = t & (kWave - 1);
@@ -500,59 +504,63 @@ __global__ __launch_bounds__(kLThreads, 1) void nvfp4_gemm_lane_kernel(
 
   const int64_t row_bytes = K / 2;
   const int64_t scale_row = K / 16;
-  const int64_t valid_a = min<int64_t>(M - m0, kLTile);
-  const int64_t valid_b = min<int64_t>(N - n0, kLTile);
+  const int64_t valid_a = min<int64_t>(M - m0, kT);
+  const int64_t valid_b = min<int64_t>(N - n0, kT);
   const __amdgpu_buffer_rsrc_t rca = uniform_rsrc(a_codes + m0 * row_bytes, valid_a * row_bytes);
   const __amdgpu_buffer_rsrc_t rcb = uniform_rsrc(b_codes + n0 * row_bytes, valid_b * row_bytes);
   const __amdgpu_buffer_rsrc_t rsa = uniform_rsrc(a_scales + m0 * scale_row, valid_a * scale_row);
   const __amdgpu_buffer_rsrc_t rsb = uniform_rsrc(b_scales + n0 * scale_row, valid_b * scale_row);
 
-  // code DMA: wave w fills 16-row groups 4 w .. 4 w + 3 of each operand; lane
-  // quad l/4 reads the 64 bytes of row l/4 of the group, lane l's 16 bytes
-  // land in slot l of the group's 1 KB
+  // code DMA: wave w fills 16-row groups kGw w .. kGw w + kGw - 1 of each
+  // operand; lane quad l/4 reads the 64 bytes of row l/4 of the group, lane
+  // l's 16 bytes land in slot l of the group's 1 KB
   const int dma_r = lane >> 2;
   const int piece = (lane & 3) ^ ((dma_r >> 2) & 3);
-  const uint32_t dma_off = (uint32_t)((64 * wave + dma_r) * row_bytes + 16 * piece);
+  const uint32_t dma_off = (uint32_t)((16 * kGw * wave + dma_r) * row_bytes + 16 * piece);
   const uint32_t group_stride = (uint32_t)(16 * row_bytes);
   // scale staging: thread t moves the 8 scale bytes of tile row t of A and B
+  // (threads past the tile's rows load zeros out of range and store nothing)
   const uint32_t sg_off = (uint32_t)(t * scale_row);
   // operand slots of this lane: row r of the tile lives in group r / 16 at
   // byte (r % 16) * 64 + 16 * (piece ^ ((r % 16) >> 2)); lane group g reads
   // piece g in K-steps 0-3 and piece 2 + g in K-steps 4-7
   const int swz = ((li & 15) >> 2) & 3;
-  const int rd_a = ((wm * kLWaveTile + li) >> 4) * 1024 + (li & 15) * 64;
-  const int rd_b = ((wn * kLWaveTile + li) >> 4) * 1024 + (li & 15) * 64;
+  const int rd_a = ((wm * kWT + li) >> 4) * 1024 + (li & 15) * 64;
+  const int rd_b = ((wn * kWT + li) >> 4) * 1024 + (li & 15) * 64;
   const int q_off[2] = {16 * (g ^ swz), 16 * ((2 + g) ^ swz)};
   // and its scale words: word p of a row holds the patterns of blocks 2p, 2p+1
-  const int rs_a = (wm * kLWaveTile + li) * kLScaleStride + g;
-  const int rs_b = (wn * kLWaveTile + li) * kLScaleStride + g;
+  const int rs_a = (wm * kWT + li) * kLScaleStride + g;
+  const int rs_b = (wn * kWT + li) * kLScaleStride + g;
 
   // the tile's bias (+0 without one: fma(alpha, acc, +0) == alpha * acc for
   // every accumulator, which never holds -0); parked in LDS once the
   // prologue's loads are out, so its latency overlaps theirs
-  const uint16_t bias_v = bias && n0 + t < N ? bias[n0 + t] : (uint16_t)0;
+  constexpr bool kAllRows = kT == kLThreads;   // every thread stages one tile row
+  const bool row_thread = kAllRows || t < kT;
+  const uint16_t bias_v = bias && row_thread && n0 + t < N ? bias[n0 + t] : (uint16_t)0;
 
-  floatx16_t acc[kLFrags][kLFrags];
+  floatx16_t acc[kFr][kFr];
 #pragma unroll
-  for (int i = 0; i < kLFrags; ++i)
+  for (int i = 0; i < kFr; ++i)
 #pragma unroll
-    for (int j = 0; j < kLFrags; ++j) acc[i][j] = floatx16_t{};
+    for (int j = 0; j < kFr; ++j) acc[i][j] = floatx16_t{};
 
-  uint32_t sca[2][kLFrags][2], scb[2][kLFrags][2];   // [stage parity][frag][half stage]
-  u32x4_t ca[2][kLFrags], cb[2][kLFrags];            // code pieces, [half stage][frag]
-  half8_t oa[2][kLFrags], ob[2][kLFrags];            // FP16 operands, [K-step parity][frag]
+  uint32_t sca[2][kFr][2], scb[2][kFr][2];   // [stage parity][frag][half stage]
+  u32x4_t ca[2][kFr], cb[2][kFr];            // code pieces, [half stage][frag]
+  half8_t oa[2][kFr], ob[2][kFr];            // FP16 operands, [K-step parity][frag]
 
-  // 8 DMA instructions per wave: stage `stage` into buffer `buf`.  Stages
-  // past K read bytes of later rows or zeros into buffers never computed.
+  // kDma DMA instructions per wave: stage `stage` into buffer `buf`.
+  // Stages past K read bytes of later rows or zeros into buffers never
+  // computed.
   auto dma_stage = [&](int buf, int stage) {
     const uint32_t base = dma_off + (uint32_t)stage * kLRowBytes;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < kGw; ++j) {
       const uint32_t off = base + j * group_stride;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(
-          rca, (lds_ptr_t)(abuf[buf] + (4 * wave + j) * 1024), 16, off, 0, 0, 1);
+          rca, (lds_ptr_t)(abuf[buf] + (kGw * wave + j) * 1024), 16, off, 0, 0, 1);
       __builtin_amdgcn_raw_ptr_buffer_load_lds(
-          rcb, (lds_ptr_t)(bbuf[buf] + (4 * wave + j) * 1024), 16, off, 0, 0, 1);
+          rcb, (lds_ptr_t)(bbuf[buf] + (kGw * wave + j) * 1024), 16, off, 0, 0, 1);
     }
   };
   // one stage's scale bytes of this thread's A and B rows, in flight
@@ -589,22 +597,24 @@ __global__ __launch_bounds__(kLThreads, 1) void nvfp4_gemm_lane_kernel(
         gb.y &= (uint32_t)(keep >> 32);
       }
     }
-    uint32_t* da = &lsc[set][0][t * kLScaleStride];
-    uint32_t* db = &lsc[set][1][t * kLScaleStride];
-    da[0] = scale_patterns(ga.x, false);
-    da[1] = scale_patterns(ga.x, true);
-    da[2] = scale_patterns(ga.y, false);
-    da[3] = scale_patterns(ga.y, true);
-    db[0] = scale_patterns(gb.x, false);
-    db[1] = scale_patterns(gb.x, true);
-    db[2] = scale_patterns(gb.y, false);
-    db[3] = scale_patterns(gb.y, true);
+    if (row_thread) {
+      uint32_t* da = &lsc[set][0][t * kLScaleStride];
+      uint32_t* db = &lsc[set][1][t * kLScaleStride];
+      da[0] = scale_patterns(ga.x, false);
+      da[1] = scale_patterns(ga.x, true);
+      da[2] = scale_patterns(ga.y, false);
+      da[3] = scale_patterns(ga.y, true);
+      db[0] = scale_patterns(gb.x, false);
+      db[1] = scale_patterns(gb.x, true);
+      db[2] = scale_patterns(gb.y, false);
+      db[3] = scale_patterns(gb.y, true);
+    }
   };
   // this lane's scale words of `stage` (its 4 A rows and 4 B rows, both pieces)
-  auto read_scales = [&](uint32_t (&da)[kLFrags][2], uint32_t (&db)[kLFrags][2], int stage) {
+  auto read_scales = [&](uint32_t (&da)[kFr][2], uint32_t (&db)[kFr][2], int stage) {
     const int set = stage & 1;
 #pragma unroll
-    for (int f = 0; f < kLFrags; ++f) {
+    for (int f = 0; f < kFr; ++f) {
       da[f][0] = lsc[set][0][rs_a + f * 32 * kLScaleStride];
       da[f][1] = lsc[set][0][rs_a + f * 32 * kLScaleStride + 2];
       db[f][0] = lsc[set][1][rs_b + f * 32 * kLScaleStride];
@@ -613,18 +623,18 @@ __global__ __launch_bounds__(kLThreads, 1) void nvfp4_gemm_lane_kernel(
   };
   auto read_codes = [&](int half, int buf) {
 #pragma unroll
-    for (int f = 0; f < kLFrags; ++f) {
+    for (int f = 0; f < kFr; ++f) {
       ca[half][f] = *reinterpret_cast<const u32x4_t*>(abuf[buf] + rd_a + f * 2048 + q_off[half]);
       cb[half][f] = *reinterpret_cast<const u32x4_t*>(bbuf[buf] + rd_b + f * 2048 + q_off[half]);
     }
   };
   // K-step j of a stage (scale words ss) into operand set d
-  auto convert = [&](auto step, const uint32_t (&ssa)[kLFrags][2],
-                     const uint32_t (&ssb)[kLFrags][2], int d) {
+  auto convert = [&](auto step, const uint32_t (&ssa)[kFr][2],
+                     const uint32_t (&ssb)[kFr][2], int d) {
     constexpr int j = decltype(step)::value;
     constexpr int h = j >> 2, w = j & 3;
 #pragma unroll
-    for (int f = 0; f < kLFrags; ++f) {
+    for (int f = 0; f < kFr; ++f) {
       const half2_t xa = as_h2(ssa[f][h]), xb = as_h2(ssb[f][h]);
       const half2_t sa = (w & 2) ? __builtin_shufflevector(xa, xa, 1, 1) : __builtin_shufflevector(xa, xa, 0, 0);
       const half2_t sb = (w & 2) ? __builtin_shufflevector(xb, xb, 1, 1) : __builtin_shufflevector(xb, xb, 0, 0);
@@ -634,24 +644,26 @@ __global__ __launch_bounds__(kLThreads, 1) void nvfp4_gemm_lane_kernel(
   };
   auto mfma_step = [&](int d) {
 #pragma unroll
-    for (int fn = 0; fn < kLFrags; ++fn)
+    for (int fn = 0; fn < kFr; ++fn)
 #pragma unroll
-      for (int fm = 0; fm < kLFrags; ++fm)
+      for (int fm = 0; fm < kFr; ++fm)
         acc[fn][fm] = __builtin_amdgcn_mfma_f32_32x32x16_f16(ob[d][fn], oa[d][fm], acc[fn][fm], 0, 0, 0);
   };
-  // 16 MFMAs, each followed by up to 4 VALU instructions of the next
-  // K-step's conversion and kR / kV / kW of the step's LDS reads, memory
-  // loads and LDS writes
+  // kFr^2 MFMAs, each followed by up to 16 / kFr VALU instructions of the
+  // next K-step's conversion and a share of the step's kR pairs of LDS
+  // reads, kV memory loads and kW LDS writes (one of each per MFMA for the
+  // 128 x 128 wave tile, four for the 64 x 64 one)
   auto interleave = [&](auto reads, auto vmem, auto writes) {
     constexpr int kR = decltype(reads)::value, kV = decltype(vmem)::value,
                   kW = decltype(writes)::value;
+    constexpr int kPer = 16 / (kFr * kFr);
 #pragma unroll
-    for (int i = 0; i < kLFrags * kLFrags; ++i) {
+    for (int i = 0; i < kFr * kFr; ++i) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                          // MFMA
-      __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);                          // VALU
-      if (i < kR) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);              // DS read
-      if (i < kV) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);              // VMEM read
-      if (i < kW) __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);              // DS write
+      __builtin_amdgcn_sched_group_barrier(0x002, 16 / kFr, 0);                   // VALU
+      if (i * kPer < kR) __builtin_amdgcn_sched_group_barrier(0x100, 2 * kPer, 0);   // DS read
+      if (i * kPer < kV) __builtin_amdgcn_sched_group_barrier(0x020, kPer, 0);       // VMEM read
+      if (i * kPer < kW) __builtin_amdgcn_sched_group_barrier(0x200, kPer, 0);       // DS write
     }
   };
 
@@ -684,10 +696,10 @@ __global__ __launch_bounds__(kLThreads, 1) void nvfp4_gemm_lane_kernel(
   dma_stage(1, 1);
   dma_stage(2, 2);
   fetch_scales(sf, 2);
-  lbias[t] = bias_v;
+  if (row_thread) lbias[t] = bias_v;
   store_scales(sf0, 0, 0);
   store_scales(sf1, 1, 1);
-  wait_counts<8 + kSL, 0>();
+  wait_counts<kDma + kSL, 0>();
   __builtin_amdgcn_s_barrier();
   read_scales(sca[0], scb[0], 0);
   read_codes(0, 0);
@@ -713,7 +725,7 @@ __global__ __launch_bounds__(kLThreads, 1) void nvfp4_gemm_lane_kernel(
     read_codes(1, P);
     mfma_step(0);
     convert(J1{}, sca[C], scb[C], 1);
-    interleave(I4{}, std::integral_constant<int, 8 + kSL>{}, I8{});
+    interleave(I4{}, std::integral_constant<int, kDma + kSL>{}, I8{});
     __builtin_amdgcn_sched_barrier(0);
     mfma_step(1);
     convert(J2{}, sca[C], scb[C], 0);
@@ -746,8 +758,8 @@ __global__ __launch_bounds__(kLThreads, 1) void nvfp4_gemm_lane_kernel(
     interleave(I0{}, I0{}, I0{});
     __builtin_amdgcn_sched_barrier(0);
     // what this wave issued after its DMA of stage s+2 may stay in flight:
-    // this stage's 8 DMA instructions and its scale loads
-    wait_counts<8 + kSL, 0>();
+    // this stage's kDma DMA instructions and its scale loads
+    wait_counts<kDma + kSL, 0>();
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
   };
@@ -783,11 +795,11 @@ __global__ __launch_bounds__(kLThreads, 1) void nvfp4_gemm_lane_kernel(
   const __amdgpu_buffer_rsrc_t ro = uniform_rsrc(out + m0 * N, valid_a * N * 2);
   constexpr uint32_t kDrop = 0x80000000u;   // beyond any output range (N < 2^22)
 #pragma unroll
-  for (int fm = 0; fm < kLFrags; ++fm) {
-    const uint32_t mrow = (uint32_t)((wm * kLWaveTile + fm * 32 + li) * N);
+  for (int fm = 0; fm < kFr; ++fm) {
+    const uint32_t mrow = (uint32_t)((wm * kWT + fm * 32 + li) * N);
 #pragma unroll
-    for (int fn = 0; fn < kLFrags; ++fn) {
-      const int nb = wn * kLWaveTile + fn * 32;
+    for (int fn = 0; fn < kFr; ++fn) {
+      const int nb = wn * kWT + fn * 32;
       float v[16];
 #pragma unroll
       for (int k = 0; k < 4; ++k) {
@@ -828,6 +840,36 @@ __global__ __launch_bounds__(kLThreads, 1) void nvfp4_gemm_lane_kernel(
   }
 }
 
+// Compute units of the current device (256 on MI355X), queried once per
+// device.
+static int device_cus() {
+  constexpr int kMaxDevices = 64;
+  static int cached[kMaxDevices];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 256;
+  int v = __atomic_load_n(&cached[dev], __ATOMIC_RELAXED);
+  if (v <= 0) {
+    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0)
+      v = 256;
+    __atomic_store_n(&cached[dev], v, __ATOMIC_RELAXED);
+  }
+  return v;
+}
+
+// Whether 128 x 128 tiles finish sooner than 256 x 256 ones: one workgroup
+// per CU at a time, so a launch takes about ceil(tiles / CUs) rounds of one
+// tile's time, and a small tile takes kSmallTileCost of a large one's
+// (measured; ideal would be 1/4).
+static bool small_tiles_pay(int64_t tiles256, int64_t tiles128) {
+#ifndef SOLFP4_SMALL_TILE_COST
+#define SOLFP4_SMALL_TILE_COST 0.46
+#endif
+  const int64_t cus = device_cus();
+  const double big = (double)((tiles256 + cus - 1) / cus);
+  const double small = (double)((tiles128 + cus - 1) / cus) * SOLFP4_SMALL_TILE_COST;
+  return small < big;
+}
+
 hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_gs,
                        const uint8_t* b_codes, const uint8_t* b_scales, const float* b_gs,
                        const uint16_t* bias, uint16_t* out, int64_t M, int64_t N, int64_t K,
@@ -841,14 +883,25 @@ hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const fl
   // about 5% faster at K % 128 == 64 (K = 2240), while at K = 5600 (where it
   // must take its unaligned path) the lane kernel is 1.46x faster.
   if (K % kLBK == 0 || K % 64 == 32) {
-#define SOLFP4_LANE_LAUNCH(V, F)                                                              \
-  hipLaunchKernelGGL((nvfp4_gemm_lane_kernel<V, F>), grid, dim3(kLThreads), 0, stream, a_codes, \
-                     a_scales, a_gs, b_codes, b_scales, b_gs, bias, out, M, N, K)
+    const int64_t t256 = ((M + 255) / 256) * ((N + 255) / 256);
+    const int64_t t128 = ((M + 127) / 128) * ((N + 127) / 128);
+    const bool small = small_tiles_pay(t256, t128);
+    const dim3 lgrid((unsigned)(small ? t128 : t256));
+#define SOLFP4_LANE_LAUNCH(V, F, W)                                                           \
+  hipLaunchKernelGGL((nvfp4_gemm_lane_kernel<V, F, W>), lgrid, dim3(kLThreads), 0, stream,     \
+                     a_codes, a_scales, a_gs, b_codes, b_scales, b_gs, bias, out, M, N, K)
     const bool full = K % kLBK == 0;
-    if (vec && full) SOLFP4_LANE_LAUNCH(true, true);
-    else if (full) SOLFP4_LANE_LAUNCH(false, true);
-    else if (vec) SOLFP4_LANE_LAUNCH(true, false);
-    else SOLFP4_LANE_LAUNCH(false, false);
+    if (small) {
+      if (vec && full) SOLFP4_LANE_LAUNCH(true, true, 64);
+      else if (full) SOLFP4_LANE_LAUNCH(false, true, 64);
+      else if (vec) SOLFP4_LANE_LAUNCH(true, false, 64);
+      else SOLFP4_LANE_LAUNCH(false, false, 64);
+    } else {
+      if (vec && full) SOLFP4_LANE_LAUNCH(true, true, 128);
+      else if (full) SOLFP4_LANE_LAUNCH(false, true, 128);
+      else if (vec) SOLFP4_LANE_LAUNCH(true, false, 128);
+      else SOLFP4_LANE_LAUNCH(false, false, 128);
+    }
 #undef SOLFP4_LANE_LAUNCH
     return hipGetLastError();
   }

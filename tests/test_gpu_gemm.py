@@ -46,11 +46,15 @@ def test_golden_gemms():
 
 # K % 128 == 0 and K % 64 == 32 run the lane-dequantizing kernel (the latter
 # with a partial last stage), K % 128 == 64 and K % 32 == 16 the
-# workgroup-shared one; each list covers every case.
+# workgroup-shared one; each list covers every case.  The lane kernel takes
+# 128 x 128 tiles when there are too few 256 x 256 tiles to fill the chip
+# (every small shape here) and 256 x 256 tiles otherwise (5376 x 5376: 441
+# of them).
 @pytest.mark.parametrize("M,N,K", [(1, 1, 16), (3, 5, 32), (37, 70, 64), (300, 260, 48),
                                    (257, 513, 16), (64, 96, 128), (300, 260, 256),
                                    (513, 700, 384), (64, 1000, 1280), (300, 260, 160),
-                                   (513, 700, 224), (260, 300, 2240)])
+                                   (513, 700, 224), (260, 300, 2240), (5376, 5376, 256),
+                                   (5376, 5400, 96)])
 def test_exact_sums_are_bit_exact(M, N, K):
     """Scales 1.0 and power-of-two alphas: every partial sum is a multiple of
     1/4 below 2^12, exact in FP32, so the only rounding is the final BF16."""
@@ -140,7 +144,8 @@ def test_wide_dynamic_range_vs_oracle(kind):
 
 SHAPES = [(1, 1, 16), (5, 7, 32), (64, 64, 128), (255, 257, 48), (300, 520, 272),
           (257, 129, 2240), (128, 1152, 1152), (513, 260, 5600), (96, 300, 3072),
-          (260, 2049, 256), (513, 777, 640), (1, 9, 128)]
+          (260, 2049, 256), (513, 777, 640), (1, 9, 128),
+          (2100, 9000, 3072)]   # 256 x 256 tiles
 
 
 @pytest.mark.parametrize("M,N,K", SHAPES)
