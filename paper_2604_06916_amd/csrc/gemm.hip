@@ -681,25 +681,26 @@ __global__ __launch_bounds__(kLThreads, 1) void nvfp4_gemm_lane_kernel(
   using J7 = std::integral_constant<int, 7>;
 
   const int nstages = (int)((K + kLBK - 1) / kLBK);
-  constexpr int kSL = kFull ? 2 : 8;   // vector-memory instructions of one scale fetch
-  // prologue: the scales of stages 0-2 and the codes of stages 0-2 all go
+  constexpr int kSL = kFull ? 2 : 8;   // vector-memory instructions of one scale fetch (at most)
+  // prologue: the scales of stages 0-2, then the codes of stages 0-2, all go
   // out first; the scales of stages 0 and 1 are parked in LDS as they land
   // (each store waits only for its own, older loads), stage 2's stay in
-  // registers; once stages 0 and 1 have landed, the first half stage's codes
+  // registers; once stages 0 and 1 have landed (only stage 2's DMA, the
+  // youngest loads, may still be in flight), the first half stage's codes
   // and the scales of stage 0 are read and K-step 0 converted.  The second
   // barrier keeps stage 0 from parking stage 2's scales over set 0 before
   // every wave has read it.
   ScaleFetch sf, sf0, sf1;   // sf: the stage in flight during the main loop
   fetch_scales(sf0, 0);
   fetch_scales(sf1, 1);
+  fetch_scales(sf, 2);
   dma_stage(0, 0);
   dma_stage(1, 1);
   dma_stage(2, 2);
-  fetch_scales(sf, 2);
   if (row_thread) lbias[t] = bias_v;
   store_scales(sf0, 0, 0);
   store_scales(sf1, 1, 1);
-  wait_counts<kDma + kSL, 0>();
+  wait_counts<kDma, 0>();
   __builtin_amdgcn_s_barrier();
   read_scales(sca[0], scb[0], 0);
   read_codes(0, 0);
@@ -719,9 +720,12 @@ __global__ __launch_bounds__(kLThreads, 1) void nvfp4_gemm_lane_kernel(
     constexpr int P = decltype(phase)::value;
     constexpr int C = P & 1;
     __builtin_amdgcn_sched_barrier(0);
-    dma_stage((P + 3) % kLBufs, s + 3);
+    // the scale loads go out before the DMA, so the wait that ends the stage
+    // can count the DMA alone (the compiler may merge the scale loads into
+    // fewer instructions than written)
     store_scales(sf, C, s + 2);
     fetch_scales(sf, s + 3);
+    dma_stage((P + 3) % kLBufs, s + 3);
     read_codes(1, P);
     mfma_step(0);
     convert(J1{}, sca[C], scb[C], 1);
@@ -757,9 +761,10 @@ __global__ __launch_bounds__(kLThreads, 1) void nvfp4_gemm_lane_kernel(
     convert(J0{}, sca[C ^ 1], scb[C ^ 1], 0);
     interleave(I0{}, I0{}, I0{});
     __builtin_amdgcn_sched_barrier(0);
-    // what this wave issued after its DMA of stage s+2 may stay in flight:
-    // this stage's kDma DMA instructions and its scale loads
-    wait_counts<kDma + kSL, 0>();
+    // this stage's kDma DMA instructions, the last vector-memory operations
+    // it issued, may stay in flight; everything older (the DMA of stage s+2
+    // and this stage's scale loads) is complete
+    wait_counts<kDma, 0>();
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
   };
@@ -860,7 +865,7 @@ static int device_cus() {
 // per CU at a time, so a launch takes about ceil(tiles / CUs) rounds of one
 // tile's time, and a small tile takes kSmallTileCost of a large one's
 // (measured; ideal would be 1/4).
-static bool small_tiles_pay(int64_t tiles256, int64_t tiles128) {
+bool small_tiles_pay(int64_t tiles256, int64_t tiles128) {
 #ifndef SOLFP4_SMALL_TILE_COST
 #define SOLFP4_SMALL_TILE_COST 0.46
 #endif

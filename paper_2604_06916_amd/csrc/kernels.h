@@ -20,6 +20,10 @@ hipError_t launch_quantize(const uint16_t* x, int64_t rows, int64_t K, uint8_t* 
                            uint8_t* scales, float* global_scale, uint32_t* partial,
                            hipStream_t stream);
 
+// Whether a GEMM should run on 128 x 128 output tiles rather than 256 x 256
+// ones, given the tile counts of both (host only).
+bool small_tiles_pay(int64_t tiles256, int64_t tiles128);
+
 hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_gs,
                        const uint8_t* b_codes, const uint8_t* b_scales, const float* b_gs,
                        const uint16_t* bias, uint16_t* out, int64_t M, int64_t N, int64_t K,

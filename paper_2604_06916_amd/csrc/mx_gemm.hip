@@ -12,8 +12,9 @@
 //
 // Tiling: a 256 x 256 output tile per workgroup of 4 waves (one per SIMD),
 // each wave owning 128 x 128 (4 x 4 MFMA tiles of 32 x 32, 256 FP32
-// accumulators per lane in AGPRs).  K advances 128 elements (64 code bytes
-// per row) per stage.  Codes go from global memory straight into LDS by
+// accumulators per lane in AGPRs); or, for GEMMs with too few such tiles to
+// fill the chip, 128 x 128 tiles with 64 x 64 per wave.  K advances 128
+// elements (64 code bytes per row) per stage.  Codes go from global memory straight into LDS by
 // buffer loads with the LDS-destination bit (no register staging), into four
 // stage buffers: the loads for stage s+3 are issued while stage s computes,
 // so about two stages of time cover their latency.  A DMA instruction puts
@@ -35,7 +36,8 @@
 // s+1 are read during the last K-step of stage s; the barrier that ends
 // stage s first waits for this wave's DMA of stage s+2 (the barrier is a
 // plain s_barrier with explicit counter waits: a release fence would wait
-// for every DMA in flight).
+// for every DMA in flight).  Every wait counts only DMA instructions, which
+// are always the youngest vector-memory operations when it is reached.
 
 #include <type_traits>
 
@@ -44,15 +46,10 @@
 
 namespace solfp4 {
 
-constexpr int kMxTile = 256;                   // output tile edge (M and N)
 constexpr int kMxBK = 128;                     // K elements per stage
 constexpr int kMxRowBytes = kMxBK / 2;         // code bytes per row per stage
 constexpr int kMxThreads = 256;
-constexpr int kMxWaveTile = 128;
-constexpr int kMxFrags = kMxWaveTile / 32;     // 32 x 32 MFMA tiles per wave edge
 constexpr int kMxBufs = 4;                     // LDS stage buffers (loads run 3 stages ahead)
-constexpr int kMxGroups = kMxTile / 16;        // 16-row groups per operand tile
-constexpr int kMxStageBytes = kMxTile * kMxRowBytes;   // one operand, one stage
 constexpr int kMxGroup = 4;                    // stages per scale group (16 scale bytes per row)
 constexpr int kMxScaleStride = 5;              // words per row in LDS (4 + 1 pad: no bank conflicts)
 
@@ -99,32 +96,36 @@ __device__ __forceinline__ u32x4_t load_scale_group(__amdgpu_buffer_rsrc_t src, 
   return u32x4_t{w[0], w[1], w[2], w[3]};
 }
 
-// vector-memory instructions one scale-group fetch issues (both operands)
-constexpr int scale_group_loads(bool fast, bool k512) { return fast ? (k512 ? 2 : 8) : 32; }
 
-template <bool kFast, bool kVecOut, bool kK512>
+template <bool kFast, bool kVecOut, bool kK512, int kWT>
 __global__ __launch_bounds__(kMxThreads, 1) void mxfp4_gemm_kernel(
     const uint8_t* __restrict__ a_codes, const uint8_t* __restrict__ a_scales,
     const uint8_t* __restrict__ b_codes, const uint8_t* __restrict__ b_scales,
     const uint16_t* __restrict__ bias, uint16_t* __restrict__ out, int64_t M, int64_t N,
     int64_t K) {
+  static_assert(kWT == 128 || kWT == 64, "wave tile edge");
+  constexpr int kT = 2 * kWT;                // output tile edge (M and N)
+  constexpr int kFr = kWT / 32;              // 32 x 32 MFMA tiles per wave edge
+  constexpr int kStage = kT * kMxRowBytes;   // one operand, one stage
+  constexpr int kGw = kT / 64;               // 16-row DMA groups per wave and operand
+  constexpr int kDma = 2 * kGw;              // DMA instructions per wave and stage
   // one array per stage buffer and operand, so the compiler can tell the
   // buffer being filled by DMA from the one being read
-  __shared__ __attribute__((aligned(1024))) uint8_t la0[kMxStageBytes], la1[kMxStageBytes],
-      la2[kMxStageBytes], la3[kMxStageBytes];
-  __shared__ __attribute__((aligned(1024))) uint8_t lb0[kMxStageBytes], lb1[kMxStageBytes],
-      lb2[kMxStageBytes], lb3[kMxStageBytes];
-  __shared__ uint32_t lsc[2][2][kMxTile * kMxScaleStride];   // [group parity][operand][row, word]
-  __shared__ uint16_t lbias[kMxTile];
+  __shared__ __attribute__((aligned(1024))) uint8_t la0[kStage], la1[kStage],
+      la2[kStage], la3[kStage];
+  __shared__ __attribute__((aligned(1024))) uint8_t lb0[kStage], lb1[kStage],
+      lb2[kStage], lb3[kStage];
+  __shared__ uint32_t lsc[2][2][kT * kMxScaleStride];   // [group parity][operand][row, word]
+  __shared__ uint16_t lbias[kT];
   uint8_t* const abuf[kMxBufs] = {la0, la1, la2, la3};
   uint8_t* const bbuf[kMxBufs] = {lb0, lb1, lb2, lb3};
 
-  const int tiles_m = (int)((M + kMxTile - 1) / kMxTile);
-  const int tiles_n = (int)((N + kMxTile - 1) / kMxTile);
+  const int tiles_m = (int)((M + kT - 1) / kT);
+  const int tiles_n = (int)((N + kT - 1) / kT);
   int tm, tn;
   tile_coords(tiles_m, tiles_n, tm, tn);
-  const int64_t m0 = (int64_t)tm * kMxTile;
-  const int64_t n0 = (int64_t)tn * kMxTile;
+  const int64_t m0 = (int64_t)tm * kT;
+  const int64_t n0 = (int64_t)tn * kT;
 
   const int t = threadIdx.x;
   const int lane = t & (kWave - 1);
@@ -136,8 +137,8 @@ __global__ __launch_bounds__(kMxThreads, 1) void mxfp4_gemm_kernel(
 
   const int64_t row_bytes = K / 2;
   const int64_t kgroups = K / 32;
-  const int64_t valid_a = min<int64_t>(M - m0, kMxTile);
-  const int64_t valid_b = min<int64_t>(N - n0, kMxTile);
+  const int64_t valid_a = min<int64_t>(M - m0, kT);
+  const int64_t valid_b = min<int64_t>(N - n0, kT);
   const __amdgpu_buffer_rsrc_t rca = uniform_rsrc(a_codes + m0 * row_bytes, valid_a * row_bytes);
   const __amdgpu_buffer_rsrc_t rcb = uniform_rsrc(b_codes + n0 * row_bytes, valid_b * row_bytes);
   const __amdgpu_buffer_rsrc_t rsa = uniform_rsrc(a_scales + m0 * kgroups, valid_a * kgroups);
@@ -152,7 +153,7 @@ __global__ __launch_bounds__(kMxThreads, 1) void mxfp4_gemm_kernel(
   // operand hit all 64 banks once.
   const int dma_r = lane >> 2;
   const int piece = (lane & 3) ^ ((dma_r >> 2) & 3);
-  const uint32_t dma_off = (uint32_t)((64 * wave + dma_r) * row_bytes + 16 * piece);
+  const uint32_t dma_off = (uint32_t)((16 * kGw * wave + dma_r) * row_bytes + 16 * piece);
   const uint32_t group_stride = (uint32_t)(16 * row_bytes);
   constexpr uint32_t kDrop = 0x80000000u;   // beyond any buffer range: loads read zero,
                                             // stores are dropped (N < 2^22, K < 2^24)
@@ -162,38 +163,40 @@ __global__ __launch_bounds__(kMxThreads, 1) void mxfp4_gemm_kernel(
   // at byte (r % 16) * 64 + 16 * (piece ^ ((r % 16) >> 2)); lane (li, g) of
   // K-step st reads piece 2 st + g
   const int swz = ((li & 15) >> 2) & 3;
-  const int rd_a = ((wm * kMxWaveTile + li) >> 4) * 1024 + (li & 15) * 64;
-  const int rd_b = ((wn * kMxWaveTile + li) >> 4) * 1024 + (li & 15) * 64;
+  const int rd_a = ((wm * kWT + li) >> 4) * 1024 + (li & 15) * 64;
+  const int rd_b = ((wn * kWT + li) >> 4) * 1024 + (li & 15) * 64;
   const int q_off[2] = {16 * (g ^ swz), 16 * ((2 + g) ^ swz)};
-  const int rs_a = (wm * kMxWaveTile + li) * kMxScaleStride;
-  const int rs_b = (wn * kMxWaveTile + li) * kMxScaleStride;
+  const int rs_a = (wm * kWT + li) * kMxScaleStride;
+  const int rs_b = (wn * kWT + li) * kMxScaleStride;
 
   // the tile's bias (+0 without one: the accumulators start at +0 and never
   // hold -0, so adding +0 changes no result); parked in LDS once the
   // prologue's loads are out, so its latency overlaps theirs
-  const uint16_t bias_v = bias && n0 + t < N ? bias[n0 + t] : (uint16_t)0;
+  constexpr bool kAllRows = kT == kMxThreads;   // every thread stages one tile row
+  const bool row_thread = kAllRows || t < kT;
+  const uint16_t bias_v = bias && row_thread && n0 + t < N ? bias[n0 + t] : (uint16_t)0;
 
-  floatx16_t acc[kMxFrags][kMxFrags];
+  floatx16_t acc[kFr][kFr];
 #pragma unroll
-  for (int i = 0; i < kMxFrags; ++i)
+  for (int i = 0; i < kFr; ++i)
 #pragma unroll
-    for (int j = 0; j < kMxFrags; ++j) acc[i][j] = floatx16_t{};
+    for (int j = 0; j < kFr; ++j) acc[i][j] = floatx16_t{};
 
   u32x4_t gsa, gsb;                      // scale group in flight
-  uint32_t sca[2][kMxFrags], scb[2][kMxFrags];
-  u32x4_t fa[2][kMxFrags], fb[2][kMxFrags];
+  uint32_t sca[2][kFr], scb[2][kFr];
+  u32x4_t fa[2][kFr], fb[2][kFr];
 
   // 8 DMA instructions per wave: stage `stage` into buffer `buf`
   auto dma_stage = [&](int buf, int stage) {
     const bool ok = kFast || (int64_t)stage * kMxBK + 32 * piece < K;
     const uint32_t base = dma_off + (uint32_t)stage * kMxRowBytes;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < kGw; ++j) {
       const uint32_t off = ok ? base + j * group_stride : kDrop;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(
-          rca, (lds_ptr_t)(abuf[buf] + (4 * wave + j) * 1024), 16, off, 0, 0, 1);
+          rca, (lds_ptr_t)(abuf[buf] + (kGw * wave + j) * 1024), 16, off, 0, 0, 1);
       __builtin_amdgcn_raw_ptr_buffer_load_lds(
-          rcb, (lds_ptr_t)(bbuf[buf] + (4 * wave + j) * 1024), 16, off, 0, 0, 1);
+          rcb, (lds_ptr_t)(bbuf[buf] + (kGw * wave + j) * 1024), 16, off, 0, 0, 1);
     }
   };
   auto load_group = [&](int grp) {
@@ -201,23 +204,25 @@ __global__ __launch_bounds__(kMxThreads, 1) void mxfp4_gemm_kernel(
     gsb = load_scale_group<kFast, kK512>(rsb, sg_off + 16 * grp, kgroups, grp);
   };
   auto store_group = [&](int set) {
-    uint32_t* da = &lsc[set][0][t * kMxScaleStride];
-    uint32_t* db = &lsc[set][1][t * kMxScaleStride];
-    da[0] = gsa.x; da[1] = gsa.y; da[2] = gsa.z; da[3] = gsa.w;
-    db[0] = gsb.x; db[1] = gsb.y; db[2] = gsb.z; db[3] = gsb.w;
+    if (row_thread) {
+      uint32_t* da = &lsc[set][0][t * kMxScaleStride];
+      uint32_t* db = &lsc[set][1][t * kMxScaleStride];
+      da[0] = gsa.x; da[1] = gsa.y; da[2] = gsa.z; da[3] = gsa.w;
+      db[0] = gsb.x; db[1] = gsb.y; db[2] = gsb.z; db[3] = gsb.w;
+    }
   };
   // this lane's scale words of `stage` (its 4 A rows and 4 B rows)
-  auto read_scales = [&](uint32_t (&da)[kMxFrags], uint32_t (&db)[kMxFrags], int stage) {
+  auto read_scales = [&](uint32_t (&da)[kFr], uint32_t (&db)[kFr], int stage) {
     const int set = (stage / kMxGroup) & 1, w = stage % kMxGroup;
 #pragma unroll
-    for (int f = 0; f < kMxFrags; ++f) {
+    for (int f = 0; f < kFr; ++f) {
       da[f] = lsc[set][0][rs_a + f * 32 * kMxScaleStride + w];
       db[f] = lsc[set][1][rs_b + f * 32 * kMxScaleStride + w];
     }
   };
-  auto read_frags = [&](u32x4_t (&da)[kMxFrags], u32x4_t (&db)[kMxFrags], int buf, int st) {
+  auto read_frags = [&](u32x4_t (&da)[kFr], u32x4_t (&db)[kFr], int buf, int st) {
 #pragma unroll
-    for (int f = 0; f < kMxFrags; ++f) {
+    for (int f = 0; f < kFr; ++f) {
       da[f] = *reinterpret_cast<const u32x4_t*>(abuf[buf] + rd_a + f * 2048 + q_off[st]);
       db[f] = *reinterpret_cast<const u32x4_t*>(bbuf[buf] + rd_b + f * 2048 + q_off[st]);
     }
@@ -225,19 +230,18 @@ __global__ __launch_bounds__(kMxThreads, 1) void mxfp4_gemm_kernel(
   // one K-step: lane group g supplies kgroup 2 st + g of the stage, i.e.
   // byte 2 st + g of its scale words; after the shift by 8 g the byte
   // select is the constant 2 st for every lane
-  auto mfma_step = [&](auto step, const u32x4_t (&xa)[kMxFrags], const u32x4_t (&xb)[kMxFrags],
-                       const uint32_t (&ssa)[kMxFrags], const uint32_t (&ssb)[kMxFrags]) {
+  auto mfma_step = [&](auto step, const u32x4_t (&xa)[kFr], const u32x4_t (&xb)[kFr],
+                       const uint32_t (&ssa)[kFr], const uint32_t (&ssb)[kFr]) {
     constexpr int st = decltype(step)::value;
 #pragma unroll
-    for (int fn = 0; fn < kMxFrags; ++fn)
+    for (int fn = 0; fn < kFr; ++fn)
 #pragma unroll
-      for (int fm = 0; fm < kMxFrags; ++fm)
+      for (int fm = 0; fm < kFr; ++fm)
         acc[fn][fm] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
             fp4_operand(xb[fn]), fp4_operand(xa[fm]), acc[fn][fm], 4, 4, 2 * st,
             (int)ssb[fn], 2 * st, (int)ssa[fm]);
   };
 
-  constexpr int kSL = scale_group_loads(kFast, kK512);
   const int nstages = (int)((K + kMxBK - 1) / kMxBK);
   // prologue: scale group 0, stages 0-2 in flight; once stages 0 and 1 have
   // landed (stage 2 may still be in flight) the scales are parked and the
@@ -246,10 +250,10 @@ __global__ __launch_bounds__(kMxThreads, 1) void mxfp4_gemm_kernel(
   dma_stage(0, 0);
   dma_stage(1, 1);
   dma_stage(2, 2);
-  lbias[t] = bias_v;
-  wait_counts<8, 15>();
+  if (row_thread) lbias[t] = bias_v;
+  wait_counts<kDma, 15>();
   store_group(0);
-  wait_counts<8, 0>();
+  wait_counts<kDma, 0>();
   __builtin_amdgcn_s_barrier();
   read_scales(sca[0], scb[0], 0);
   read_frags(fa[0], fb[0], 0, 0);
@@ -267,25 +271,40 @@ __global__ __launch_bounds__(kMxThreads, 1) void mxfp4_gemm_kernel(
   auto run_stage = [&](auto phase, int s) {
     constexpr int P = decltype(phase)::value;
     constexpr int C = P & 1;               // scale-word register set of stage s
-    uint32_t ssa[kMxFrags], ssb[kMxFrags];
+    uint32_t ssa[kFr], ssb[kFr];
 #pragma unroll
-    for (int f = 0; f < kMxFrags; ++f) {
+    for (int f = 0; f < kFr; ++f) {
       ssa[f] = sca[C][f] >> (8 * g);
       ssb[f] = scb[C][f] >> (8 * g);
     }
     __builtin_amdgcn_sched_barrier(0);
-    // K-step 0
-    dma_stage((P + 3) % kMxBufs, s + 3);
+    // K-step 0: the scale group goes out before the DMA, so the wait that
+    // ends the stage can count the DMA alone (the compiler may merge the
+    // scale loads into fewer instructions than written: counting them would
+    // let older DMA still be in flight)
     if (P == 0) load_group(s / kMxGroup + 1);
+    dma_stage((P + 3) % kMxBufs, s + 3);
     read_frags(fa[1], fb[1], P, 1);
     mfma_step(S0{}, fa[0], fb[0], ssa, ssb);
     if (P == 2) store_group((s / kMxGroup + 1) & 1);
+    if constexpr (kFr == 4) {
 #pragma unroll
-    for (int i = 0; i < kMxFrags * kMxFrags; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                 // MFMA
-      if (i < 8) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);      // DS read
-      __builtin_amdgcn_sched_group_barrier(0x020, P == 0 ? 3 : 1, 0);    // VMEM read
-      if (P == 2 && i >= 8) __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);   // DS write
+      for (int i = 0; i < kFr * kFr; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                 // MFMA
+        if (i < 8) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);      // DS read
+        __builtin_amdgcn_sched_group_barrier(0x020, P == 0 ? 3 : 1, 0);    // VMEM read
+        if (P == 2 && i >= 8) __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);   // DS write
+      }
+    } else {
+      // 4 MFMAs share the step's 4 LDS reads, kDma (+ scale) loads and the
+      // 8 scale stores
+#pragma unroll
+      for (int i = 0; i < kFr * kFr; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x020, P == 0 ? 4 : 1, 0);
+        if (P == 2) __builtin_amdgcn_sched_group_barrier(0x200, 2, 0);
+      }
     }
     __builtin_amdgcn_sched_barrier(0);
     // K-step 1, with the scales and operands of the next stage's first K-step
@@ -293,15 +312,15 @@ __global__ __launch_bounds__(kMxThreads, 1) void mxfp4_gemm_kernel(
     read_frags(fa[0], fb[0], (P + 1) % kMxBufs, 0);
     mfma_step(S1{}, fa[1], fb[1], ssa, ssb);
 #pragma unroll
-    for (int i = 0; i < kMxFrags * kMxFrags; ++i) {
+    for (int i = 0; i < kFr * kFr; ++i) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 16 / (kFr * kFr), 0);
     }
     __builtin_amdgcn_sched_barrier(0);
-    // what this wave issued after its DMA of stage s+2 may stay in flight:
-    // at least this stage's 8 DMA instructions, plus at P == 0 the scale
-    // loads issued in this stage (never more than is certainly younger)
-    wait_counts<8 + (P == 0 ? kSL : 0), 0>();
+    // this stage's kDma DMA instructions, the last vector-memory operations
+    // it issued, may stay in flight; everything older (the DMA of stage s+2
+    // and any scale loads) is complete
+    wait_counts<kDma, 0>();
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
   };
@@ -334,11 +353,11 @@ __global__ __launch_bounds__(kMxThreads, 1) void mxfp4_gemm_kernel(
   // the hardware range check; columns past N get an offset beyond the range.
   const __amdgpu_buffer_rsrc_t ro = uniform_rsrc(out + m0 * N, valid_a * N * 2);
 #pragma unroll
-  for (int fm = 0; fm < kMxFrags; ++fm) {
-    const uint32_t mrow = (uint32_t)((wm * kMxWaveTile + fm * 32 + li) * N);
+  for (int fm = 0; fm < kFr; ++fm) {
+    const uint32_t mrow = (uint32_t)((wm * kWT + fm * 32 + li) * N);
 #pragma unroll
-    for (int fn = 0; fn < kMxFrags; ++fn) {
-      const int nb = wn * kMxWaveTile + fn * 32;
+    for (int fn = 0; fn < kFr; ++fn) {
+      const int nb = wn * kWT + fn * 32;
       float v[16];
 #pragma unroll
       for (int q = 0; q < 16; ++q) v[q] = acc[fn][fm][q];
@@ -385,14 +404,22 @@ hipError_t launch_mx_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const
                           const uint8_t* b_scales, const uint16_t* bias, uint16_t* out, int64_t M,
                           int64_t N, int64_t K, hipStream_t stream) {
   if (M == 0 || N == 0) return hipSuccess;
-  const int64_t tiles = ((M + kMxTile - 1) / kMxTile) * ((N + kMxTile - 1) / kMxTile);
-  const dim3 grid((unsigned)tiles), block(kMxThreads);
+  const int64_t t256 = ((M + 255) / 256) * ((N + 255) / 256);
+  const int64_t t128 = ((M + 127) / 128) * ((N + 127) / 128);
+  const bool small = small_tiles_pay(t256, t128);
+  const dim3 grid((unsigned)(small ? t128 : t256)), block(kMxThreads);
   const bool fast = K % kMxBK == 0;
   const bool k512 = K % 512 == 0;
   const bool vec = N % 8 == 0;
-#define SOLFP4_MX_LAUNCH(F, V, W)                                                           \
-  hipLaunchKernelGGL((mxfp4_gemm_kernel<F, V, W>), grid, block, 0, stream, a_codes, a_scales, \
-                     b_codes, b_scales, bias, out, M, N, K)
+#define SOLFP4_MX_LAUNCH(F, V, W)                                                              \
+  do {                                                                                         \
+    if (small)                                                                                 \
+      hipLaunchKernelGGL((mxfp4_gemm_kernel<F, V, W, 64>), grid, block, 0, stream, a_codes,   \
+                         a_scales, b_codes, b_scales, bias, out, M, N, K);                     \
+    else                                                                                       \
+      hipLaunchKernelGGL((mxfp4_gemm_kernel<F, V, W, 128>), grid, block, 0, stream, a_codes,  \
+                         a_scales, b_codes, b_scales, bias, out, M, N, K);                     \
+  } while (0)
   if (fast && k512) {
     if (vec) SOLFP4_MX_LAUNCH(true, true, true);
     else SOLFP4_MX_LAUNCH(true, false, true);

@@ -54,7 +54,7 @@ def test_golden_gemms():
                                    (257, 513, 16), (64, 96, 128), (300, 260, 256),
                                    (513, 700, 384), (64, 1000, 1280), (300, 260, 160),
                                    (513, 700, 224), (260, 300, 2240), (5376, 5376, 256),
-                                   (5376, 5400, 96)])
+                                   (5376, 5400, 96), (4200, 4360, 1120)])
 def test_exact_sums_are_bit_exact(M, N, K):
     """Scales 1.0 and power-of-two alphas: every partial sum is a multiple of
     1/4 below 2^12, exact in FP32, so the only rounding is the final BF16."""
