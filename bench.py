@@ -226,7 +226,8 @@ def run_graphs(layers, reps):
     def linears():
         for L in layers:
             sol.nvfp4_quantize(L["x"], L["xc"], L["xs"], L["xa"], L["qws"])
-            sol.nvfp4_gemm(L["xc"], L["xs"], L["xa"], L["wc"], L["ws"], L["wa"], L["b"], L["out"])
+            sol.nvfp4_gemm(L["xc"], L["xs"], L["xa"], L["wc"], L["ws"], L["wa"], L["b"], L["out"],
+                           L["gws"])
 
     def timed(fn):
         fn()
@@ -278,7 +279,7 @@ def run_small_linear(reps):
     b = to_dev(draw_bias(N, wl.w_sigma, seed_for(wl.config_id, layer.index, ROLE_BIAS)))
     wc, ws, wa = sol.nvfp4_quantize(w)
     out = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
-    lws = torch.empty(sol.nvfp4_linear_workspace_bytes(M, K), dtype=torch.uint8, device=dev)
+    lws = torch.empty(sol.nvfp4_linear_workspace_bytes(M, N, K), dtype=torch.uint8, device=dev)
     batch = 50
 
     def lin():
@@ -445,6 +446,8 @@ def main():
             xa=torch.empty(1, dtype=torch.float32, device=dev),
             qws=torch.empty(max(sol.nvfp4_quantize_workspace_bytes(max(M, N), K), 256),
                             dtype=torch.uint8, device=dev),
+            gws=(torch.empty(sol.nvfp4_gemm_workspace_bytes(M, N, K), dtype=torch.uint8, device=dev)
+                 if sol.nvfp4_gemm_workspace_bytes(M, N, K) else None),
             out=torch.empty((M, N), dtype=torch.bfloat16, device=dev),
             M=M, N=N, K=K, name=layer.name)
         layers.append(buf)
@@ -461,7 +464,8 @@ def main():
             sol.nvfp4_quantize(L["x"], L["xc"], L["xs"], L["xa"], L["qws"])
             if e:
                 e[2].record()
-            sol.nvfp4_gemm(L["xc"], L["xs"], L["xa"], L["wc"], L["ws"], L["wa"], L["b"], L["out"])
+            sol.nvfp4_gemm(L["xc"], L["xs"], L["xa"], L["wc"], L["ws"], L["wa"], L["b"], L["out"],
+                           L["gws"])
             if e:
                 e[3].record()
 

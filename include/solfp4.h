@@ -12,15 +12,17 @@
  * --------------------------------
  * - All data pointers are DEVICE pointers (HIP global memory) owned by the
  *   caller; the library allocates and frees nothing and keeps no state
- *   between calls.
+ *   between calls (workspaces are scratch for the duration of one call).
  * - `stream` is a hipStream_t passed as void* (NULL = the null stream).
  *   Calls only enqueue work and return; nothing synchronises the host.
  * - Matrices are row-major and contiguous.  BF16 values travel as their
  *   uint16_t bit patterns.  K, the reduction length, must be a multiple of
  *   16 (one NVFP4 block).
  * - Every pointer must be 16-byte aligned.
- * - Argument errors are detected on the host and returned BEFORE any HIP
- *   call, so they are safe to provoke on a machine without a GPU.  Non-finite
+ * - Argument errors are detected on the host and returned BEFORE any kernel
+ *   launch (the only HIP calls before that are device-attribute queries,
+ *   which fall back to MI355X's values without a GPU), so they are safe to
+ *   provoke on a machine without one.  Non-finite
  *   inputs (NaN, Inf) give unspecified codes but never fault.
  * - Return value: SOLFP4_OK (0) or one of the negative status codes below.
  *   Nothing throws across this boundary.
@@ -119,13 +121,38 @@ SOLFP4_API int nvfp4_quantize(const uint16_t* x, int64_t rows, int64_t K,
  */
 SOLFP4_API int nvfp4_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_global_scale,
                const uint8_t* b_codes, const uint8_t* b_scales, const float* b_global_scale,
-               const uint16_t* bias, uint16_t* out,
+               const uint16_t* bias, uint16_t* out, void* workspace, size_t workspace_bytes,
                int64_t M, int64_t N, int64_t K, void* stream);
 
+/*
+ * Device workspace, in bytes, that nvfp4_gemm uses for an M x N x K product
+ * on the current device (host only; 0 for invalid sizes).  The GEMM runs
+ * one workgroup per 256 x 256 output tile, about ceil(tiles / CUs) rounds
+ * of one tile's time; when the last round holds few tiles, each of those is
+ * computed as two K halves by two workgroups, which add their FP32 partial
+ * sums through this workspace (one 256 KB partial tile per half, plus an
+ * 8-byte slot per tile that tells the second half to finish that it is
+ * second).  0 means the shape runs without it.
+ *
+ * nvfp4_gemm's workspace argument:
+ *   NULL       no split (workspace_bytes is ignored)
+ *   otherwise  16-byte aligned, at least nvfp4_gemm_workspace_bytes(M, N, K)
+ *              bytes, else SOLFP4_EWORKSPACE; its contents on entry are
+ *              ignored and undefined on return (it is scratch).  Calls that
+ *              may run at the same time must not share one.
+ * The split changes the order of the FP32 summation for the affected tiles
+ * (two partial sums added once), so outputs with and without a workspace
+ * may differ in their last bits; for a given choice results are
+ * deterministic (the two halves are added by one commutative addition,
+ * whichever finishes last).
+ */
+SOLFP4_API size_t nvfp4_gemm_workspace_bytes(int64_t M, int64_t N, int64_t K);
+
 /* Device workspace, in bytes, that nvfp4_linear needs for [M, K]
- * activations (their NVFP4 codes, scales, alpha and the quantizer's
- * scratch).  Host only; 0 for invalid sizes. */
-SOLFP4_API size_t nvfp4_linear_workspace_bytes(int64_t M, int64_t K);
+ * activations times an [N, K] weight: the activations' NVFP4 codes,
+ * scales and alpha, the quantizer's scratch, then nvfp4_gemm's workspace.
+ * Host only; 0 for invalid sizes. */
+SOLFP4_API size_t nvfp4_linear_workspace_bytes(int64_t M, int64_t N, int64_t K);
 
 /*
  * The NVFP4 linear layer of the denoiser (Sec. 4.1: the model's linears run
@@ -138,7 +165,7 @@ SOLFP4_API size_t nvfp4_linear_workspace_bytes(int64_t M, int64_t K);
  *            (the weight quantized with nvfp4_quantize)
  *   bias     [N] BF16 or NULL
  *   out      [M][N] BF16
- *   workspace >= nvfp4_linear_workspace_bytes(M, K) bytes; on return it
+ *   workspace >= nvfp4_linear_workspace_bytes(M, N, K) bytes; on return it
  *            holds the activation codes at offset 0, then their scales and
  *            alpha (offsets are an implementation detail).
  *

@@ -31,9 +31,11 @@ lib.nvfp4_quantize_workspace_bytes.argtypes = [_i64, _i64]
 lib.nvfp4_quantize.restype = ctypes.c_int
 lib.nvfp4_quantize.argtypes = [_p, _i64, _i64, _p, _p, _p, _p, _sz, _p]
 lib.nvfp4_gemm.restype = ctypes.c_int
-lib.nvfp4_gemm.argtypes = [_p, _p, _p, _p, _p, _p, _p, _p, _i64, _i64, _i64, _p]
+lib.nvfp4_gemm.argtypes = [_p, _p, _p, _p, _p, _p, _p, _p, _p, _sz, _i64, _i64, _i64, _p]
+lib.nvfp4_gemm_workspace_bytes.restype = _sz
+lib.nvfp4_gemm_workspace_bytes.argtypes = [_i64, _i64, _i64]
 lib.nvfp4_linear_workspace_bytes.restype = _sz
-lib.nvfp4_linear_workspace_bytes.argtypes = [_i64, _i64]
+lib.nvfp4_linear_workspace_bytes.argtypes = [_i64, _i64, _i64]
 lib.nvfp4_linear.restype = ctypes.c_int
 lib.nvfp4_linear.argtypes = [_p, _p, _p, _p, _p, _p, _p, _sz, _i64, _i64, _i64, _p]
 
@@ -47,7 +49,8 @@ lib.mxfp4_linear.restype = ctypes.c_int
 lib.mxfp4_linear.argtypes = [_p, _p, _p, _p, _p, _p, _sz, _i64, _i64, _i64, _p]
 
 EXPORTED = ["solfp4_strerror", "solfp4_version", "nvfp4_quantize_workspace_bytes",
-            "nvfp4_quantize", "nvfp4_gemm", "nvfp4_linear_workspace_bytes", "nvfp4_linear",
+            "nvfp4_quantize", "nvfp4_gemm", "nvfp4_gemm_workspace_bytes",
+            "nvfp4_linear_workspace_bytes", "nvfp4_linear",
             "mxfp4_quantize", "mxfp4_gemm", "mxfp4_linear_workspace_bytes", "mxfp4_linear"]
 
 
@@ -82,8 +85,12 @@ def nvfp4_quantize_workspace_bytes(rows: int, K: int) -> int:
     return lib.nvfp4_quantize_workspace_bytes(rows, K)
 
 
-def nvfp4_linear_workspace_bytes(M: int, K: int) -> int:
-    return lib.nvfp4_linear_workspace_bytes(M, K)
+def nvfp4_gemm_workspace_bytes(M: int, N: int, K: int) -> int:
+    return lib.nvfp4_gemm_workspace_bytes(M, N, K)
+
+
+def nvfp4_linear_workspace_bytes(M: int, N: int, K: int) -> int:
+    return lib.nvfp4_linear_workspace_bytes(M, N, K)
 
 
 def nvfp4_quantize(x, codes=None, scales=None, global_scale=None, workspace=None, stream=None):
@@ -107,8 +114,11 @@ def nvfp4_quantize(x, codes=None, scales=None, global_scale=None, workspace=None
 
 
 def nvfp4_gemm(a_codes, a_scales, a_global_scale, b_codes, b_scales, b_global_scale,
-               bias=None, out=None, stream=None):
-    """Block-scaled NVFP4 GEMM: A [M, K] (packed), B [N, K] (packed) -> BF16 [M, N]."""
+               bias=None, out=None, workspace=None, stream=None, split=True):
+    """Block-scaled NVFP4 GEMM: A [M, K] (packed), B [N, K] (packed) -> BF16 [M, N].
+    `workspace` (uint8, at least nvfp4_gemm_workspace_bytes(M, N, K)) is
+    allocated when needed and not given; split=False passes none (no split
+    of the last round's tiles)."""
     M, N = a_codes.shape[0], b_codes.shape[0]
     K = a_codes.shape[1] * 2
     if b_codes.shape[1] * 2 != K:
@@ -118,8 +128,15 @@ def nvfp4_gemm(a_codes, a_scales, a_global_scale, b_codes, b_scales, b_global_sc
     _need(out, torch.bfloat16, (M, N), "out")
     if bias is not None:
         _need(bias, torch.bfloat16, (N,), "bias")
+    if not split:
+        workspace = None
+    elif workspace is None:
+        need = nvfp4_gemm_workspace_bytes(M, N, K)
+        if need:
+            workspace = torch.empty(need, dtype=torch.uint8, device=a_codes.device)
     _check(lib.nvfp4_gemm(_ptr(a_codes), _ptr(a_scales), _ptr(a_global_scale), _ptr(b_codes),
                           _ptr(b_scales), _ptr(b_global_scale), _ptr(bias), _ptr(out),
+                          _ptr(workspace), 0 if workspace is None else workspace.numel(),
                           M, N, K, _stream(stream)))
     return out
 
@@ -137,7 +154,7 @@ def nvfp4_linear(x, w_codes, w_scales, w_global_scale, bias=None, out=None, work
     if bias is not None:
         _need(bias, torch.bfloat16, (N,), "bias")
     if workspace is None:
-        workspace = torch.empty(nvfp4_linear_workspace_bytes(M, K), dtype=torch.uint8,
+        workspace = torch.empty(nvfp4_linear_workspace_bytes(M, N, K), dtype=torch.uint8,
                                 device=x.device)
     _check(lib.nvfp4_linear(_ptr(x), _ptr(w_codes), _ptr(w_scales), _ptr(w_global_scale),
                             _ptr(bias), _ptr(out), _ptr(workspace), workspace.numel(),

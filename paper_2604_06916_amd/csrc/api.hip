@@ -27,16 +27,17 @@ size_t quantize_scratch_bytes(int64_t rows, int64_t K) {
 }
 
 struct LinearLayout {
-  size_t codes, scales, alpha, partial, total;
+  size_t codes, scales, alpha, partial, gemm, total;
 };
 
-LinearLayout linear_layout(int64_t M, int64_t K) {
+LinearLayout linear_layout(int64_t M, int64_t N, int64_t K) {
   LinearLayout l;
   l.codes = 0;
   l.scales = round_up((size_t)(M * K / 2));
   l.alpha = l.scales + round_up((size_t)(M * K / 16));
   l.partial = l.alpha + kAlign;
-  l.total = l.partial + quantize_scratch_bytes(M, K);
+  l.gemm = l.partial + quantize_scratch_bytes(M, K);
+  l.total = l.gemm + round_up(solfp4::gemm_workspace_bytes(M, N, K));
   return l;
 }
 
@@ -56,7 +57,7 @@ int quantize_checks(const uint16_t* x, int64_t rows, int64_t K, const uint8_t* c
 
 int gemm_checks(const uint8_t* ac, const uint8_t* as, const float* ags, const uint8_t* bc,
                 const uint8_t* bs, const float* bgs, const uint16_t* bias, const uint16_t* out,
-                int64_t M, int64_t N, int64_t K) {
+                const void* ws, size_t ws_bytes, int64_t M, int64_t N, int64_t K) {
   int rc = check_dims(M, N);
   if (rc) return rc;
   rc = check_dims(K, 0);
@@ -72,6 +73,10 @@ int gemm_checks(const uint8_t* ac, const uint8_t* as, const float* ags, const ui
     return SOLFP4_EALIGN;
   if (K > 0 && (!aligned16(ac) || !aligned16(as) || !aligned16(bc) || !aligned16(bs)))
     return SOLFP4_EALIGN;
+  if (ws) {
+    if (!aligned16(ws)) return SOLFP4_EALIGN;
+    if (ws_bytes < solfp4::gemm_workspace_bytes(M, N, K)) return SOLFP4_EWORKSPACE;
+  }
   return SOLFP4_OK;
 }
 
@@ -154,21 +159,27 @@ int nvfp4_quantize(const uint16_t* x, int64_t rows, int64_t K, uint8_t* codes, u
 
 int nvfp4_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_global_scale,
                const uint8_t* b_codes, const uint8_t* b_scales, const float* b_global_scale,
-               const uint16_t* bias, uint16_t* out, int64_t M, int64_t N, int64_t K,
-               void* stream) {
+               const uint16_t* bias, uint16_t* out, void* workspace, size_t workspace_bytes,
+               int64_t M, int64_t N, int64_t K, void* stream) {
   const int rc = gemm_checks(a_codes, a_scales, a_global_scale, b_codes, b_scales, b_global_scale,
-                             bias, out, M, N, K);
+                             bias, out, workspace, workspace_bytes, M, N, K);
   if (rc) return rc;
   if (M == 0 || N == 0) return SOLFP4_OK;
   const hipError_t e = solfp4::launch_gemm(a_codes, a_scales, a_global_scale, b_codes, b_scales,
-                                           b_global_scale, bias, out, M, N, K,
+                                           b_global_scale, bias, out, M, N, K, workspace,
+                                           workspace ? workspace_bytes : 0,
                                            static_cast<hipStream_t>(stream));
   return e == hipSuccess ? SOLFP4_OK : SOLFP4_EHIP;
 }
 
-size_t nvfp4_linear_workspace_bytes(int64_t M, int64_t K) {
-  if (check_dims(M, K) || K % 16) return 0;
-  return linear_layout(M, K).total;
+size_t nvfp4_gemm_workspace_bytes(int64_t M, int64_t N, int64_t K) {
+  if (check_dims(M, N) || check_dims(K, 0) || K % 16 || K >= kMaxGemmK || N >= kMaxN) return 0;
+  return solfp4::gemm_workspace_bytes(M, N, K);
+}
+
+size_t nvfp4_linear_workspace_bytes(int64_t M, int64_t N, int64_t K) {
+  if (check_dims(M, N) || check_dims(K, 0) || K % 16 || K >= kMaxGemmK || N >= kMaxN) return 0;
+  return linear_layout(M, N, K).total;
 }
 
 int nvfp4_linear(const uint16_t* x, const uint8_t* w_codes, const uint8_t* w_scales,
@@ -182,22 +193,26 @@ int nvfp4_linear(const uint16_t* x, const uint8_t* w_codes, const uint8_t* w_sca
   if (K % 16 || K >= kMaxGemmK || N >= kMaxN) return SOLFP4_ESHAPE;
   if (!workspace) return SOLFP4_EINVAL;
   if (!aligned16(workspace)) return SOLFP4_EALIGN;
-  const LinearLayout l = linear_layout(M, K);
+  const LinearLayout l = linear_layout(M, N, K);
   if (workspace_bytes < l.total) return SOLFP4_EWORKSPACE;
   uint8_t* ws = static_cast<uint8_t*>(workspace);
   uint8_t* xc = ws + l.codes;
   uint8_t* xs = ws + l.scales;
   float* xa = reinterpret_cast<float*>(ws + l.alpha);
   uint32_t* partial = reinterpret_cast<uint32_t*>(ws + l.partial);
-  rc = quantize_checks(x, M, K, xc, xs, xa, partial, l.total - l.partial);
+  void* gws = ws + l.gemm;
+  const size_t gws_bytes = l.total - l.gemm;
+  rc = quantize_checks(x, M, K, xc, xs, xa, partial, l.gemm - l.partial);
   if (rc) return rc;
-  rc = gemm_checks(xc, xs, xa, w_codes, w_scales, w_global_scale, bias, out, M, N, K);
+  rc = gemm_checks(xc, xs, xa, w_codes, w_scales, w_global_scale, bias, out, gws, gws_bytes, M,
+                   N, K);
   if (rc) return rc;
   const hipStream_t s = static_cast<hipStream_t>(stream);
   hipError_t e = solfp4::launch_quantize(x, M, K, xc, xs, xa, partial, s);
   if (e != hipSuccess) return SOLFP4_EHIP;
   if (M == 0 || N == 0) return SOLFP4_OK;
-  e = solfp4::launch_gemm(xc, xs, xa, w_codes, w_scales, w_global_scale, bias, out, M, N, K, s);
+  e = solfp4::launch_gemm(xc, xs, xa, w_codes, w_scales, w_global_scale, bias, out, M, N, K, gws,
+                          gws_bytes, s);
   return e == hipSuccess ? SOLFP4_OK : SOLFP4_EHIP;
 }
 

@@ -98,9 +98,9 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t uniform_rsrc(const void* base,
 constexpr int kXcds = 8;
 constexpr int kGroupM = 8;
 
-__device__ __forceinline__ void tile_coords(int tiles_m, int tiles_n, int& tm, int& tn) {
+// Tile b of that order (b in [0, tiles_m * tiles_n)).
+__device__ __forceinline__ void tile_coords_at(int b, int tiles_m, int tiles_n, int& tm, int& tn) {
   const int total = tiles_m * tiles_n;
-  const int b = blockIdx.x;
   const int per_xcd = total / kXcds;
   const int t = b < per_xcd * kXcds ? (b % kXcds) * per_xcd + b / kXcds : b;
   const int group_size = kGroupM * tiles_n;
@@ -110,6 +110,10 @@ __device__ __forceinline__ void tile_coords(int tiles_m, int tiles_n, int& tm, i
   const int in_group = t % group_size;
   tm = first_m + in_group % gm;
   tn = in_group / gm;
+}
+
+__device__ __forceinline__ void tile_coords(int tiles_m, int tiles_n, int& tm, int& tn) {
+  tile_coords_at(blockIdx.x, tiles_m, tiles_n, tm, tn);
 }
 
 }  // namespace solfp4

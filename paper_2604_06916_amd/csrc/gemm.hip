@@ -469,7 +469,7 @@ __global__ __launch_bounds__(kLThreads, 1) void nvfp4_gemm_lane_kernel(
     const float* __restrict__ a_gs, const uint8_t* __restrict__ b_codes,
     const uint8_t* __restrict__ b_scales, const float* __restrict__ b_gs,
     const uint16_t* __restrict__ bias, uint16_t* __restrict__ out, int64_t M, int64_t N,
-    int64_t K) {
+    int64_t K, SplitK split) {
   static_assert(kWT == 128 || kWT == 64, "wave tile edge");
   constexpr int kT = 2 * kWT;                // output tile edge (M and N)
   constexpr int kFr = kWT / 32;              // 32 x 32 MFMA tiles per wave edge
@@ -489,10 +489,17 @@ __global__ __launch_bounds__(kLThreads, 1) void nvfp4_gemm_lane_kernel(
 
   const int tiles_m = (int)((M + kT - 1) / kT);
   const int tiles_n = (int)((N + kT - 1) / kT);
+  // workgroups past split.dp_tiles each take one K range of a remainder tile
+  const int sub = (int)blockIdx.x - split.dp_tiles;
+  const int rem = sub < 0 ? -1 : sub / split.splits;
+  const int part_idx = sub < 0 ? 0 : sub - rem * split.splits;
   int tm, tn;
-  tile_coords(tiles_m, tiles_n, tm, tn);
+  tile_coords_at(sub < 0 ? (int)blockIdx.x : split.dp_tiles + rem, tiles_m, tiles_n, tm, tn);
   const int64_t m0 = (int64_t)tm * kT;
   const int64_t n0 = (int64_t)tn * kT;
+  const int all_stages = (int)((K + kLBK - 1) / kLBK);
+  const int s_first = sub < 0 ? 0 : part_idx * split.stages;
+  const int nstages = sub < 0 ? all_stages : min(all_stages - s_first, split.stages);
 
   const int t = threadIdx.x;
   const int lane = t & (kWave - 1);
@@ -516,11 +523,12 @@ __global__ __launch_bounds__(kLThreads, 1) void nvfp4_gemm_lane_kernel(
   // l's 16 bytes land in slot l of the group's 1 KB
   const int dma_r = lane >> 2;
   const int piece = (lane & 3) ^ ((dma_r >> 2) & 3);
-  const uint32_t dma_off = (uint32_t)((16 * kGw * wave + dma_r) * row_bytes + 16 * piece);
+  const uint32_t dma_off =
+      (uint32_t)((16 * kGw * wave + dma_r) * row_bytes + 16 * piece + s_first * kLRowBytes);
   const uint32_t group_stride = (uint32_t)(16 * row_bytes);
   // scale staging: thread t moves the 8 scale bytes of tile row t of A and B
   // (threads past the tile's rows load zeros out of range and store nothing)
-  const uint32_t sg_off = (uint32_t)(t * scale_row);
+  const uint32_t sg_off = (uint32_t)(t * scale_row + 8 * s_first);
   // operand slots of this lane: row r of the tile lives in group r / 16 at
   // byte (r % 16) * 64 + 16 * (piece ^ ((r % 16) >> 2)); lane group g reads
   // piece g in K-steps 0-3 and piece 2 + g in K-steps 4-7
@@ -588,7 +596,7 @@ __global__ __launch_bounds__(kLThreads, 1) void nvfp4_gemm_lane_kernel(
     if (!kFull) {
       ga = u32x2_t{f.ha[0] | (f.ha[1] << 16), f.ha[2] | (f.ha[3] << 16)};
       gb = u32x2_t{f.hb[0] | (f.hb[1] << 16), f.hb[2] | (f.hb[3] << 16)};
-      const int64_t valid = scale_row - 8 * (int64_t)stage;   // blocks of this stage inside K
+      const int64_t valid = scale_row - 8 * (int64_t)(s_first + stage);   // blocks inside K
       if (valid < 8) {
         const uint64_t keep = valid <= 0 ? 0ull : (~0ull >> (64 - 8 * valid));
         ga.x &= (uint32_t)keep;
@@ -680,7 +688,6 @@ __global__ __launch_bounds__(kLThreads, 1) void nvfp4_gemm_lane_kernel(
   using J6 = std::integral_constant<int, 6>;
   using J7 = std::integral_constant<int, 7>;
 
-  const int nstages = (int)((K + kLBK - 1) / kLBK);
   constexpr int kSL = kFull ? 2 : 8;   // vector-memory instructions of one scale fetch (at most)
   // prologue: the scales of stages 0-2, then the codes of stages 0-2, all go
   // out first; the scales of stages 0 and 1 are parked in LDS as they land
@@ -789,6 +796,81 @@ __global__ __launch_bounds__(kLThreads, 1) void nvfp4_gemm_lane_kernel(
   // no DMA may still be writing LDS when the workgroup ends
   wait_counts<0, 0>();
 
+  if (sub >= 0) {
+    // One of the two K halves of a remainder tile: park the FP32
+    // accumulators in the workspace; the second of the tile's two
+    // workgroups to finish adds the other half's sums to its own (FP32
+    // addition is commutative, so the result does not depend on which one
+    // that is) and runs the epilogue.  The partial sums are written and read
+    // with the sc1 cache policy (written through to memory, read past this
+    // XCD's L2), so they are coherent across XCDs without writing back or
+    // invalidating whole L2 caches; a half's stores are complete before its
+    // workgroup counts itself in.  Lane-major 16-byte slots: each store or
+    // load instruction covers 1 KB.
+    constexpr int kSlots = kFr * kFr * 4;           // 16-byte slots per lane
+    constexpr uint32_t kSlotBytes = 16 * kWave;     // one slot of a wave
+    constexpr uint32_t kHalfBytes = 4 * kSlots * kSlotBytes;   // one half's partial tile
+    constexpr int kSc1 = 16;                        // cache policy bits: sc1
+    const __amdgpu_buffer_rsrc_t rp = uniform_rsrc(
+        reinterpret_cast<const uint8_t*>(split.part) + (size_t)rem * 2 * kHalfBytes,
+        (int64_t)2 * kHalfBytes);
+    const uint32_t lane_off = (uint32_t)wave * kSlots * kSlotBytes + 16u * lane;
+#pragma unroll
+    for (int fn = 0; fn < kFr; ++fn)
+#pragma unroll
+      for (int fm = 0; fm < kFr; ++fm)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const floatx16_t& a = acc[fn][fm];
+          const u32x4_t v = {__float_as_uint(a[4 * q]), __float_as_uint(a[4 * q + 1]),
+                             __float_as_uint(a[4 * q + 2]), __float_as_uint(a[4 * q + 3])};
+          __builtin_amdgcn_raw_buffer_store_b128(
+              v, rp, lane_off + part_idx * kHalfBytes + ((fn * kFr + fm) * 4 + q) * kSlotBytes, 0, kSc1);
+        }
+    __shared__ int last_flag;
+    wait_counts<0, 0>();   // this thread's partial sums have reached memory
+    __syncthreads();
+    if (t == 0) {
+      const uint64_t mine = kSplitToken ^ (uint64_t)(2 * rem + part_idx);
+      const uint64_t before = __hip_atomic_exchange(&split.slots[rem], mine, __ATOMIC_RELAXED,
+                                                    __HIP_MEMORY_SCOPE_AGENT);
+      last_flag = before == (mine ^ 1u);   // the other half's token: it finished first
+      if (last_flag)
+        __hip_atomic_store(&split.slots[rem], (uint64_t)0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    __syncthreads();
+    if (!last_flag) return;
+    // The other half's sums come in through LDS, whose stage buffers are
+    // free now: each wave moves its own slots by DMA (no registers held
+    // while the loads are in flight), half of them at a time into two of
+    // the stage buffers, then reads each slot back and adds it.
+    constexpr int kPerBuf = kStage / 1024;   // 1 KB slots per stage buffer
+    constexpr int kPass = kSlots / 2;
+    static_assert(kSlots % 2 == 0 && kPass <= 2 * kPerBuf, "slots per pass");
+    uint8_t* const lds_lo = wave == 0 ? la0 : wave == 1 ? la2 : wave == 2 ? lb0 : lb2;
+    uint8_t* const lds_hi = wave == 0 ? la1 : wave == 1 ? la3 : wave == 2 ? lb1 : lb3;
+    const uint32_t other = lane_off + (1 - part_idx) * kHalfBytes;
+#pragma unroll
+    for (int pass = 0; pass < 2; ++pass) {
+#pragma unroll
+      for (int i = 0; i < kPass; ++i) {
+        uint8_t* const dst = (i < kPerBuf ? lds_lo : lds_hi) + (i % kPerBuf) * 1024;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rp, (lds_ptr_t)dst, 16,
+                                                 other + (pass * kPass + i) * kSlotBytes, 0, 0, kSc1);
+      }
+      wait_counts<0, 0>();
+#pragma unroll
+      for (int i = 0; i < kPass; ++i) {
+        const int slot = pass * kPass + i;
+        const int fn = slot / (4 * kFr), fm = (slot / 4) % kFr, q = slot % 4;
+        const uint8_t* const src = (i < kPerBuf ? lds_lo : lds_hi) + (i % kPerBuf) * 1024 + 16 * lane;
+        const u32x4_t v = *reinterpret_cast<const u32x4_t*>(src);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc[fn][fm][4 * q + e] += __uint_as_float(v[e]);
+      }
+    }
+  }
+
   // epilogue: out = bf16(fp32(fma(alpha, acc, bias))), alpha = aA * aB in
   // FP32.  Lane (li, g) holds, per MFMA tile, row m = li and the column runs
   // 8k + 4g .. 8k + 4g + 3 (k = 0..3); swapping halves with the lane 32 apart
@@ -875,10 +957,73 @@ bool small_tiles_pay(int64_t tiles256, int64_t tiles128) {
   return small < big;
 }
 
+SplitPlan plan_split(int64_t tiles, int64_t nstages, double fixed_cost, double part_cost) {
+  SplitPlan plan;
+  plan.dp_tiles = tiles;
+  plan.stages = nstages;
+  const int64_t cus = device_cus();
+  const int64_t rem = tiles % cus;
+  if (rem == 0 || nstages < 2) return plan;
+  // two K halves per remainder tile (the kernels add exactly two), when
+  // both halves of every remainder tile fit in one round
+  if (2 * rem > cus) return plan;
+  const double whole = (double)nstages + fixed_cost;
+  const double halves = (double)((nstages + 1) / 2) + fixed_cost + 2.0 * part_cost;
+  if (!(halves < whole)) return plan;
+  plan.stages = (nstages + 1) / 2;
+  plan.splits = 2;
+  plan.rem_tiles = rem;
+  plan.dp_tiles = tiles - rem;
+  plan.bytes = ((size_t)rem * 8 + 255) / 256 * 256 + (size_t)(rem * plan.splits) * kPartTileBytes;
+  return plan;
+}
+
+SplitK split_args(const SplitPlan& plan, void* workspace) {
+  SplitK a{};
+  a.dp_tiles = (int)plan.dp_tiles;
+  a.splits = (int)plan.splits;
+  a.stages = (int)plan.stages;
+  if (plan.active()) {
+    a.slots = static_cast<uint64_t*>(workspace);
+    a.part = reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) +
+                                      ((size_t)plan.rem_tiles * 8 + 255) / 256 * 256);
+  }
+  return a;
+}
+
+// Timing estimates in units of one K stage of the NVFP4 lane kernel
+// (measured about 5.1k cycles on a busy chip): prologue plus epilogue of a
+// tile about 3.3 stages; writing one 256 KB partial tile, or reading one
+// back, with every remainder workgroup doing so at once, 2-3.5 stages.
+#ifndef SOLFP4_SPLIT_FIXED
+#define SOLFP4_SPLIT_FIXED 3.3
+#endif
+#ifndef SOLFP4_SPLIT_PART
+#define SOLFP4_SPLIT_PART 2.5
+#endif
+
+// The lane kernel on 256 x 256 tiles is the one that splits.
+static SplitPlan gemm_plan(int64_t M, int64_t N, int64_t K, bool* small_out) {
+  SplitPlan plan;
+  const bool lane = K % kLBK == 0 || K % 64 == 32;
+  const int64_t t256 = ((M + 255) / 256) * ((N + 255) / 256);
+  const int64_t t128 = ((M + 127) / 128) * ((N + 127) / 128);
+  const bool small = lane && small_tiles_pay(t256, t128);
+  if (small_out) *small_out = small;
+  plan.dp_tiles = t256;
+  if (!lane || small) return plan;
+  return plan_split(t256, (K + kLBK - 1) / kLBK, SOLFP4_SPLIT_FIXED, SOLFP4_SPLIT_PART);
+}
+
+size_t gemm_workspace_bytes(int64_t M, int64_t N, int64_t K) {
+  if (M <= 0 || N <= 0 || K <= 0) return 0;
+  return gemm_plan(M, N, K, nullptr).bytes;
+}
+
 hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_gs,
                        const uint8_t* b_codes, const uint8_t* b_scales, const float* b_gs,
                        const uint16_t* bias, uint16_t* out, int64_t M, int64_t N, int64_t K,
-                       hipStream_t stream) {
+                       void* workspace, size_t workspace_bytes, hipStream_t stream) {
   if (M == 0 || N == 0) return hipSuccess;
   const int64_t tiles = ((M + kBM - 1) / kBM) * ((N + kBN - 1) / kBN);
   const dim3 grid((unsigned)tiles);
@@ -888,13 +1033,20 @@ hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const fl
   // about 5% faster at K % 128 == 64 (K = 2240), while at K = 5600 (where it
   // must take its unaligned path) the lane kernel is 1.46x faster.
   if (K % kLBK == 0 || K % 64 == 32) {
-    const int64_t t256 = ((M + 255) / 256) * ((N + 255) / 256);
+    bool small = false;
+    SplitPlan plan = gemm_plan(M, N, K, &small);
+    if (plan.active() && (workspace == nullptr || workspace_bytes < plan.bytes)) {
+      plan = SplitPlan{};   // no room: every tile whole
+      plan.dp_tiles = ((M + 255) / 256) * ((N + 255) / 256);
+      plan.stages = (K + kLBK - 1) / kLBK;
+    }
+    const SplitK split = split_args(plan, workspace);
     const int64_t t128 = ((M + 127) / 128) * ((N + 127) / 128);
-    const bool small = small_tiles_pay(t256, t128);
-    const dim3 lgrid((unsigned)(small ? t128 : t256));
+    const dim3 lgrid((unsigned)(small ? t128 : plan.dp_tiles + plan.rem_tiles * plan.splits));
 #define SOLFP4_LANE_LAUNCH(V, F, W)                                                           \
   hipLaunchKernelGGL((nvfp4_gemm_lane_kernel<V, F, W>), lgrid, dim3(kLThreads), 0, stream,     \
-                     a_codes, a_scales, a_gs, b_codes, b_scales, b_gs, bias, out, M, N, K)
+                     a_codes, a_scales, a_gs, b_codes, b_scales, b_gs, bias, out, M, N, K,     \
+                     small ? SplitK{nullptr, nullptr, (int)t128, 1, 0} : split)
     const bool full = K % kLBK == 0;
     if (small) {
       if (vec && full) SOLFP4_LANE_LAUNCH(true, true, 64);

@@ -24,10 +24,51 @@ hipError_t launch_quantize(const uint16_t* x, int64_t rows, int64_t K, uint8_t* 
 // ones, given the tile counts of both (host only).
 bool small_tiles_pay(int64_t tiles256, int64_t tiles128);
 
+// Split-K for the last, partial round of 256 x 256 tiles.  A GEMM with T
+// tiles on C compute units runs about ceil(T / C) rounds of one tile's time;
+// when the last round holds only R = T mod C tiles, most of the chip idles
+// through it.  Instead, workgroups [0, dp_tiles) take whole tiles and each
+// of the R remainder tiles is computed as two K halves, one workgroup each
+// (when 2R <= C); each half parks its FP32 partial sums in a workspace, and
+// the second of the two to finish adds the other's sums to its own and runs
+// the epilogue.  Which one is second: each half swaps its own 64-bit token
+// (a fixed pattern times the tile and half) into the tile's slot, and the
+// one that gets the other half's token back is second and clears the slot.
+// This works whatever the slot held before the launch (other than one of
+// the two tokens), so the workspace needs no clearing between calls.
+struct SplitK {
+  float* part;          // two 256 KB partial tiles per remainder tile
+  uint64_t* slots;      // one per remainder tile: 0 after every launch, or
+                        // the token of the half that finished first
+  int dp_tiles;         // workgroups that take whole tiles (all of them: no split)
+  int splits;           // K ranges per remainder tile: 2 (1: no split)
+  int stages;           // K stages of the first half (the second may have fewer)
+};
+
+struct SplitPlan {
+  int64_t dp_tiles = 0, rem_tiles = 0, splits = 1, stages = 0;
+  size_t bytes = 0;      // workspace: slots (256-byte aligned), then partial sums
+  bool active() const { return splits > 1; }
+};
+
+// The plan for `tiles` 256 x 256 tiles of `nstages` K stages each: split
+// the remainder tiles when the estimated last round, ceil(nstages / 2) +
+// fixed_cost + 2 part_cost stages (a half, then writing its partial tile
+// and reading the other's), beats nstages + fixed_cost.
+SplitPlan plan_split(int64_t tiles, int64_t nstages, double fixed_cost, double part_cost);
+SplitK split_args(const SplitPlan& plan, void* workspace);
+constexpr size_t kPartTileBytes = 256 * 256 * 4;
+// token of half h of remainder tile r: kSplitToken ^ (2 r + h), never 0
+constexpr uint64_t kSplitToken = 0xC6A4A7935BD1E995ull;
+
+// Bytes of workspace launch_gemm uses to split this GEMM's last round (0:
+// it runs unsplit).
+size_t gemm_workspace_bytes(int64_t M, int64_t N, int64_t K);
+
 hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_gs,
                        const uint8_t* b_codes, const uint8_t* b_scales, const float* b_gs,
                        const uint16_t* bias, uint16_t* out, int64_t M, int64_t N, int64_t K,
-                       hipStream_t stream);
+                       void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 // MXFP4 (32-element blocks, E8M0 scales): one quantize pass, and the GEMM
 // on the scaled FP4 matrix instructions.

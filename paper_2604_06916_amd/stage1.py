@@ -120,7 +120,8 @@ class Runner:
             self.layers.append(L)
         kmax = max(K for _, _, K in layer_shapes(cfg))
         if backend == "nvfp4":
-            self.ws = torch.empty(sol.nvfp4_linear_workspace_bytes(M, kmax), dtype=torch.uint8, device=device)
+            wsb = max(sol.nvfp4_linear_workspace_bytes(M, N, K) for _, N, K in layer_shapes(cfg))
+            self.ws = torch.empty(wsb, dtype=torch.uint8, device=device)
         elif backend == "mxfp4":
             self.ws = torch.empty(sol.mxfp4_linear_workspace_bytes(M, kmax), dtype=torch.uint8, device=device)
         H, D = cfg.hidden, cfg.mlp

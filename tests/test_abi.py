@@ -62,9 +62,37 @@ def test_workspace_queries():
     assert q(0, 0) >= 4 and q(128, 1152) >= 4 and q(10 ** 6, 4096) <= 4096 * 4
     assert q(-1, 16) == 0 and q(4, 24) == 0
     L = sol.nvfp4_linear_workspace_bytes
-    for M, K in [(1, 16), (128, 1152), (18432, 3072), (26574, 9728)]:
-        assert L(M, K) >= M * K // 2 + M * K // 16 + 4 + q(M, K)
-    assert L(-1, 16) == 0 and L(3, 40) == 0
+    G = sol.nvfp4_gemm_workspace_bytes
+    for M, N, K in [(1, 1, 16), (128, 1152, 1152), (18432, 3072, 3072), (26574, 2432, 9728),
+                    (18432, 3072, 12288)]:
+        assert L(M, N, K) >= M * K // 2 + M * K // 16 + 4 + q(M, K) + G(M, N, K)
+    assert L(-1, 16, 16) == 0 and L(3, 8, 40) == 0 and L(3, -8, 16) == 0
+    assert G(-1, 16, 16) == 0 and G(3, 8, 40) == 0 and G(3, 8, 1 << 24) == 0
+
+
+def test_gemm_workspace_plan():
+    """Which shapes split their last round's tiles into two K halves, and
+    the workspace that takes (an 8-byte slot per remainder tile, 256-byte
+    aligned, then two 256 KB FP32 partial tiles per tile).  Without a GPU
+    the CU count is MI355X's 256."""
+    G = sol.nvfp4_gemm_workspace_bytes
+    part = 256 * 256 * 4
+
+    def bytes_for(rem):
+        return (rem * 8 + 255) // 256 * 256 + rem * 2 * part
+    # FLUX.1 layers, 18432 tokens: 2592, 864, 3456 and 864 tiles of 256 x 256
+    assert G(18432, 9216, 3072) == bytes_for(2592 % 256)
+    assert G(18432, 3072, 3072) == bytes_for(864 % 256)
+    assert G(18432, 12288, 3072) == bytes_for(3456 % 256)
+    assert G(18432, 3072, 12288) == bytes_for(864 % 256)
+    # whole rounds, remainders too large to split in two within one round,
+    # too little K to gain, and shapes on other kernels or tile sizes
+    assert G(4096, 4096, 4096) == 0            # 256 tiles
+    assert G(26574, 7296, 2432) == 0           # 3016 tiles: 200 left over
+    assert G(18432, 3072, 512) == 0            # 4 K stages
+    assert G(8192, 6720, 2240) == 0            # K % 128 == 64: shared-conversion kernel
+    assert G(128, 1152, 1152) == 0             # 128 x 128 tiles
+    assert G(0, 3072, 3072) == 0 and G(18432, 0, 3072) == 0
 
 
 def quant(x=P, rows=4, K=32, codes=P2, scales=P3, gs=P, ws=P, wsb=4096):
@@ -87,8 +115,9 @@ def test_quantize_rejects_bad_arguments():
     assert quant(wsb=0) == EWORKSPACE
 
 
-def gemm(ac=P, as_=P2, ag=P3, bc=P, bs=P2, bg=P3, bias=NULL, out=P, M=8, N=8, K=32):
-    return sol.lib.nvfp4_gemm(ac, as_, ag, bc, bs, bg, bias, out, M, N, K, S)
+def gemm(ac=P, as_=P2, ag=P3, bc=P, bs=P2, bg=P3, bias=NULL, out=P, ws=NULL, wsb=0, M=8, N=8,
+         K=32):
+    return sol.lib.nvfp4_gemm(ac, as_, ag, bc, bs, bg, bias, out, ws, wsb, M, N, K, S)
 
 
 def test_gemm_rejects_bad_arguments():
@@ -103,6 +132,14 @@ def test_gemm_rejects_bad_arguments():
     assert gemm(as_=MIS) == EALIGN
     assert gemm(bias=MIS) == EALIGN
     assert gemm(out=MIS) == EALIGN
+    # a workspace is optional, but one that is passed must be aligned and
+    # large enough for the shape's split
+    big = dict(M=18432, N=3072, K=12288)
+    need = sol.nvfp4_gemm_workspace_bytes(**big)
+    assert need > 0
+    assert gemm(ws=MIS, wsb=need, **big) == EALIGN
+    assert gemm(ws=P, wsb=need - 1, **big) == EWORKSPACE
+    assert gemm(ws=P, wsb=need - 1, out=NULL, **big) == EINVAL
     # nothing to compute: valid, and no HIP call is made
     assert gemm(M=0, out=NULL) == OK
     assert gemm(N=0, out=NULL) == OK
@@ -113,6 +150,10 @@ def linear(x=P, wc=P2, ws_=P3, wg=P, bias=NULL, out=P2, ws=P3, wsb=1 << 20, M=8,
 
 
 def test_linear_rejects_bad_arguments():
+    big = dict(M=18432, N=3072, K=12288)
+    need = sol.nvfp4_linear_workspace_bytes(**big)
+    assert need > sol.nvfp4_linear_workspace_bytes(18432, 3072, 512)
+    assert linear(wsb=need - 1, **big) == EWORKSPACE
     assert linear(M=-1) == EINVAL
     assert linear(K=20) == ESHAPE
     assert linear(ws=NULL) == EINVAL

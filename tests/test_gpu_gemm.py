@@ -19,11 +19,11 @@ pytestmark = pytest.mark.gpu
 TOL = 2e-3
 
 
-def gpu_gemm(ac, as_, aa, bc, bs, ba, bias=None):
+def gpu_gemm(ac, as_, aa, bc, bs, ba, bias=None, split=True):
     M, N = ac.shape[0], bc.shape[0]
     out = poison_bf16((M, N))
     sol.nvfp4_gemm(u8_to_dev(ac), u8_to_dev(as_), f32_to_dev(aa), u8_to_dev(bc), u8_to_dev(bs),
-                   f32_to_dev(ba), None if bias is None else bf16_to_dev(bias), out)
+                   f32_to_dev(ba), None if bias is None else bf16_to_dev(bias), out, split=split)
     torch.cuda.synchronize()
     return bf16_from_dev(out)
 
@@ -49,15 +49,22 @@ def test_golden_gemms():
 # workgroup-shared one; each list covers every case.  The lane kernel takes
 # 128 x 128 tiles when there are too few 256 x 256 tiles to fill the chip
 # (every small shape here) and 256 x 256 tiles otherwise (5376 x 5376: 441
-# of them).
+# of them).  With 256 x 256 tiles, a last round of at most half the CUs'
+# worth of tiles is split into K halves when K is long enough (the last
+# three shapes: 272, 289 and 306 tiles, the middle one with a partial last
+# stage, the last one with N % 8 != 0).
+SPLIT_SHAPES = [(4352, 4096, 1536), (4352, 4200, 1440), (4353, 4100, 1536)]
+
+
 @pytest.mark.parametrize("M,N,K", [(1, 1, 16), (3, 5, 32), (37, 70, 64), (300, 260, 48),
                                    (257, 513, 16), (64, 96, 128), (300, 260, 256),
                                    (513, 700, 384), (64, 1000, 1280), (300, 260, 160),
                                    (513, 700, 224), (260, 300, 2240), (5376, 5376, 256),
-                                   (5376, 5400, 96), (4200, 4360, 1120)])
+                                   (5376, 5400, 96), (4200, 4360, 1120)] + SPLIT_SHAPES)
 def test_exact_sums_are_bit_exact(M, N, K):
     """Scales 1.0 and power-of-two alphas: every partial sum is a multiple of
-    1/4 below 2^12, exact in FP32, so the only rounding is the final BF16."""
+    1/4 of magnitude at most 36 K < 2^16, exact in FP32 in any order, so the
+    only rounding is the final BF16."""
     g = np.random.Generator(np.random.PCG64(M * 1000 + N + K))
     ac = g.integers(0, 256, size=(M, K // 2), dtype=np.uint8)
     bc = g.integers(0, 256, size=(N, K // 2), dtype=np.uint8)
@@ -175,6 +182,72 @@ def test_zero_k_writes_bias():
     sol.nvfp4_gemm(z, z, f32_to_dev(1.0), zb, zb, f32_to_dev(1.0), bf16_to_dev(bias), out)
     torch.cuda.synchronize()
     assert np.array_equal(bf16_from_dev(out), np.broadcast_to(bias, (M, N)))
+
+
+@pytest.mark.parametrize("M,N,K", SPLIT_SHAPES)
+def test_split_last_round_vs_oracle(M, N, K):
+    """The last round's tiles as two K halves: within the bar of the oracle,
+    and the same bits on a second call (the workspace is reused, its
+    counters cleared by the call itself) as on the first."""
+    need = sol.nvfp4_gemm_workspace_bytes(M, N, K)
+    assert need > 0
+    ac, as_, aa = quantized("normal", M, K, 5 * M + K)
+    bc, bs, ba = quantized(None, N, K, 3 * N + K, sigma=0.02)
+    bias = draw_bias(N, 0.02, N)
+    dev = device()
+    args = [u8_to_dev(ac), u8_to_dev(as_), f32_to_dev(aa), u8_to_dev(bc), u8_to_dev(bs),
+            f32_to_dev(ba), bf16_to_dev(bias)]
+    ws = torch.full((need,), 0xA5, dtype=torch.uint8, device=dev)
+    outs = []
+    for _ in range(2):
+        out = poison_bf16((M, N))
+        sol.nvfp4_gemm(*args, out, workspace=ws)
+        torch.cuda.synchronize()
+        outs.append(bf16_from_dev(out))
+    whole = gpu_gemm(ac, as_, aa, bc, bs, ba, bias, split=False)
+    ref = O.nvfp4_gemm_ref(ac, as_, aa, bc, bs, ba, bias)
+    err, err_whole = rel_fro(outs[0], ref), rel_fro(whole, ref)
+    diff = float(np.mean(outs[0] != whole))
+    say(f"split M={M} N={N} K={K}: rel_fro={err:.3e} (unsplit {err_whole:.3e}), "
+        f"outputs differing from unsplit {diff:.2e}")
+    assert np.array_equal(outs[0], outs[1])
+    assert err <= TOL and err_whole <= TOL
+    assert bf16_mismatch_fraction(outs[0], ref) <= 0.01
+
+
+def test_split_gemm_in_a_replayed_graph():
+    """A split GEMM captured once and replayed: the tile slots left by each
+    replay (and by the eager calls between replays) must not confuse the
+    next; every replay equals the eager result bit for bit."""
+    M, N, K = SPLIT_SHAPES[0]
+    ac, as_, aa = quantized("normal", M, K, 17)
+    bc, bs, ba = quantized(None, N, K, 19, sigma=0.02)
+    args = [u8_to_dev(ac), u8_to_dev(as_), f32_to_dev(aa), u8_to_dev(bc), u8_to_dev(bs),
+            f32_to_dev(ba), None]
+    dev = device()
+    ws = torch.empty(sol.nvfp4_gemm_workspace_bytes(M, N, K), dtype=torch.uint8, device=dev)
+    eager = poison_bf16((M, N))
+    sol.nvfp4_gemm(*args, eager, workspace=ws)
+    torch.cuda.synchronize()
+    want = bf16_from_dev(eager)
+    out = poison_bf16((M, N))
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):   # warm-up on the capture stream, as torch asks
+        sol.nvfp4_gemm(*args, out, workspace=ws)
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        sol.nvfp4_gemm(*args, out, workspace=ws)
+    for _ in range(3):
+        out.view(torch.int16).fill_(0x7FC1)
+        g.replay()
+        torch.cuda.synchronize()
+        assert np.array_equal(bf16_from_dev(out), want)
+        sol.nvfp4_gemm(*args, eager, workspace=ws)
+        torch.cuda.synchronize()
+        assert np.array_equal(bf16_from_dev(eager), want)
 
 
 def test_deterministic():

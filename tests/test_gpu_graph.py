@@ -50,7 +50,7 @@ def setup(fmt, M, dims, seed):
             L["wa"] = torch.empty(1, dtype=torch.float32, device=dev)
             L["qws"] = torch.empty(max(sol.nvfp4_quantize_workspace_bytes(N, K), 256),
                                    dtype=torch.uint8, device=dev)
-            L["lws"] = torch.empty(sol.nvfp4_linear_workspace_bytes(M, K), dtype=torch.uint8,
+            L["lws"] = torch.empty(sol.nvfp4_linear_workspace_bytes(M, N, K), dtype=torch.uint8,
                                    device=dev)
         else:
             L["ws"] = torch.empty((N, K // 32), dtype=torch.uint8, device=dev)

@@ -44,7 +44,7 @@ def test_linear_workspace_holds_the_activation_codes():
     wb = draw_weights(N, K, 0.02, seed=4)
     x = bf16_to_dev(xb)
     wc, ws, wa = sol.nvfp4_quantize(bf16_to_dev(wb))
-    wsp = torch.empty(sol.nvfp4_linear_workspace_bytes(M, K), dtype=torch.uint8, device=x.device)
+    wsp = torch.empty(sol.nvfp4_linear_workspace_bytes(M, N, K), dtype=torch.uint8, device=x.device)
     sol.nvfp4_linear(x, wc, ws, wa, workspace=wsp)
     torch.cuda.synchronize()
     rc, _, _ = O.nvfp4_quantize_ref(xb)
