@@ -488,7 +488,8 @@ def main():
     for i, L in enumerate(layers):
         wq = np.mean([ev[s][i][0].elapsed_time(ev[s][i][1]) for s in range(args.steps)])
         xq = np.mean([ev[s][i][1].elapsed_time(ev[s][i][2]) for s in range(args.steps)])
-        gm = np.mean([ev[s][i][2].elapsed_time(ev[s][i][3]) for s in range(args.steps)])
+        gms = np.array([ev[s][i][2].elapsed_time(ev[s][i][3]) for s in range(args.steps)])
+        gm = float(np.mean(gms))
         gemm_ms_tot += gm
         wq_ms_tot += wq
         xq_ms_tot += xq
@@ -497,6 +498,7 @@ def main():
         per_layer.append({
             "layer": L["name"], "M": L["M"], "N": L["N"], "K": L["K"],
             "gemm_us": round(gm * 1e3, 2), "gemm_tflops": round(fl / (gm * 1e-3) / 1e12, 1),
+            "gemm_us_p10_p50_p90": [round(float(np.percentile(gms, q)) * 1e3, 2) for q in (10, 50, 90)],
             "quantize_x_us": round(xq * 1e3, 2),
             "quantize_x_gbs": round(xbytes / (xq * 1e-3) / 1e9, 1),
             "quantize_w_us": round(wq * 1e3, 2),
