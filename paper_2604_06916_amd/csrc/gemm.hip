@@ -460,9 +460,12 @@ __device__ __forceinline__ uint32_t scale_patterns(uint32_t w, bool high_pair) {
 // scale bytes per row are one aligned 8-byte load.  Otherwise (K % 32 == 0)
 // the last stage is partial: its code pieces past K read bytes of the next
 // row (or zeros past the tile), which stay harmless because the scales of
-// those blocks are set to zero (E2M1 codes are all finite, and q * 0 = 0);
-// scale bytes are then fetched as four 2-byte loads (a row's scales start at
-// an even offset only).
+// those blocks are set to zero (E2M1 codes are all finite, and q * 0 = 0).
+// A row's scales then start at an even offset only; the 8-byte load works
+// at any byte alignment, but the buffer range check drops a whole 4-byte
+// word that straddles the end of the range, so the one lane whose stage
+// reaches past the operand's last scale byte (the last row, last stage)
+// fetches its bytes as four 2-byte loads instead.
 template <bool kVecOut, bool kFull, int kWT>
 __global__ __launch_bounds__(kLThreads, 1) void nvfp4_gemm_lane_kernel(
     const uint8_t* __restrict__ a_codes, const uint8_t* __restrict__ a_scales,
@@ -572,20 +575,26 @@ __global__ __launch_bounds__(kLThreads, 1) void nvfp4_gemm_lane_kernel(
     }
   };
   // one stage's scale bytes of this thread's A and B rows, in flight
+  const uint32_t range_a = (uint32_t)(valid_a * scale_row);
+  const uint32_t range_b = (uint32_t)(valid_b * scale_row);
   struct ScaleFetch {
-    u32x2_t a, b;            // kFull: one 8-byte load each
-    uint32_t ha[4], hb[4];   // otherwise four 2-byte loads each, combined when parked
+    u32x2_t a, b;            // one 8-byte load each
+    uint32_t ha[4], hb[4];   // !kFull, a stage straddling the end of the range: 2-byte loads
+    bool whole_a, whole_b;   // the 8-byte load holds every in-range byte
   };
   auto fetch_scales = [&](ScaleFetch& f, int stage) {
     const uint32_t off = sg_off + 8 * stage;
-    if (kFull) {
-      f.a = __builtin_amdgcn_raw_buffer_load_b64(rsa, off, 0, 0);
-      f.b = __builtin_amdgcn_raw_buffer_load_b64(rsb, off, 0, 0);
-    } else {
+    f.a = __builtin_amdgcn_raw_buffer_load_b64(rsa, off, 0, 0);
+    f.b = __builtin_amdgcn_raw_buffer_load_b64(rsb, off, 0, 0);
+    if (!kFull) {
+      f.whole_a = off + 8 <= range_a || off >= range_a;
+      f.whole_b = off + 8 <= range_b || off >= range_b;
+      if (!(f.whole_a && f.whole_b)) {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        f.ha[j] = __builtin_amdgcn_raw_buffer_load_b16(rsa, off + 2 * j, 0, 0);
-        f.hb[j] = __builtin_amdgcn_raw_buffer_load_b16(rsb, off + 2 * j, 0, 0);
+        for (int j = 0; j < 4; ++j) {
+          f.ha[j] = __builtin_amdgcn_raw_buffer_load_b16(rsa, off + 2 * j, 0, 0);
+          f.hb[j] = __builtin_amdgcn_raw_buffer_load_b16(rsb, off + 2 * j, 0, 0);
+        }
       }
     }
   };
@@ -594,8 +603,8 @@ __global__ __launch_bounds__(kLThreads, 1) void nvfp4_gemm_lane_kernel(
   auto store_scales = [&](ScaleFetch& f, int set, int stage) {
     u32x2_t ga = f.a, gb = f.b;
     if (!kFull) {
-      ga = u32x2_t{f.ha[0] | (f.ha[1] << 16), f.ha[2] | (f.ha[3] << 16)};
-      gb = u32x2_t{f.hb[0] | (f.hb[1] << 16), f.hb[2] | (f.hb[3] << 16)};
+      if (!f.whole_a) ga = u32x2_t{f.ha[0] | (f.ha[1] << 16), f.ha[2] | (f.ha[3] << 16)};
+      if (!f.whole_b) gb = u32x2_t{f.hb[0] | (f.hb[1] << 16), f.hb[2] | (f.hb[3] << 16)};
       const int64_t valid = scale_row - 8 * (int64_t)(s_first + stage);   // blocks inside K
       if (valid < 8) {
         const uint64_t keep = valid <= 0 ? 0ull : (~0ull >> (64 - 8 * valid));
@@ -688,7 +697,7 @@ __global__ __launch_bounds__(kLThreads, 1) void nvfp4_gemm_lane_kernel(
   using J6 = std::integral_constant<int, 6>;
   using J7 = std::integral_constant<int, 7>;
 
-  constexpr int kSL = kFull ? 2 : 8;   // vector-memory instructions of one scale fetch (at most)
+  constexpr int kSL = 2;   // vector-memory instructions of one scale fetch (but for one stage of one lane)
   // prologue: the scales of stages 0-2, then the codes of stages 0-2, all go
   // out first; the scales of stages 0 and 1 are parked in LDS as they land
   // (each store waits only for its own, older loads), stage 2's stay in
@@ -1003,15 +1012,21 @@ SplitK split_args(const SplitPlan& plan, void* workspace) {
 #endif
 
 // The lane kernel on 256 x 256 tiles is the one that splits.
+// The lane kernel takes K % 128 == 0 and K % 64 == 32 always.  At
+// K % 128 == 64 (a half last stage) the workgroup-shared kernel is 1-2%
+// faster on whole rounds of 256 x 256 tiles (the 8192-token 2240 -> 6720
+// and 2240 -> 5600 layers), so the lane kernel takes those shapes only
+// where its 128 x 128 tiles or its split last round apply (2240 -> 2240:
+// 1.08x; 300 x 260: 2.6x).  K % 32 == 16 is the shared kernel's alone.
 static SplitPlan gemm_plan(int64_t M, int64_t N, int64_t K, bool* small_out) {
   SplitPlan plan;
-  const bool lane = K % kLBK == 0 || K % 64 == 32;
+  const bool lane_ok = K % 32 == 0;
   const int64_t t256 = ((M + 255) / 256) * ((N + 255) / 256);
   const int64_t t128 = ((M + 127) / 128) * ((N + 127) / 128);
-  const bool small = lane && small_tiles_pay(t256, t128);
+  const bool small = lane_ok && small_tiles_pay(t256, t128);
   if (small_out) *small_out = small;
   plan.dp_tiles = t256;
-  if (!lane || small) return plan;
+  if (!lane_ok || small) return plan;
   return plan_split(t256, (K + kLBK - 1) / kLBK, SOLFP4_SPLIT_FIXED, SOLFP4_SPLIT_PART);
 }
 
@@ -1028,18 +1043,16 @@ hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const fl
   const int64_t tiles = ((M + kBM - 1) / kBM) * ((N + kBN - 1) / kBN);
   const dim3 grid((unsigned)tiles);
   const bool vec = N % 8 == 0;
-  // The lane kernel for K % 128 == 0 and for K % 64 == 32; measured on the
-  // 8192-token 2240 -> 6720/2240/5600 layers, the workgroup-shared kernel is
-  // about 5% faster at K % 128 == 64 (K = 2240), while at K = 5600 (where it
-  // must take its unaligned path) the lane kernel is 1.46x faster.
-  if (K % kLBK == 0 || K % 64 == 32) {
-    bool small = false;
-    SplitPlan plan = gemm_plan(M, N, K, &small);
-    if (plan.active() && (workspace == nullptr || workspace_bytes < plan.bytes)) {
-      plan = SplitPlan{};   // no room: every tile whole
-      plan.dp_tiles = ((M + 255) / 256) * ((N + 255) / 256);
-      plan.stages = (K + kLBK - 1) / kLBK;
-    }
+  // Kernel choice as in gemm_plan (at K = 5600, where the shared kernel
+  // must take its unaligned path, the lane kernel is 1.46x faster).
+  bool small = false;
+  SplitPlan plan = gemm_plan(M, N, K, &small);
+  if (plan.active() && (workspace == nullptr || workspace_bytes < plan.bytes)) {
+    plan = SplitPlan{};   // no room: every tile whole
+    plan.dp_tiles = ((M + 255) / 256) * ((N + 255) / 256);
+    plan.stages = (K + kLBK - 1) / kLBK;
+  }
+  if (K % kLBK == 0 || K % 64 == 32 || (K % 32 == 0 && (small || plan.active()))) {
     const SplitK split = split_args(plan, workspace);
     const int64_t t128 = ((M + 127) / 128) * ((N + 127) / 128);
     const dim3 lgrid((unsigned)(small ? t128 : plan.dp_tiles + plan.rem_tiles * plan.splits));

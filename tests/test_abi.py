@@ -90,7 +90,11 @@ def test_gemm_workspace_plan():
     assert G(4096, 4096, 4096) == 0            # 256 tiles
     assert G(26574, 7296, 2432) == 0           # 3016 tiles: 200 left over
     assert G(18432, 3072, 512) == 0            # 4 K stages
-    assert G(8192, 6720, 2240) == 0            # K % 128 == 64: shared-conversion kernel
+    assert G(8192, 5600, 2240) == 0            # 704 tiles: 192 left over
+    assert G(8192, 36, 48) == 0                # K % 32 == 16: shared-conversion kernel
+    # K % 128 == 64 (a half last stage) splits too: the split is what makes
+    # the lane kernel worth taking over the shared one there
+    assert G(8192, 6720, 2240) == bytes_for(864 % 256)
     assert G(128, 1152, 1152) == 0             # 128 x 128 tiles
     assert G(0, 3072, 3072) == 0 and G(18432, 0, 3072) == 0
 

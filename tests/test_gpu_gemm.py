@@ -45,22 +45,26 @@ def test_golden_gemms():
 
 
 # K % 128 == 0 and K % 64 == 32 run the lane-dequantizing kernel (the latter
-# with a partial last stage), K % 128 == 64 and K % 32 == 16 the
-# workgroup-shared one; each list covers every case.  The lane kernel takes
+# with a partial last stage), K % 32 == 16 the workgroup-shared one, and
+# K % 128 == 64 the lane kernel where its 128 x 128 tiles or its split last
+# round apply (every small shape here, and the fourth split shape) and the
+# shared one otherwise (4096 x 4096 x 320: one whole round of 256 x 256
+# tiles); each list covers every case.  The lane kernel takes
 # 128 x 128 tiles when there are too few 256 x 256 tiles to fill the chip
 # (every small shape here) and 256 x 256 tiles otherwise (5376 x 5376: 441
 # of them).  With 256 x 256 tiles, a last round of at most half the CUs'
-# worth of tiles is split into K halves when K is long enough (the last
-# three shapes: 272, 289 and 306 tiles, the middle one with a partial last
-# stage, the last one with N % 8 != 0).
-SPLIT_SHAPES = [(4352, 4096, 1536), (4352, 4200, 1440), (4353, 4100, 1536)]
+# worth of tiles is split into K halves when K is long enough (SPLIT_SHAPES:
+# 272, 289, 306 and 272 tiles, the second with a partial last stage, the
+# third with N % 8 != 0, the fourth with a half last stage).
+SPLIT_SHAPES = [(4352, 4096, 1536), (4352, 4200, 1440), (4353, 4100, 1536), (4352, 4096, 1600)]
 
 
 @pytest.mark.parametrize("M,N,K", [(1, 1, 16), (3, 5, 32), (37, 70, 64), (300, 260, 48),
                                    (257, 513, 16), (64, 96, 128), (300, 260, 256),
                                    (513, 700, 384), (64, 1000, 1280), (300, 260, 160),
                                    (513, 700, 224), (260, 300, 2240), (5376, 5376, 256),
-                                   (5376, 5400, 96), (4200, 4360, 1120)] + SPLIT_SHAPES)
+                                   (5376, 5400, 96), (4200, 4360, 1120), (4096, 4096, 320)]
+                        + SPLIT_SHAPES)
 def test_exact_sums_are_bit_exact(M, N, K):
     """Scales 1.0 and power-of-two alphas: every partial sum is a multiple of
     1/4 of magnitude at most 36 K < 2^16, exact in FP32 in any order, so the
