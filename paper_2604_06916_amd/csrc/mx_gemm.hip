@@ -71,33 +71,42 @@ __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
 }
 
 // The 16 scale bytes of one row for stages 4 grp .. 4 grp + 3 (byte 4 j + i
-// is kgroup i of stage 4 grp + j).  kFast: K % 128 == 0, so the bytes of every
+// is kgroup i of stage 4 grp + j), one 16-byte load: buffer loads read
+// correctly at any byte offset.  kFast: K % 128 == 0, so the bytes of every
 // stage that is computed lie inside the row (a group reaching past K only
-// covers stages that are never computed).  Otherwise byte loads, with kgroups
-// past K zeroed (a stray 0xFF byte would be NaN).
-template <bool kFast, bool kK512>
+// covers stages that are never computed), and with rows of a multiple of 4
+// bytes every 4-byte word of the load lies inside the operand's range or
+// past it.  Otherwise kgroups past K are zeroed (a stray 0xFF byte would be
+// NaN), and the range check, which drops a whole word straddling the end of
+// the range, would drop in-range bytes of the one lane whose group reaches
+// past the operand's last scale byte: that lane loads bytes instead.
+template <bool kFast>
 __device__ __forceinline__ u32x4_t load_scale_group(__amdgpu_buffer_rsrc_t src, uint32_t off,
-                                                    int64_t kgroups, int grp) {
-  if (kFast && kK512) return __builtin_amdgcn_raw_buffer_load_b128(src, off, 0, 0);
-  if (kFast) {
-    u32x4_t v;
-    v.x = __builtin_amdgcn_raw_buffer_load_b32(src, off, 0, 0);
-    v.y = __builtin_amdgcn_raw_buffer_load_b32(src, off + 4, 0, 0);
-    v.z = __builtin_amdgcn_raw_buffer_load_b32(src, off + 8, 0, 0);
-    v.w = __builtin_amdgcn_raw_buffer_load_b32(src, off + 12, 0, 0);
-    return v;
-  }
-  uint32_t w[4] = {0, 0, 0, 0};
+                                                    int64_t kgroups, int grp, uint32_t range) {
+  if (kFast) return __builtin_amdgcn_raw_buffer_load_b128(src, off, 0, 0);
+  u32x4_t v;
+  if (off + 16 <= range || off >= range) {
+    v = __builtin_amdgcn_raw_buffer_load_b128(src, off, 0, 0);
+  } else {
+    uint32_t w[4] = {0, 0, 0, 0};
 #pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    const uint32_t b = __builtin_amdgcn_raw_buffer_load_b8(src, off + i, 0, 0);
-    w[i / 4] |= ((int64_t)grp * 16 + i < kgroups ? b : 0u) << (8 * (i % 4));
+    for (int i = 0; i < 16; ++i)
+      w[i / 4] |= __builtin_amdgcn_raw_buffer_load_b8(src, off + i, 0, 0) << (8 * (i % 4));
+    v = u32x4_t{w[0], w[1], w[2], w[3]};
   }
-  return u32x4_t{w[0], w[1], w[2], w[3]};
+  const int64_t valid = kgroups - (int64_t)grp * 16;   // bytes of this group inside K
+  if (valid < 16) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int64_t n = valid - 4 * q;                  // valid bytes of word q
+      v[q] &= n >= 4 ? 0xFFFFFFFFu : n <= 0 ? 0u : (1u << (8 * n)) - 1u;
+    }
+  }
+  return v;
 }
 
 
-template <bool kFast, bool kVecOut, bool kK512, int kWT>
+template <bool kFast, bool kVecOut, int kWT>
 __global__ __launch_bounds__(kMxThreads, 1) void mxfp4_gemm_kernel(
     const uint8_t* __restrict__ a_codes, const uint8_t* __restrict__ a_scales,
     const uint8_t* __restrict__ b_codes, const uint8_t* __restrict__ b_scales,
@@ -141,8 +150,10 @@ __global__ __launch_bounds__(kMxThreads, 1) void mxfp4_gemm_kernel(
   const int64_t valid_b = min<int64_t>(N - n0, kT);
   const __amdgpu_buffer_rsrc_t rca = uniform_rsrc(a_codes + m0 * row_bytes, valid_a * row_bytes);
   const __amdgpu_buffer_rsrc_t rcb = uniform_rsrc(b_codes + n0 * row_bytes, valid_b * row_bytes);
-  const __amdgpu_buffer_rsrc_t rsa = uniform_rsrc(a_scales + m0 * kgroups, valid_a * kgroups);
-  const __amdgpu_buffer_rsrc_t rsb = uniform_rsrc(b_scales + n0 * kgroups, valid_b * kgroups);
+  const uint32_t range_sa = (uint32_t)(valid_a * kgroups);
+  const uint32_t range_sb = (uint32_t)(valid_b * kgroups);
+  const __amdgpu_buffer_rsrc_t rsa = uniform_rsrc(a_scales + m0 * kgroups, range_sa);
+  const __amdgpu_buffer_rsrc_t rsb = uniform_rsrc(b_scales + n0 * kgroups, range_sb);
 
   // Code DMA: wave w fills 16-row groups 4 w .. 4 w + 3 of each operand.  In
   // one instruction lane quad l/4 reads the 64 contiguous bytes of row l/4 of
@@ -200,8 +211,8 @@ __global__ __launch_bounds__(kMxThreads, 1) void mxfp4_gemm_kernel(
     }
   };
   auto load_group = [&](int grp) {
-    gsa = load_scale_group<kFast, kK512>(rsa, sg_off + 16 * grp, kgroups, grp);
-    gsb = load_scale_group<kFast, kK512>(rsb, sg_off + 16 * grp, kgroups, grp);
+    gsa = load_scale_group<kFast>(rsa, sg_off + 16 * grp, kgroups, grp, range_sa);
+    gsb = load_scale_group<kFast>(rsb, sg_off + 16 * grp, kgroups, grp, range_sb);
   };
   auto store_group = [&](int set) {
     if (row_thread) {
@@ -409,26 +420,22 @@ hipError_t launch_mx_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const
   const bool small = small_tiles_pay(t256, t128);
   const dim3 grid((unsigned)(small ? t128 : t256)), block(kMxThreads);
   const bool fast = K % kMxBK == 0;
-  const bool k512 = K % 512 == 0;
   const bool vec = N % 8 == 0;
-#define SOLFP4_MX_LAUNCH(F, V, W)                                                              \
+#define SOLFP4_MX_LAUNCH(F, V)                                                                 \
   do {                                                                                         \
     if (small)                                                                                 \
-      hipLaunchKernelGGL((mxfp4_gemm_kernel<F, V, W, 64>), grid, block, 0, stream, a_codes,   \
+      hipLaunchKernelGGL((mxfp4_gemm_kernel<F, V, 64>), grid, block, 0, stream, a_codes,      \
                          a_scales, b_codes, b_scales, bias, out, M, N, K);                     \
     else                                                                                       \
-      hipLaunchKernelGGL((mxfp4_gemm_kernel<F, V, W, 128>), grid, block, 0, stream, a_codes,  \
+      hipLaunchKernelGGL((mxfp4_gemm_kernel<F, V, 128>), grid, block, 0, stream, a_codes,     \
                          a_scales, b_codes, b_scales, bias, out, M, N, K);                     \
   } while (0)
-  if (fast && k512) {
-    if (vec) SOLFP4_MX_LAUNCH(true, true, true);
-    else SOLFP4_MX_LAUNCH(true, false, true);
-  } else if (fast) {
-    if (vec) SOLFP4_MX_LAUNCH(true, true, false);
-    else SOLFP4_MX_LAUNCH(true, false, false);
+  if (fast) {
+    if (vec) SOLFP4_MX_LAUNCH(true, true);
+    else SOLFP4_MX_LAUNCH(true, false);
   } else {
-    if (vec) SOLFP4_MX_LAUNCH(false, true, false);
-    else SOLFP4_MX_LAUNCH(false, false, false);
+    if (vec) SOLFP4_MX_LAUNCH(false, true);
+    else SOLFP4_MX_LAUNCH(false, false);
   }
 #undef SOLFP4_MX_LAUNCH
   return hipGetLastError();

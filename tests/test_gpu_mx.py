@@ -155,13 +155,17 @@ def test_golden_gemm():
 
 
 # The small shapes run on 128 x 128 tiles, (4200, 4360, K) and (6000, 6152,
-# 1024) on 256 x 256 ones (ragged M and N); K = 1152 (K % 512 != 0) fetches
-# scale groups as four 4-byte loads, which the compiler may merge into one
-# (a stage-end wait that counted them as four let the previous stage's loads
-# still be in flight)
+# 1024) on 256 x 256 ones (ragged M and N).  Scale groups (16 bytes of a row)
+# are one 16-byte load; with K % 128 != 0 (K = 96, 2240) rows start at any
+# byte offset and the lane of an operand's last row whose group reaches past
+# the range loads bytes instead, on both tile sizes.  K = 1152 (K % 512 !=
+# 0) once fetched groups as four 4-byte loads that the compiler merged (a
+# stage-end wait that counted them as four let the previous stage's loads
+# still be in flight).
 @pytest.mark.parametrize("M,N,K", [(1, 1, 32), (3, 5, 64), (37, 70, 128), (300, 260, 96),
                                    (257, 513, 32), (64, 96, 512), (260, 300, 1152),
-                                   (4200, 4360, 1024), (6000, 6152, 1024), (4200, 4360, 1152)])
+                                   (4200, 4360, 1024), (6000, 6152, 1024), (4200, 4360, 1152),
+                                   (300, 260, 2240), (4200, 4360, 2240), (4201, 4359, 96)])
 def test_exact_sums_are_bit_exact(M, N, K):
     """Scales 2^-2 and 2^3: every partial sum is a multiple of 1/2 below
     2^17, exact in FP32, so the only rounding is the final BF16."""
