@@ -574,6 +574,14 @@ __global__ __launch_bounds__(kLThreads, 1) void nvfp4_gemm_lane_kernel(
           rcb, (lds_ptr_t)(bbuf[buf] + (kGw * wave + j) * 1024), 16, off, 0, 0, 1);
     }
   };
+  // group j of the DMA of `stage` (2 of its kDma instructions)
+  auto dma_part = [&](int buf, int stage, int j) {
+    const uint32_t off = dma_off + (uint32_t)stage * kLRowBytes + j * group_stride;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(
+        rca, (lds_ptr_t)(abuf[buf] + (kGw * wave + j) * 1024), 16, off, 0, 0, 1);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(
+        rcb, (lds_ptr_t)(bbuf[buf] + (kGw * wave + j) * 1024), 16, off, 0, 0, 1);
+  };
   // one stage's scale bytes of this thread's A and B rows, in flight
   const uint32_t range_a = (uint32_t)(valid_a * scale_row);
   const uint32_t range_b = (uint32_t)(valid_b * scale_row);
@@ -724,9 +732,9 @@ __global__ __launch_bounds__(kLThreads, 1) void nvfp4_gemm_lane_kernel(
   __builtin_amdgcn_s_barrier();
   convert(J0{}, sca[0], scb[0], 0);
 
-  // Stage s with P = s % 4 (buffer P, scale parity C = P % 2).  K-step 0
-  // issues the DMA of stage s+3 into buffer (P + 3) % 4 (last read in stage
-  // s-1), parks the scales of stage s+2 in set C (last read in stage s-1,
+  // Stage s with P = s % 4 (buffer P, scale parity C = P % 2).  K-steps 0
+  // .. kGw-1 issue the DMA of stage s+3 into buffer (P + 3) % 4 (last read in
+  // stage s-1); K-step 0 parks the scales of stage s+2 in set C (last read in stage s-1,
   // next read in stage s+1) and fetches those of stage s+3, and reads this
   // stage's second code half; K-step 4 reads the next stage's first code
   // half and scales; K-step 7 converts the next stage's K-step 0.  The
@@ -741,23 +749,31 @@ __global__ __launch_bounds__(kLThreads, 1) void nvfp4_gemm_lane_kernel(
     // fewer instructions than written)
     store_scales(sf, C, s + 2);
     fetch_scales(sf, s + 3);
-    dma_stage((P + 3) % kLBufs, s + 3);
+    // the DMA of stage s+3 goes out a group (2 instructions) per K-step over
+    // K-steps 0 .. kGw-1: issued at once, the 8 instructions of a 128 x 128
+    // wave tile filled the texture addresser's queues and held up the MFMA
+    // issue behind them (3% slower)
+    using I2 = std::integral_constant<int, 2>;
+    dma_part((P + 3) % kLBufs, s + 3, 0);
     read_codes(1, P);
     mfma_step(0);
     convert(J1{}, sca[C], scb[C], 1);
-    interleave(I4{}, std::integral_constant<int, kDma + kSL>{}, I8{});
+    interleave(I4{}, std::integral_constant<int, 2 + kSL>{}, I8{});
     __builtin_amdgcn_sched_barrier(0);
+    dma_part((P + 3) % kLBufs, s + 3, 1);
     mfma_step(1);
     convert(J2{}, sca[C], scb[C], 0);
-    interleave(I0{}, I0{}, I0{});
+    interleave(I0{}, I2{}, I0{});
     __builtin_amdgcn_sched_barrier(0);
+    if (kGw > 2) dma_part((P + 3) % kLBufs, s + 3, 2);
     mfma_step(0);
     convert(J3{}, sca[C], scb[C], 1);
-    interleave(I0{}, I0{}, I0{});
+    interleave(I0{}, std::integral_constant<int, (kGw > 2 ? 2 : 0)>{}, I0{});
     __builtin_amdgcn_sched_barrier(0);
+    if (kGw > 3) dma_part((P + 3) % kLBufs, s + 3, 3);
     mfma_step(1);
     convert(J4{}, sca[C], scb[C], 0);
-    interleave(I0{}, I0{}, I0{});
+    interleave(I0{}, std::integral_constant<int, (kGw > 3 ? 2 : 0)>{}, I0{});
     __builtin_amdgcn_sched_barrier(0);
     read_codes(0, (P + 1) % kLBufs);
     read_scales(sca[C ^ 1], scb[C ^ 1], s + 1);
