@@ -89,10 +89,20 @@ def measured_traffic(summary, source):
     return float(kv["hbm_bytes_per_launch_avg"])
 
 
-def nvfp4_gemm_kernel_name(K):
-    """The kernel nvfp4_gemm launches for this K (the library's dispatch:
-    lane-side dequantization for K % 128 == 0 and K % 64 == 32)."""
-    return "nvfp4_gemm_lane_kernel" if K % 128 == 0 or K % 64 == 32 else "nvfp4_gemm_kernel"
+def nvfp4_gemm_kernel_name(M, N, K, cus=256):
+    """The kernel nvfp4_gemm launches for this shape (the library's dispatch:
+    lane-side dequantization for K % 128 == 0 and K % 64 == 32, and for
+    K % 128 == 64 where 128 x 128 tiles or the split last round apply)."""
+    import paper_2604_06916_amd as sol
+    if K % 128 == 0 or K % 64 == 32:
+        return "nvfp4_gemm_lane_kernel"
+    if K % 32:
+        return "nvfp4_gemm_kernel"
+    t256 = -(-M // 256) * -(-N // 256)
+    t128 = -(-M // 128) * -(-N // 128)
+    small = -(-t128 // cus) * 0.46 < -(-t256 // cus)
+    split = sol.nvfp4_gemm_workspace_bytes(M, N, K) > 0
+    return "nvfp4_gemm_lane_kernel" if small or split else "nvfp4_gemm_kernel"
 
 
 def vendor_mxfp4(layers, bufs, steps):
@@ -532,7 +542,7 @@ def main():
         },
         "roofline": {
             "bound": "mfma",
-            "kernel": " + ".join(sorted({nvfp4_gemm_kernel_name(L["K"]) for L in layers})),
+            "kernel": " + ".join(sorted({nvfp4_gemm_kernel_name(L["M"], L["N"], L["K"]) for L in layers})),
             "achieved": round(gemm_tflops, 1),
             "peak": PEAK_FP16_MFMA_TFLOPS,
             "unit": "TFLOP/s",

@@ -58,3 +58,16 @@ def test_paper_context_is_marked_not_comparable():
         assert abs(naive / ours - ctx["rollout_speedup"][model]) < 0.01
     for model, (naive, ours) in ctx["end_to_end_s"].items():
         assert abs(naive / ours - ctx["end_to_end_speedup"][model]) < 0.01
+
+
+def test_roofline_kernel_name_follows_the_dispatch():
+    """The name bench.py reports for the NVFP4 GEMM roofline follows the
+    library's kernel choice (the CU count is MI355X's 256 without a GPU)."""
+    import bench
+    lane, shared = "nvfp4_gemm_lane_kernel", "nvfp4_gemm_kernel"
+    for M, N, K in [(18432, 9216, 3072), (18432, 3072, 12288), (8192, 2240, 5600)]:
+        assert bench.nvfp4_gemm_kernel_name(M, N, K) == lane
+    assert bench.nvfp4_gemm_kernel_name(8192, 5600, 2240) == shared   # whole rounds, no split
+    assert bench.nvfp4_gemm_kernel_name(8192, 2240, 2240) == lane     # split last round
+    assert bench.nvfp4_gemm_kernel_name(300, 260, 2240) == lane       # 128 x 128 tiles
+    assert bench.nvfp4_gemm_kernel_name(300, 260, 48) == shared       # K % 32 == 16
