@@ -22,10 +22,13 @@
 // FP16 subnormals) gives q * s exactly.
 //
 // Two kernels:
-//   nvfp4_gemm_lane_kernel (K % 128 == 0 or K % 64 == 32): codes travel
+//   nvfp4_gemm_lane_kernel (K % 128 == 0 or K % 64 == 32, and K % 128 == 64
+//     where its 128 x 128 tiles or its split last round apply): codes travel
 //     from HBM into LDS by DMA and each wave dequantizes its own MFMA operands
 //     in registers, so LDS carries 0.5 B/element of codes instead of 2 B of
-//     FP16 per operand read;
+//     FP16 per operand read; with too few tiles for one 256 x 256 tile per
+//     CU it runs on 128 x 128 tiles, and a last round of at most half the
+//     CUs' worth of tiles runs as two K halves per tile (SplitK);
 //   nvfp4_gemm_kernel (the other K % 16 == 0): the workgroup converts each
 //     stage once into FP16 tiles in LDS, which all waves read.
 #include <type_traits>
