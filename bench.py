@@ -41,8 +41,8 @@ MX_QUANT_BYTES = 2.53125
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="flux-12b")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-mxfp4", action="store_true", help="skip the MXFP4 variant")
@@ -497,7 +497,8 @@ def main():
     gemm_ms_tot = wq_ms_tot = xq_ms_tot = 0.0
     for i, L in enumerate(layers):
         wq = np.mean([ev[s][i][0].elapsed_time(ev[s][i][1]) for s in range(args.steps)])
-        xq = np.mean([ev[s][i][1].elapsed_time(ev[s][i][2]) for s in range(args.steps)])
+        xqs = np.array([ev[s][i][1].elapsed_time(ev[s][i][2]) for s in range(args.steps)])
+        xq = float(np.mean(xqs))
         gms = np.array([ev[s][i][2].elapsed_time(ev[s][i][3]) for s in range(args.steps)])
         gm = float(np.mean(gms))
         gemm_ms_tot += gm
@@ -510,6 +511,7 @@ def main():
             "gemm_us": round(gm * 1e3, 2), "gemm_tflops": round(fl / (gm * 1e-3) / 1e12, 1),
             "gemm_us_p10_p50_p90": [round(float(np.percentile(gms, q)) * 1e3, 2) for q in (10, 50, 90)],
             "quantize_x_us": round(xq * 1e3, 2),
+            "quantize_x_us_p10_p50_p90": [round(float(np.percentile(xqs, q)) * 1e3, 2) for q in (10, 50, 90)],
             "quantize_x_gbs": round(xbytes / (xq * 1e-3) / 1e9, 1),
             "quantize_w_us": round(wq * 1e3, 2),
         })
