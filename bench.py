@@ -381,6 +381,18 @@ PAPER_CONTEXT = {
 }
 
 
+def cpu_model():
+    """The host CPU's model name (first processor in /proc/cpuinfo)."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(wl, rows, wrows):
     """The CPU oracle on a bounded sample of the same step: per layer, `rows`
     activation rows and `wrows` weight rows at full K (each clipped to the
@@ -406,12 +418,17 @@ def cpu_baseline(wl, rows, wrows):
         secs += time.perf_counter() - t0
         flops += 2.0 * m * n * layer.K
         assert out.shape == (m, n)
-    blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    pools = threadpool_info()
+    blas_threads = max([i.get("num_threads", 1) for i in pools] or [1])
+    blas = sorted({f"{i.get('internal_api', '?')} {i.get('version', '')}".strip()
+                   for i in pools if i.get("user_api") == "blas"})
     return {
         "value": flops / secs / 1e12,
         "unit": "TFLOP/s",
         "cores": int(blas_threads),
         "kind": "oracle",
+        "cpu": cpu_model(),
+        "blas": ", ".join(blas) or "unknown",
         "sample": (f"per layer min({rows}, M) activation rows x min({wrows}, N) weight rows at "
                    f"full K: oracle "
                    f"quantize of both (numpy float32, 1 thread) + float64 GEMM (BLAS, "

@@ -27,6 +27,7 @@ def test_cpu_baseline_leg_on_a_tiny_sample():
     assert cb["kind"] == "oracle" and cb["unit"] == "TFLOP/s"
     assert cb["value"] > 0 and cb["cores"] >= 1
     assert "min(8, M) activation rows x min(16, N) weight rows" in cb["sample"]
+    assert cb["cpu"] and cb["blas"]
 
 
 def test_cpu_baseline_clips_the_sample_to_the_layer():
