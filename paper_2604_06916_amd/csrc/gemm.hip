@@ -985,7 +985,8 @@ bool small_tiles_pay(int64_t tiles256, int64_t tiles128) {
   return small < big;
 }
 
-SplitPlan plan_split(int64_t tiles, int64_t nstages, double fixed_cost, double part_cost) {
+SplitPlan plan_split(int64_t tiles, int64_t nstages, double fixed_cost, double part_cost,
+                     size_t part_tile_bytes) {
   SplitPlan plan;
   plan.dp_tiles = tiles;
   plan.stages = nstages;
@@ -1002,7 +1003,7 @@ SplitPlan plan_split(int64_t tiles, int64_t nstages, double fixed_cost, double p
   plan.splits = 2;
   plan.rem_tiles = rem;
   plan.dp_tiles = tiles - rem;
-  plan.bytes = ((size_t)rem * 8 + 255) / 256 * 256 + (size_t)(rem * plan.splits) * kPartTileBytes;
+  plan.bytes = ((size_t)rem * 8 + 255) / 256 * 256 + (size_t)(rem * plan.splits) * part_tile_bytes;
   return plan;
 }
 
@@ -1029,8 +1030,18 @@ SplitK split_args(const SplitPlan& plan, void* workspace) {
 #ifndef SOLFP4_SPLIT_PART
 #define SOLFP4_SPLIT_PART 2.5
 #endif
+// The same for 128 x 128 tiles, in units of their own (latency-bound) stage:
+// fitted to the measured gain of the split on the 128-token 3072 -> 3072
+// (1.32x), 128-token 1152 -> 1152 at K = 4608 (1.49x), 512-token 2240 ->
+// 2240 (1.16x) and 128-token 1152 -> 1152 (none) layers.
+#ifndef SOLFP4_SPLIT_FIXED_SMALL
+#define SOLFP4_SPLIT_FIXED_SMALL 9.0
+#endif
+#ifndef SOLFP4_SPLIT_PART_SMALL
+#define SOLFP4_SPLIT_PART_SMALL 2.0
+#endif
 
-// The lane kernel on 256 x 256 tiles is the one that splits.
+// The lane kernel is the one that splits, on either tile size.
 // The lane kernel takes K % 128 == 0 and K % 64 == 32 always.  At
 // K % 128 == 64 (a half last stage) the workgroup-shared kernel is 1-2%
 // faster on whole rounds of 256 x 256 tiles (the 8192-token 2240 -> 6720
@@ -1044,9 +1055,12 @@ static SplitPlan gemm_plan(int64_t M, int64_t N, int64_t K, bool* small_out) {
   const int64_t t128 = ((M + 127) / 128) * ((N + 127) / 128);
   const bool small = lane_ok && small_tiles_pay(t256, t128);
   if (small_out) *small_out = small;
-  plan.dp_tiles = t256;
-  if (!lane_ok || small) return plan;
-  return plan_split(t256, (K + kLBK - 1) / kLBK, SOLFP4_SPLIT_FIXED, SOLFP4_SPLIT_PART);
+  plan.dp_tiles = small ? t128 : t256;
+  if (!lane_ok) return plan;
+  const int64_t nstages = (K + kLBK - 1) / kLBK;
+  if (small)
+    return plan_split(t128, nstages, SOLFP4_SPLIT_FIXED_SMALL, SOLFP4_SPLIT_PART_SMALL, 128 * 128 * 4);
+  return plan_split(t256, nstages, SOLFP4_SPLIT_FIXED, SOLFP4_SPLIT_PART, 256 * 256 * 4);
 }
 
 size_t gemm_workspace_bytes(int64_t M, int64_t N, int64_t K) {
@@ -1068,17 +1082,16 @@ hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const fl
   SplitPlan plan = gemm_plan(M, N, K, &small);
   if (plan.active() && (workspace == nullptr || workspace_bytes < plan.bytes)) {
     plan = SplitPlan{};   // no room: every tile whole
-    plan.dp_tiles = ((M + 255) / 256) * ((N + 255) / 256);
+    plan.dp_tiles = small ? ((M + 127) / 128) * ((N + 127) / 128) : ((M + 255) / 256) * ((N + 255) / 256);
     plan.stages = (K + kLBK - 1) / kLBK;
   }
   if (K % kLBK == 0 || K % 64 == 32 || (K % 32 == 0 && (small || plan.active()))) {
     const SplitK split = split_args(plan, workspace);
-    const int64_t t128 = ((M + 127) / 128) * ((N + 127) / 128);
-    const dim3 lgrid((unsigned)(small ? t128 : plan.dp_tiles + plan.rem_tiles * plan.splits));
+    const dim3 lgrid((unsigned)(plan.dp_tiles + plan.rem_tiles * plan.splits));
 #define SOLFP4_LANE_LAUNCH(V, F, W)                                                           \
   hipLaunchKernelGGL((nvfp4_gemm_lane_kernel<V, F, W>), lgrid, dim3(kLThreads), 0, stream,     \
                      a_codes, a_scales, a_gs, b_codes, b_scales, b_gs, bias, out, M, N, K,     \
-                     small ? SplitK{nullptr, nullptr, (int)t128, 1, 0} : split)
+                     split)
     const bool full = K % kLBK == 0;
     if (small) {
       if (vec && full) SOLFP4_LANE_LAUNCH(true, true, 64);

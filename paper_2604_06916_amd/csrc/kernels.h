@@ -37,7 +37,8 @@ bool small_tiles_pay(int64_t tiles256, int64_t tiles128);
 // This works whatever the slot held before the launch (other than one of
 // the two tokens), so the workspace needs no clearing between calls.
 struct SplitK {
-  float* part;          // two 256 KB partial tiles per remainder tile
+  float* part;          // two FP32 partial tiles per remainder tile (2 x 256 KB
+                        // for 256 x 256 tiles, 2 x 64 KB for 128 x 128)
   uint64_t* slots;      // one per remainder tile: 0 after every launch, or
                         // the token of the half that finished first
   int dp_tiles;         // workgroups that take whole tiles (all of them: no split)
@@ -51,13 +52,14 @@ struct SplitPlan {
   bool active() const { return splits > 1; }
 };
 
-// The plan for `tiles` 256 x 256 tiles of `nstages` K stages each: split
-// the remainder tiles when the estimated last round, ceil(nstages / 2) +
+// The plan for `tiles` output tiles of `nstages` K stages each: split the
+// remainder tiles when the estimated last round, ceil(nstages / 2) +
 // fixed_cost + 2 part_cost stages (a half, then writing its partial tile
-// and reading the other's), beats nstages + fixed_cost.
-SplitPlan plan_split(int64_t tiles, int64_t nstages, double fixed_cost, double part_cost);
+// and reading the other's), beats nstages + fixed_cost.  A tile's FP32
+// partial sums take part_tile_bytes.
+SplitPlan plan_split(int64_t tiles, int64_t nstages, double fixed_cost, double part_cost,
+                     size_t part_tile_bytes);
 SplitK split_args(const SplitPlan& plan, void* workspace);
-constexpr size_t kPartTileBytes = 256 * 256 * 4;
 // token of half h of remainder tile r: kSplitToken ^ (2 r + h), never 0
 constexpr uint64_t kSplitToken = 0xC6A4A7935BD1E995ull;
 

@@ -73,13 +73,16 @@ def test_workspace_queries():
 def test_gemm_workspace_plan():
     """Which shapes split their last round's tiles into two K halves, and
     the workspace that takes (an 8-byte slot per remainder tile, 256-byte
-    aligned, then two 256 KB FP32 partial tiles per tile).  Without a GPU
-    the CU count is MI355X's 256."""
+    aligned, then two FP32 partial tiles per tile: 256 KB each for 256 x 256
+    tiles, 64 KB for 128 x 128).  Without a GPU the CU count is MI355X's
+    256."""
     G = sol.nvfp4_gemm_workspace_bytes
-    part = 256 * 256 * 4
 
-    def bytes_for(rem):
+    def bytes_for(rem, part=256 * 256 * 4):
         return (rem * 8 + 255) // 256 * 256 + rem * 2 * part
+
+    def small_bytes_for(rem):
+        return bytes_for(rem, 128 * 128 * 4)
     # FLUX.1 layers, 18432 tokens: 2592, 864, 3456 and 864 tiles of 256 x 256
     assert G(18432, 9216, 3072) == bytes_for(2592 % 256)
     assert G(18432, 3072, 3072) == bytes_for(864 % 256)
@@ -95,7 +98,13 @@ def test_gemm_workspace_plan():
     # K % 128 == 64 (a half last stage) splits too: the split is what makes
     # the lane kernel worth taking over the shared one there
     assert G(8192, 6720, 2240) == bytes_for(864 % 256)
-    assert G(128, 1152, 1152) == 0             # 128 x 128 tiles
+    # 128 x 128 tiles split as well, given enough K stages: 24 tiles of 24
+    # stages, 9 of 36 and 72 of 18 do; the 128-token 1152 -> 1152 layer's 9
+    # tiles of 9 stages gain nothing
+    assert G(128, 3072, 3072) == small_bytes_for(24)
+    assert G(128, 1152, 4608) == small_bytes_for(9)
+    assert G(512, 2240, 2240) == small_bytes_for(72)
+    assert G(128, 1152, 1152) == 0
     assert G(0, 3072, 3072) == 0 and G(18432, 0, 3072) == 0
 
 

@@ -57,6 +57,9 @@ def test_golden_gemms():
 # 272, 289, 306 and 272 tiles, the second with a partial last stage, the
 # third with N % 8 != 0, the fourth with a half last stage).
 SPLIT_SHAPES = [(4352, 4096, 1536), (4352, 4200, 1440), (4353, 4100, 1536), (4352, 4096, 1600)]
+# 128 x 128 tiles split too when K is long: 24 tiles of 24 stages, 9 of 36,
+# 72 of 18 (a half last stage), and a ragged 3 x 7 tiles with N % 8 != 0
+SMALL_SPLIT_SHAPES = [(128, 3072, 3072), (128, 1152, 4608), (512, 2240, 2240), (300, 836, 4096)]
 
 
 @pytest.mark.parametrize("M,N,K", [(1, 1, 16), (3, 5, 32), (37, 70, 64), (300, 260, 48),
@@ -64,7 +67,7 @@ SPLIT_SHAPES = [(4352, 4096, 1536), (4352, 4200, 1440), (4353, 4100, 1536), (435
                                    (513, 700, 384), (64, 1000, 1280), (300, 260, 160),
                                    (513, 700, 224), (260, 300, 2240), (5376, 5376, 256),
                                    (5376, 5400, 96), (4200, 4360, 1120), (4096, 4096, 320)]
-                        + SPLIT_SHAPES)
+                        + SPLIT_SHAPES + SMALL_SPLIT_SHAPES)
 def test_exact_sums_are_bit_exact(M, N, K):
     """Scales 1.0 and power-of-two alphas: every partial sum is a multiple of
     1/4 of magnitude at most 36 K < 2^16, exact in FP32 in any order, so the
@@ -188,7 +191,7 @@ def test_zero_k_writes_bias():
     assert np.array_equal(bf16_from_dev(out), np.broadcast_to(bias, (M, N)))
 
 
-@pytest.mark.parametrize("M,N,K", SPLIT_SHAPES)
+@pytest.mark.parametrize("M,N,K", SPLIT_SHAPES + SMALL_SPLIT_SHAPES)
 def test_split_last_round_vs_oracle(M, N, K):
     """The last round's tiles as two K halves: within the bar of the oracle,
     and the same bits on a second call (the workspace is reused, its
@@ -219,11 +222,11 @@ def test_split_last_round_vs_oracle(M, N, K):
     assert bf16_mismatch_fraction(outs[0], ref) <= 0.01
 
 
-def test_split_gemm_in_a_replayed_graph():
+@pytest.mark.parametrize("M,N,K", [SPLIT_SHAPES[0], SMALL_SPLIT_SHAPES[0]])
+def test_split_gemm_in_a_replayed_graph(M, N, K):
     """A split GEMM captured once and replayed: the tile slots left by each
     replay (and by the eager calls between replays) must not confuse the
     next; every replay equals the eager result bit for bit."""
-    M, N, K = SPLIT_SHAPES[0]
     ac, as_, aa = quantized("normal", M, K, 17)
     bc, bs, ba = quantized(None, N, K, 19, sigma=0.02)
     args = [u8_to_dev(ac), u8_to_dev(as_), f32_to_dev(aa), u8_to_dev(bc), u8_to_dev(bs),

@@ -12,10 +12,12 @@ from workloads import draw_activations, draw_bias, draw_weights
 pytestmark = pytest.mark.gpu
 
 
-# 4352 x 4096 x 1536: the GEMM's last round splits into K halves, through the
-# part of the linear's workspace after the activation codes
+# 4352 x 4096 x 1536 and 128 x 3072 x 3072: the GEMM's last round splits into
+# K halves (256 x 256 and 128 x 128 tiles), through the part of the linear's
+# workspace after the activation codes
 @pytest.mark.parametrize("M,N,K", [(1, 16, 16), (7, 33, 48), (128, 1152, 1152), (300, 520, 2240),
-                                   (517, 260, 5600), (1000, 3072, 3072), (4352, 4096, 1536)])
+                                   (517, 260, 5600), (1000, 3072, 3072), (4352, 4096, 1536),
+                                   (128, 3072, 3072)])
 @pytest.mark.parametrize("with_bias", [False, True])
 def test_linear_matches_quantize_then_gemm_and_oracle(M, N, K, with_bias):
     xb = draw_activations("t3_1pct", M, K, seed=M + K)
