@@ -127,12 +127,13 @@ SOLFP4_API int nvfp4_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const
 /*
  * Device workspace, in bytes, that nvfp4_gemm uses for an M x N x K product
  * on the current device (host only; 0 for invalid sizes).  The GEMM runs
- * one workgroup per 256 x 256 output tile, about ceil(tiles / CUs) rounds
- * of one tile's time; when the last round holds few tiles, each of those is
+ * one workgroup per 256 x 256 output tile (128 x 128 when there are too few
+ * of those to fill the device), about ceil(tiles / CUs) rounds of one
+ * tile's time; when the last round holds few tiles, each of those is
  * computed as two K halves by two workgroups, which add their FP32 partial
- * sums through this workspace (one 256 KB partial tile per half, plus an
- * 8-byte slot per tile that tells the second half to finish that it is
- * second).  0 means the shape runs without it.
+ * sums through this workspace (one partial tile per half: 256 KB, or 64 KB
+ * for 128 x 128 tiles; plus an 8-byte slot per tile that tells the second
+ * half to finish that it is second).  0 means the shape runs without it.
  *
  * nvfp4_gemm's workspace argument:
  *   NULL       no split (workspace_bytes is ignored)
