@@ -324,9 +324,10 @@ def run_small_linear(reps):
 
 def run_stage1():
     """Synthetic Stage-1 rollouts (8 blocks of the FLUX-like width, 8 rollouts
-    x 4608 tokens, 6 Euler steps, reward, top/bottom selection) with every
-    linear on each backend: rollout time, the linears' share of it (HIP
-    events around every linear) and the speed-up over BF16 linears."""
+    x 4608 tokens, 4 Euler steps, reward, top/bottom selection) with every
+    linear on each backend: rollout time, the linears' time, TFLOP/s and
+    share (HIP events around every linear), the other ops' time by kind, and
+    the speed-ups over BF16 linears (whole rollout, and linears alone)."""
     import torch
 
     from paper_2604_06916_amd import stage1 as G
@@ -335,10 +336,12 @@ def run_stage1():
     model = G.make_weights(cfg, dev)
     x0 = G.initial_latents(cfg, dev)
     u = G.reward_direction(cfg)
+    lin_flops = G.linear_flops(cfg)
     out = {"config": {"blocks": cfg.blocks, "hidden": cfg.hidden, "heads": cfg.heads,
                       "mlp": cfg.mlp, "rollouts": cfg.rollouts, "tokens": cfg.tokens,
                       "euler_steps": cfg.steps, "keep": cfg.keep,
-                      "attention": "BF16, torch fused attention"}}
+                      "attention": "BF16, torch fused attention",
+                      "linear_flops": lin_flops, "attention_flops": G.attention_flops(cfg)}}
     for backend in G.BACKENDS:
         runner = G.Runner(cfg, model, backend, dev)
         warm = G.Stage1Config(**{**cfg.__dict__, "steps": 1})
@@ -347,6 +350,7 @@ def run_stage1():
         runner.cfg = cfg
         torch.cuda.synchronize()
         runner.linear_events = []
+        runner.op_events = {}
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()
         x = runner.rollout(x0)
@@ -355,14 +359,19 @@ def run_stage1():
         torch.cuda.synchronize()
         total = e0.elapsed_time(e1)
         lin = sum(a.elapsed_time(b) for a, b in runner.linear_events)
+        ops = {k: round(sum(a.elapsed_time(b) for a, b in v), 2) for k, v in runner.op_events.items()}
         top, bottom = G.select_rollouts(r.cpu().numpy(), cfg.keep)
         out[backend] = {"rollout_ms": round(total, 2), "linear_ms": round(lin, 2),
+                        "linear_tflops": round(lin_flops / (lin * 1e-3) / 1e12, 1),
                         "linear_share": round(lin / total, 4),
+                        "other_ms": round(total - lin, 2), "other_ms_by_op": ops,
+                        "unattributed_ms": round(total - lin - sum(ops.values()), 2),
                         "top": [int(i) for i in top], "bottom": [int(i) for i in bottom]}
         del runner
         torch.cuda.empty_cache()
     for backend in ("nvfp4", "mxfp4"):
-        out[backend]["speedup_vs_bf16"] = round(out["bf16"]["rollout_ms"] / out[backend]["rollout_ms"], 3)
+        out[backend]["linear_speedup_vs_bf16"] = round(out["bf16"]["linear_ms"] / out[backend]["linear_ms"], 3)
+        out[backend]["rollout_speedup_vs_bf16"] = round(out["bf16"]["rollout_ms"] / out[backend]["rollout_ms"], 3)
     return out
 
 

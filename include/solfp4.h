@@ -170,12 +170,44 @@ SOLFP4_API size_t nvfp4_linear_workspace_bytes(int64_t M, int64_t N, int64_t K);
  *            holds the activation codes at offset 0, then their scales and
  *            alpha (offsets are an implementation detail).
  *
- * The result is bit-identical to nvfp4_quantize followed by nvfp4_gemm.
+ * The result is bit-identical to nvfp4_quantize followed by nvfp4_gemm
+ * with a workspace of at least nvfp4_gemm_workspace_bytes(M, N, K) (the
+ * linear always splits the last round where the GEMM would; nvfp4_gemm
+ * without a workspace runs every tile whole, which may change the last bits
+ * of the affected outputs).
  */
 SOLFP4_API int nvfp4_linear(const uint16_t* x, const uint8_t* w_codes, const uint8_t* w_scales,
                  const float* w_global_scale, const uint16_t* bias, uint16_t* out,
                  void* workspace, size_t workspace_bytes,
                  int64_t M, int64_t N, int64_t K, void* stream);
+
+/*
+ * How a GEMM of this shape runs on the current device (host only; without a
+ * GPU the device is taken to have MI355X's 256 compute units).  The kernel
+ * choice depends only on the shape and the CU count, so callers (a
+ * benchmark naming the kernel it times, a scheduler sizing its streams) can
+ * ask instead of re-deriving it.
+ *
+ *   format          SOLFP4_FORMAT_NVFP4 (nvfp4_gemm) or SOLFP4_FORMAT_MXFP4
+ *                   (mxfp4_gemm)
+ *   with_workspace  nonzero: nvfp4_gemm gets a workspace of at least
+ *                   nvfp4_gemm_workspace_bytes(M, N, K) (ignored for MXFP4)
+ *   kernel          written: one of the SOLFP4_KERNEL_* ids below
+ *   tile            written: output tile edge, 256 or 128
+ *   workgroups      written: workgroups of the launch
+ *   splits          written: K ranges per tile of the last round (1: none)
+ *
+ * Returns SOLFP4_OK, SOLFP4_EINVAL for a null output pointer, a negative
+ * size or an unknown format, or SOLFP4_ESHAPE for a shape the GEMM rejects.
+ * M == 0 or N == 0 writes kernel 0 and workgroups 0 (nothing is launched).
+ */
+#define SOLFP4_FORMAT_NVFP4 0
+#define SOLFP4_FORMAT_MXFP4 1
+#define SOLFP4_KERNEL_NVFP4_LANE 1     /* codes to LDS by DMA, per-wave dequantization */
+#define SOLFP4_KERNEL_NVFP4_SHARED 2   /* workgroup-shared dequantization into LDS */
+#define SOLFP4_KERNEL_MXFP4 3          /* scaled FP4 matrix instructions */
+SOLFP4_API int solfp4_gemm_plan(int format, int64_t M, int64_t N, int64_t K, int with_workspace,
+                     int* kernel, int* tile, int64_t* workgroups, int* splits);
 
 /*
  * MXFP4 variant (Preliminaries: the OCP MX format, E2M1 elements with one

@@ -5,7 +5,8 @@ instructions, as a C-ABI HIP library with a thin Python binding.
 The binding (and so libsolfp4.so) loads on first use of any name below and
 raises ImportError if the library has not been built.
 """
-_NAMES = ("EXPORTED", "LIB_PATH", "Solfp4Error", "lib", "nvfp4_gemm",
+_NAMES = ("EXPORTED", "LIB_PATH", "Solfp4Error", "lib", "gemm_plan", "FORMAT_NVFP4",
+          "FORMAT_MXFP4", "nvfp4_gemm",
           "nvfp4_gemm_workspace_bytes", "nvfp4_linear", "nvfp4_linear_workspace_bytes",
           "nvfp4_quantize", "nvfp4_quantize_workspace_bytes", "mxfp4_gemm", "mxfp4_linear", "mxfp4_linear_workspace_bytes", "mxfp4_quantize")
 __all__ = list(_NAMES)

@@ -140,7 +140,30 @@ const char* solfp4_strerror(int status) {
   }
 }
 
-int solfp4_version(void) { return 100; }
+int solfp4_version(void) { return 200; }
+
+int solfp4_gemm_plan(int format, int64_t M, int64_t N, int64_t K, int with_workspace, int* kernel,
+                     int* tile, int64_t* workgroups, int* splits) {
+  if (!kernel || !tile || !workgroups || !splits) return SOLFP4_EINVAL;
+  if (format != SOLFP4_FORMAT_NVFP4 && format != SOLFP4_FORMAT_MXFP4) return SOLFP4_EINVAL;
+  int rc = check_dims(M, N);
+  if (rc) return rc;
+  rc = check_dims(K, 0);
+  if (rc) return rc;
+  const int64_t block = format == SOLFP4_FORMAT_NVFP4 ? 16 : 32;
+  if (K % block || K >= kMaxGemmK || N >= kMaxN) return SOLFP4_ESHAPE;
+  if (((M + 255) / 256) * ((N + 255) / 256) >= kMaxDim) return SOLFP4_ESHAPE;
+  *kernel = 0;
+  *tile = 256;
+  *workgroups = 0;
+  *splits = 1;
+  if (M == 0 || N == 0) return SOLFP4_OK;
+  if (format == SOLFP4_FORMAT_NVFP4)
+    solfp4::describe_gemm(M, N, K, with_workspace != 0, kernel, tile, workgroups, splits);
+  else
+    solfp4::describe_mx_gemm(M, N, K, kernel, tile, workgroups);
+  return SOLFP4_OK;
+}
 
 size_t nvfp4_quantize_workspace_bytes(int64_t rows, int64_t K) {
   if (check_dims(rows, K) || K % 16) return 0;

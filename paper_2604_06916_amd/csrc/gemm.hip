@@ -34,6 +34,7 @@
 #include <type_traits>
 
 #include "device_common.h"
+#include "solfp4.h"
 #include "kernels.h"
 
 namespace solfp4 {
@@ -1068,6 +1069,20 @@ size_t gemm_workspace_bytes(int64_t M, int64_t N, int64_t K) {
   return gemm_plan(M, N, K, nullptr).bytes;
 }
 
+void describe_gemm(int64_t M, int64_t N, int64_t K, bool with_workspace, int* kernel, int* tile,
+                   int64_t* workgroups, int* splits) {
+  bool small = false;
+  SplitPlan plan = gemm_plan(M, N, K, &small);
+  const bool split = plan.active() && with_workspace;
+  const bool lane = K % kLBK == 0 || K % 64 == 32 || (K % 32 == 0 && (small || split));
+  *kernel = lane ? SOLFP4_KERNEL_NVFP4_LANE : SOLFP4_KERNEL_NVFP4_SHARED;
+  *tile = small ? 128 : 256;
+  *splits = split ? (int)plan.splits : 1;
+  const int64_t tiles = small ? ((M + 127) / 128) * ((N + 127) / 128)
+                              : ((M + 255) / 256) * ((N + 255) / 256);
+  *workgroups = split ? plan.dp_tiles + plan.rem_tiles * plan.splits : tiles;
+}
+
 hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_gs,
                        const uint8_t* b_codes, const uint8_t* b_scales, const float* b_gs,
                        const uint16_t* bias, uint16_t* out, int64_t M, int64_t N, int64_t K,
@@ -1089,39 +1104,34 @@ hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const fl
     const SplitK split = split_args(plan, workspace);
     const dim3 lgrid((unsigned)(plan.dp_tiles + plan.rem_tiles * plan.splits));
 #define SOLFP4_LANE_LAUNCH(V, F, W)                                                           \
-  hipLaunchKernelGGL((nvfp4_gemm_lane_kernel<V, F, W>), lgrid, dim3(kLThreads), 0, stream,     \
-                     a_codes, a_scales, a_gs, b_codes, b_scales, b_gs, bias, out, M, N, K,     \
-                     split)
+  launch_kernel(nvfp4_gemm_lane_kernel<V, F, W>, lgrid, dim3(kLThreads), stream, a_codes,      \
+                a_scales, a_gs, b_codes, b_scales, b_gs, bias, out, M, N, K, split)
     const bool full = K % kLBK == 0;
+    hipError_t e;
     if (small) {
-      if (vec && full) SOLFP4_LANE_LAUNCH(true, true, 64);
-      else if (full) SOLFP4_LANE_LAUNCH(false, true, 64);
-      else if (vec) SOLFP4_LANE_LAUNCH(true, false, 64);
-      else SOLFP4_LANE_LAUNCH(false, false, 64);
+      if (vec && full) e = SOLFP4_LANE_LAUNCH(true, true, 64);
+      else if (full) e = SOLFP4_LANE_LAUNCH(false, true, 64);
+      else if (vec) e = SOLFP4_LANE_LAUNCH(true, false, 64);
+      else e = SOLFP4_LANE_LAUNCH(false, false, 64);
     } else {
-      if (vec && full) SOLFP4_LANE_LAUNCH(true, true, 128);
-      else if (full) SOLFP4_LANE_LAUNCH(false, true, 128);
-      else if (vec) SOLFP4_LANE_LAUNCH(true, false, 128);
-      else SOLFP4_LANE_LAUNCH(false, false, 128);
+      if (vec && full) e = SOLFP4_LANE_LAUNCH(true, true, 128);
+      else if (full) e = SOLFP4_LANE_LAUNCH(false, true, 128);
+      else if (vec) e = SOLFP4_LANE_LAUNCH(true, false, 128);
+      else e = SOLFP4_LANE_LAUNCH(false, false, 128);
     }
 #undef SOLFP4_LANE_LAUNCH
-    return hipGetLastError();
+    return e;
   }
   const dim3 block(kGemmThreads);
   const bool fast = K % kBK == 0;
-  if (fast && vec)
-    hipLaunchKernelGGL((nvfp4_gemm_kernel<true, true>), grid, block, 0, stream, a_codes, a_scales,
-                       a_gs, b_codes, b_scales, b_gs, bias, out, M, N, K);
-  else if (fast)
-    hipLaunchKernelGGL((nvfp4_gemm_kernel<true, false>), grid, block, 0, stream, a_codes, a_scales,
-                       a_gs, b_codes, b_scales, b_gs, bias, out, M, N, K);
-  else if (vec)
-    hipLaunchKernelGGL((nvfp4_gemm_kernel<false, true>), grid, block, 0, stream, a_codes, a_scales,
-                       a_gs, b_codes, b_scales, b_gs, bias, out, M, N, K);
-  else
-    hipLaunchKernelGGL((nvfp4_gemm_kernel<false, false>), grid, block, 0, stream, a_codes, a_scales,
-                       a_gs, b_codes, b_scales, b_gs, bias, out, M, N, K);
-  return hipGetLastError();
+#define SOLFP4_SHARED_LAUNCH(F, V)                                                             \
+  launch_kernel(nvfp4_gemm_kernel<F, V>, grid, block, stream, a_codes, a_scales, a_gs, b_codes, \
+                b_scales, b_gs, bias, out, M, N, K)
+  if (fast && vec) return SOLFP4_SHARED_LAUNCH(true, true);
+  if (fast) return SOLFP4_SHARED_LAUNCH(true, false);
+  if (vec) return SOLFP4_SHARED_LAUNCH(false, true);
+  return SOLFP4_SHARED_LAUNCH(false, false);
+#undef SOLFP4_SHARED_LAUNCH
 }
 
 }  // namespace solfp4

@@ -4,7 +4,29 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <tuple>
+#include <utility>
+
 namespace solfp4 {
+
+// Launch `kernel` and return the status of this launch alone (the runtime's
+// own, not whatever error an earlier, unrelated call may have left for
+// hipGetLastError to report).  Arguments are converted to the kernel's
+// parameter types first.
+template <typename... P, size_t... I>
+hipError_t launch_impl(void (*kernel)(P...), dim3 grid, dim3 block, hipStream_t stream,
+                       std::index_sequence<I...>, std::tuple<P...>& args) {
+  void* argv[] = {static_cast<void*>(&std::get<I>(args))..., nullptr};
+  return hipLaunchKernel(reinterpret_cast<const void*>(kernel), grid, block, argv, 0, stream);
+}
+
+template <typename... P, typename... A>
+hipError_t launch_kernel(void (*kernel)(P...), dim3 grid, dim3 block, hipStream_t stream,
+                         A&&... args) {
+  static_assert(sizeof...(P) == sizeof...(A), "argument count");
+  std::tuple<P...> t(std::forward<A>(args)...);
+  return launch_impl(kernel, grid, block, stream, std::index_sequence_for<P...>{}, t);
+}
 
 // First quantize pass: at most this many partial maxima (workspace words).
 constexpr int kMaxPartials = 1024;
@@ -66,6 +88,14 @@ constexpr uint64_t kSplitToken = 0xC6A4A7935BD1E995ull;
 // Bytes of workspace launch_gemm uses to split this GEMM's last round (0:
 // it runs unsplit).
 size_t gemm_workspace_bytes(int64_t M, int64_t N, int64_t K);
+
+// What launch_gemm runs for this shape (host only): kernel id (the
+// SOLFP4_KERNEL_* values of solfp4.h), output tile edge, workgroups, and K
+// ranges per remainder tile (1: no split).  `with_workspace`: a workspace of
+// at least gemm_workspace_bytes(M, N, K) is passed.
+void describe_gemm(int64_t M, int64_t N, int64_t K, bool with_workspace, int* kernel, int* tile,
+                   int64_t* workgroups, int* splits);
+void describe_mx_gemm(int64_t M, int64_t N, int64_t K, int* kernel, int* tile, int64_t* workgroups);
 
 hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_gs,
                        const uint8_t* b_codes, const uint8_t* b_scales, const float* b_gs,

@@ -42,6 +42,7 @@
 #include <type_traits>
 
 #include "device_common.h"
+#include "solfp4.h"
 #include "kernels.h"
 
 namespace solfp4 {
@@ -431,6 +432,16 @@ __global__ __launch_bounds__(kMxThreads, 1) void mxfp4_gemm_kernel(
   }
 }
 
+void describe_mx_gemm(int64_t M, int64_t N, int64_t K, int* kernel, int* tile, int64_t* workgroups) {
+  const int64_t t256 = ((M + 255) / 256) * ((N + 255) / 256);
+  const int64_t t128 = ((M + 127) / 128) * ((N + 127) / 128);
+  const bool small = small_tiles_pay(t256, t128);
+  (void)K;
+  *kernel = SOLFP4_KERNEL_MXFP4;
+  *tile = small ? 128 : 256;
+  *workgroups = small ? t128 : t256;
+}
+
 hipError_t launch_mx_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const uint8_t* b_codes,
                           const uint8_t* b_scales, const uint16_t* bias, uint16_t* out, int64_t M,
                           int64_t N, int64_t K, hipStream_t stream) {
@@ -442,23 +453,15 @@ hipError_t launch_mx_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const
   const bool fast = K % kMxBK == 0;
   const bool vec = N % 8 == 0;
 #define SOLFP4_MX_LAUNCH(F, V)                                                                 \
-  do {                                                                                         \
-    if (small)                                                                                 \
-      hipLaunchKernelGGL((mxfp4_gemm_kernel<F, V, 64>), grid, block, 0, stream, a_codes,      \
-                         a_scales, b_codes, b_scales, bias, out, M, N, K);                     \
-    else                                                                                       \
-      hipLaunchKernelGGL((mxfp4_gemm_kernel<F, V, 128>), grid, block, 0, stream, a_codes,     \
-                         a_scales, b_codes, b_scales, bias, out, M, N, K);                     \
-  } while (0)
-  if (fast) {
-    if (vec) SOLFP4_MX_LAUNCH(true, true);
-    else SOLFP4_MX_LAUNCH(true, false);
-  } else {
-    if (vec) SOLFP4_MX_LAUNCH(false, true);
-    else SOLFP4_MX_LAUNCH(false, false);
-  }
+  (small ? launch_kernel(mxfp4_gemm_kernel<F, V, 64>, grid, block, stream, a_codes, a_scales,  \
+                         b_codes, b_scales, bias, out, M, N, K)                                \
+         : launch_kernel(mxfp4_gemm_kernel<F, V, 128>, grid, block, stream, a_codes, a_scales, \
+                         b_codes, b_scales, bias, out, M, N, K))
+  hipError_t e;
+  if (fast) e = vec ? SOLFP4_MX_LAUNCH(true, true) : SOLFP4_MX_LAUNCH(true, false);
+  else e = vec ? SOLFP4_MX_LAUNCH(false, true) : SOLFP4_MX_LAUNCH(false, false);
 #undef SOLFP4_MX_LAUNCH
-  return hipGetLastError();
+  return e;
 }
 
 }  // namespace solfp4

@@ -92,10 +92,9 @@ hipError_t launch_mx_quantize(const uint16_t* x, int64_t rows, int64_t K, uint8_
   const int64_t per_wg = (int64_t)kMxQuantThreads * kMxQuantUnroll;
   int64_t grid = (npieces + per_wg - 1) / per_wg;
   if (grid > kMxQuantMaxGrid) grid = kMxQuantMaxGrid;
-  hipLaunchKernelGGL(mxfp4_quantize_kernel, dim3((unsigned)grid), dim3(kMxQuantThreads), 0, stream,
-                     reinterpret_cast<const u32x4_t*>(x), npieces, reinterpret_cast<uint32_t*>(codes),
-                     scales);
-  return hipGetLastError();
+  return launch_kernel(mxfp4_quantize_kernel, dim3((unsigned)grid), dim3(kMxQuantThreads), stream,
+                       reinterpret_cast<const u32x4_t*>(x), npieces,
+                       reinterpret_cast<uint32_t*>(codes), scales);
 }
 
 }  // namespace solfp4

@@ -185,16 +185,16 @@ hipError_t launch_quantize(const uint16_t* x, int64_t rows, int64_t K, uint8_t* 
   const int64_t n = rows * K;
   const int64_t npieces = n / 8;           // 8 elements per lane, 2 lanes per block
   const int npartial = amax_partial_count(n);
-  hipLaunchKernelGGL(amax_partial_kernel, dim3(npartial), dim3(kQuantThreads), 0, stream,
-                     reinterpret_cast<const uint4*>(x), n / 8, partial);
+  hipError_t e = launch_kernel(amax_partial_kernel, dim3(npartial), dim3(kQuantThreads), stream,
+                               reinterpret_cast<const uint4*>(x), n / 8, partial);
+  if (e != hipSuccess) return e;
   const int64_t per_wg = (int64_t)kQuantThreads * kEncodeUnroll;
   int64_t grid = (npieces + per_wg - 1) / per_wg;
   if (grid > kEncodeMaxGrid) grid = kEncodeMaxGrid;
   if (grid < 1) grid = 1;
-  hipLaunchKernelGGL(nvfp4_encode_kernel, dim3((unsigned)grid), dim3(kQuantThreads), 0, stream,
-                     reinterpret_cast<const u32x4_t*>(x), npieces, partial, npartial,
-                     reinterpret_cast<uint32_t*>(codes), scales, global_scale);
-  return hipGetLastError();
+  return launch_kernel(nvfp4_encode_kernel, dim3((unsigned)grid), dim3(kQuantThreads), stream,
+                       reinterpret_cast<const u32x4_t*>(x), npieces, partial, npartial,
+                       reinterpret_cast<uint32_t*>(codes), scales, global_scale);
 }
 
 }  // namespace solfp4

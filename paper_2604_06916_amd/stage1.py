@@ -46,7 +46,7 @@ class Stage1Config:
     mlp: int = 12288
     rollouts: int = 8
     tokens: int = 4608
-    steps: int = 6
+    steps: int = 4
     keep: int = 4            # K: K/2 highest- and K/2 lowest-rewarded rollouts
     w_sigma: float = 0.015
     seed: int = 5000
@@ -60,6 +60,19 @@ def layer_shapes(cfg):
     """(name, N, K) of one block's linears."""
     return [("qkv", 3 * cfg.hidden, cfg.hidden), ("out", cfg.hidden, cfg.hidden),
             ("up", cfg.mlp, cfg.hidden), ("down", cfg.hidden, cfg.mlp)]
+
+
+def linear_flops(cfg):
+    """FLOPs of every linear of one rollout (2 M N K per linear, M = all
+    rollouts' tokens, four linears per block, every block, every step)."""
+    M = cfg.rollouts * cfg.tokens
+    return cfg.steps * cfg.blocks * sum(2.0 * M * N * K for _, N, K in layer_shapes(cfg))
+
+
+def attention_flops(cfg):
+    """FLOPs of the attention products of one rollout (Q K^T and P V, each
+    2 T^2 d per head and rollout)."""
+    return cfg.steps * cfg.blocks * cfg.rollouts * cfg.heads * 4.0 * cfg.tokens ** 2 * cfg.head_dim
 
 
 def select_rollouts(rewards, keep):
@@ -128,7 +141,18 @@ class Runner:
         self.buf = {n: torch.empty((M, c), dtype=torch.bfloat16, device=device)
                     for n, c in [("h", H), ("qkv", 3 * H), ("a", H), ("o", H), ("u", D), ("d", H)]}
         self.linear_events = None
+        self.op_events = None    # dict: op kind -> [(start, end)] of HIP events, when timing
         self.trace = None        # list: (stage name, tensor copy) of every block stage
+        self.step_trace = None   # list: latents after each Euler step (copies)
+
+    def _op(self, kind):
+        """A (start, end) event pair for one op of this kind, or None."""
+        if self.op_events is None:
+            return None
+        ev = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+        ev[0].record()
+        self.op_events.setdefault(kind, []).append(ev)
+        return ev
 
     def _t(self, name, t):
         if self.trace is not None:
@@ -155,21 +179,41 @@ class Runner:
     def blocks(self, x):
         cfg, B = self.cfg, self.buf
         R, T, Hh, hd = cfg.rollouts, cfg.tokens, cfg.heads, cfg.head_dim
+        def end(ev):
+            if ev is not None:
+                ev[1].record()
+
         for L in self.layers:
             self._t("x", x)
+            ev = self._op("norm")
             h = self._t("h1", _rmsnorm(x, B["h"]))
+            end(ev)
             qkv = self._t("qkv", self.linear(h, L["qkv"], B["qkv"])).view(R, T, 3, Hh, hd)
             q, k, v = (qkv[:, :, i].transpose(1, 2) for i in range(3))   # [R, heads, T, hd] views
+            ev = self._op("attention")
             with sdpa_kernel([SDPBackend.FLASH_ATTENTION, SDPBackend.EFFICIENT_ATTENTION]):
                 a = F.scaled_dot_product_attention(q, k, v)
+            end(ev)
+            ev = self._op("copy")
             B["a"].copy_(a.transpose(1, 2).reshape(R * T, cfg.hidden))
+            end(ev)
             self._t("a", B["a"])
-            x = self._t("x2", x + self._t("o", self.linear(B["a"], L["out"], B["o"])))
+            o = self._t("o", self.linear(B["a"], L["out"], B["o"]))
+            ev = self._op("residual")
+            x = self._t("x2", x + o)
+            end(ev)
+            ev = self._op("norm")
             h = self._t("h2", _rmsnorm(x, B["h"]))
+            end(ev)
             u = self._t("up", self.linear(h, L["up"], B["u"]))
+            ev = self._op("gelu")
             B["u"].copy_(F.gelu(u, approximate="tanh"))
+            end(ev)
             self._t("g", B["u"])
-            x = self._t("x3", x + self._t("d", self.linear(B["u"], L["down"], B["d"])))
+            d = self._t("d", self.linear(B["u"], L["down"], B["d"]))
+            ev = self._op("residual")
+            x = self._t("x3", x + d)
+            end(ev)
         return x
 
     def rollout(self, x0):
@@ -178,7 +222,12 @@ class Runner:
         dt = 1.0 / self.cfg.steps
         for _ in range(self.cfg.steps):
             y = self.blocks(x)
+            ev = self._op("euler")
             x = (x.float() + dt * (y.float() - x.float())).to(torch.bfloat16)
+            if ev is not None:
+                ev[1].record()
+            if self.step_trace is not None:
+                self.step_trace.append(x.clone())
         return x
 
 

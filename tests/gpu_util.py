@@ -63,3 +63,38 @@ def poison_u8(shape, value=0xAB):
 def poison_bf16(shape):
     # a NaN pattern: any element the kernel fails to write stays NaN
     return torch.full(shape, 0x7FC1, dtype=torch.int16, device=device()).view(torch.bfloat16)
+
+
+def abs_products(a_deq: np.ndarray, b_deq: np.ndarray) -> np.ndarray:
+    """sum_k |a[m, k]| |b[n, k]| in float64, from the oracle's dequantized
+    operands (block scale times element value, per-tensor scale excluded)."""
+    return np.abs(a_deq) @ np.abs(b_deq).T
+
+
+def assert_per_element(got_bits: np.ndarray, ref: np.ndarray, sabs: np.ndarray, alpha, K: int,
+                       bias_bits=None, label=""):
+    """Every output within a bound that any FP32 summation order meets:
+
+        |got - ref| <= ulp_bf16(max(|got|, |ref|))
+                       + (K + 4) 2^-24 (|alpha| sum_k |a_k b_k| + |bias|)
+
+    The first term covers the final rounding to BF16 (half an ulp, doubled so
+    that a result rounded into the next binade still passes).  The second
+    covers the FP32 arithmetic: the products are exact, a sum of K of them
+    in any order rounds at most K - 1 times, each time by at most 2^-24 of a
+    partial sum no larger than sum |a b|; then the product of the two tensor
+    scales and the epilogue's fused multiply-add round once each.  (The
+    matrix instructions add 16 or 64 products per rounding of the
+    accumulator, so the count is generous.)  A wrong block scale or a
+    misplaced 16-element block moves an output by far more."""
+    g = O.bf16_bits_to_f32(got_bits).astype(np.float64)
+    b = 0.0 if bias_bits is None else np.abs(O.bf16_bits_to_f32(bias_bits).astype(np.float64))[None, :]
+    mag = np.maximum(np.abs(g), np.abs(ref))
+    _, e = np.frexp(np.where(mag > 0, mag, 1.0))
+    ulp = np.where(mag > 0, np.exp2(np.maximum(e - 8, -133)), 2.0 ** -133)
+    bound = ulp + (K + 4) * 2.0 ** -24 * (abs(float(alpha)) * sabs + b)
+    excess = np.abs(g - ref) / bound
+    worst = float(excess.max()) if excess.size else 0.0
+    say(f"  {label}per-element: worst |err| / bound = {worst:.3f}")
+    assert np.all(np.isfinite(g))
+    assert worst <= 1.0, (label, np.unravel_index(int(np.argmax(excess)), excess.shape))

@@ -10,8 +10,8 @@ import torch
 
 import oracle.nvfp4 as O
 import paper_2604_06916_amd as sol
-from gpu_util import bf16_from_dev, bf16_mismatch_fraction, bf16_to_dev, f32_bits, poison_bf16, \
-    rel_fro, say, u8_from_dev
+from gpu_util import abs_products, assert_per_element, bf16_from_dev, bf16_mismatch_fraction, \
+    bf16_to_dev, f32_bits, poison_bf16, rel_fro, say, u8_from_dev
 from workloads import (ROLE_BIAS, ROLE_W, ROLE_X, WORKLOADS, draw_activations, draw_bias,
                        draw_weights, seed_for)
 
@@ -68,6 +68,8 @@ def test_layer(wname, lname):
     say(f"  rel_fro={err:.3e} mismatch={mism:.2e} on {len(rm)}x{len(rn)} sampled outputs")
     assert err <= 2e-3
     assert mism <= 0.01
+    sabs = abs_products(O.nvfp4_unscaled_ref(rxc, rxs), O.nvfp4_unscaled_ref(rwc, rws))
+    assert_per_element(got, ref, sabs, np.float32(rxa) * np.float32(rwa), K, bias[rn])
     del x, w, b, out, out2, xc, xs, xa, wc, ws, wa
     torch.cuda.empty_cache()
 
@@ -114,5 +116,7 @@ def test_layer_mxfp4(wname, lname):
     say(f"  rel_fro={err:.3e} mismatch={mism:.2e} on {len(rm)}x{len(rn)} sampled outputs")
     assert err <= 2e-3
     assert mism <= 0.01
+    sabs = abs_products(O.mxfp4_unscaled_ref(rxc, rxs), O.mxfp4_unscaled_ref(rwc, rws))
+    assert_per_element(got, ref, sabs, 1.0, K, bias[rn])
     del x, w, b, out, out2, xc, xs, wc, ws
     torch.cuda.empty_cache()

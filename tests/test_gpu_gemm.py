@@ -2,16 +2,17 @@
 
 Operands are quantized by the oracle on the CPU and uploaded, so the GEMM is
 tested on exactly the oracle's inputs.  Bar: relative Frobenius error
-<= 2e-3 against the float64 oracle; cases whose FP32 sums are exact must be
-bit-identical to the oracle's BF16 rounding."""
+<= 2e-3 against the float64 oracle and every element within the FP32
+summation bound of gpu_util.assert_per_element; cases whose FP32 sums are
+exact must be bit-identical to the oracle's BF16 rounding."""
 import numpy as np
 import pytest
 import torch
 
 import oracle.nvfp4 as O
 import paper_2604_06916_amd as sol
-from gpu_util import (bf16_from_dev, bf16_mismatch_fraction, bf16_to_dev, device, f32_to_dev,
-                      poison_bf16, rel_fro, say, u8_to_dev)
+from gpu_util import (abs_products, assert_per_element, bf16_from_dev, bf16_mismatch_fraction,
+                      bf16_to_dev, device, f32_to_dev, poison_bf16, rel_fro, say, u8_to_dev)
 from workloads import draw_activations, draw_bias, draw_weights
 
 pytestmark = pytest.mark.gpu
@@ -26,6 +27,14 @@ def gpu_gemm(ac, as_, aa, bc, bs, ba, bias=None, split=True):
                    f32_to_dev(ba), None if bias is None else bf16_to_dev(bias), out, split=split)
     torch.cuda.synchronize()
     return bf16_from_dev(out)
+
+
+def check_elements(got, a, b, ref, bias=None, label=""):
+    """Per-element bound for a GEMM of quantized operands a, b = (codes,
+    scales, alpha)."""
+    sabs = abs_products(O.nvfp4_unscaled_ref(a[0], a[1]), O.nvfp4_unscaled_ref(b[0], b[1]))
+    alpha = np.float32(np.float32(a[2]) * np.float32(b[2]))
+    assert_per_element(got, ref, sabs, alpha, a[0].shape[1] * 2, bias, label)
 
 
 def quantized(kind, rows, K, seed, sigma=None):
@@ -154,6 +163,7 @@ def test_wide_dynamic_range_vs_oracle(kind):
     err = rel_fro(got, ref)
     say(f"{kind}: rel_fro={err:.3e}")
     assert err <= TOL
+    check_elements(got, a, b, ref)
 
 
 SHAPES = [(1, 1, 16), (5, 7, 32), (64, 64, 128), (255, 257, 48), (300, 520, 272),
@@ -178,6 +188,7 @@ def test_random_vs_oracle(M, N, K, with_bias):
     assert np.isfinite(O.bf16_bits_to_f32(got)).all()
     assert err <= TOL
     assert mism <= 0.01
+    check_elements(got, (ac, as_, aa), (bc, bs, ba), ref, bias)
 
 
 def test_zero_k_writes_bias():
@@ -220,6 +231,8 @@ def test_split_last_round_vs_oracle(M, N, K):
     assert np.array_equal(outs[0], outs[1])
     assert err <= TOL and err_whole <= TOL
     assert bf16_mismatch_fraction(outs[0], ref) <= 0.01
+    check_elements(outs[0], (ac, as_, aa), (bc, bs, ba), ref, bias, "split ")
+    check_elements(whole, (ac, as_, aa), (bc, bs, ba), ref, bias, "unsplit ")
 
 
 @pytest.mark.parametrize("M,N,K", [SPLIT_SHAPES[0], SMALL_SPLIT_SHAPES[0]])

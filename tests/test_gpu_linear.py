@@ -6,7 +6,8 @@ import torch
 
 import oracle.nvfp4 as O
 import paper_2604_06916_amd as sol
-from gpu_util import bf16_from_dev, bf16_mismatch_fraction, bf16_to_dev, poison_bf16, rel_fro, say
+from gpu_util import (abs_products, assert_per_element, bf16_from_dev, bf16_mismatch_fraction,
+                      bf16_to_dev, poison_bf16, rel_fro, say)
 from workloads import draw_activations, draw_bias, draw_weights
 
 pytestmark = pytest.mark.gpu
@@ -34,12 +35,15 @@ def test_linear_matches_quantize_then_gemm_and_oracle(M, N, K, with_bias):
     got = bf16_from_dev(out)
     assert np.array_equal(got, bf16_from_dev(out2))
 
-    ref, _ = O.nvfp4_linear_ref(xb, *O.nvfp4_quantize_ref(wb), bias)
+    rw = O.nvfp4_quantize_ref(wb)
+    ref, rx = O.nvfp4_linear_ref(xb, *rw, bias)
     err = rel_fro(got, ref)
     mism = bf16_mismatch_fraction(got, ref)
     say(f"linear M={M} N={N} K={K} bias={with_bias}: rel_fro={err:.3e} mismatch={mism:.2e}")
     assert err <= 2e-3
     assert mism <= 0.01
+    sabs = abs_products(O.nvfp4_unscaled_ref(rx[0], rx[1]), O.nvfp4_unscaled_ref(rw[0], rw[1]))
+    assert_per_element(got, ref, sabs, np.float32(rx[2]) * np.float32(rw[2]), K, bias)
 
 
 def test_linear_workspace_holds_the_activation_codes():

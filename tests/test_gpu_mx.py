@@ -12,7 +12,8 @@ import torch
 
 import oracle.nvfp4 as O
 import paper_2604_06916_amd as sol
-from gpu_util import (bf16_from_dev, bf16_mismatch_fraction, bf16_to_dev, device, poison_bf16,
+from gpu_util import (abs_products, assert_per_element, bf16_from_dev, bf16_mismatch_fraction,
+                      bf16_to_dev, device, poison_bf16,
                       poison_u8, rel_fro, say, u8_from_dev, u8_to_dev)
 from workloads import draw_activations, draw_bias, draw_weights, f32_to_bf16_bits
 
@@ -226,6 +227,8 @@ def test_random_vs_oracle(M, N, K, with_bias):
     assert np.isfinite(O.bf16_bits_to_f32(got)).all()
     assert err <= TOL
     assert mism <= 0.01
+    sabs = abs_products(O.mxfp4_unscaled_ref(ac, as_), O.mxfp4_unscaled_ref(bc, bs))
+    assert_per_element(got, ref, sabs, 1.0, K, bias)
 
 
 def test_wide_dynamic_range_vs_oracle():
@@ -242,6 +245,8 @@ def test_wide_dynamic_range_vs_oracle():
     err = rel_fro(got, ref)
     say(f"wide: rel_fro={err:.3e}")
     assert err <= TOL
+    sabs = abs_products(O.mxfp4_unscaled_ref(*a), O.mxfp4_unscaled_ref(*b))
+    assert_per_element(got, ref, sabs, 1.0, K)
 
 
 def test_zero_k_writes_bias():
@@ -286,3 +291,5 @@ def test_linear_equals_quantize_then_gemm(M, N, K):
     err = rel_fro(got, ref)
     say(f"linear M={M} N={N} K={K}: rel_fro={err:.3e}")
     assert err <= TOL
+    sabs = abs_products(O.mxfp4_unscaled_ref(rc, rs), O.mxfp4_unscaled_ref(wc, ws))
+    assert_per_element(got, ref, sabs, 1.0, K, bias)

@@ -89,3 +89,31 @@ def test_rollout_vs_oracle(backend):
     assert err <= (1e-2 if backend == "bf16" else 0.15)
     top, bottom = G.select_rollouts(r_gpu, cfg.keep)
     assert r_gpu[top].min() >= r_gpu[bottom].max()
+
+
+@pytest.mark.parametrize("backend", ["bf16", "nvfp4", "mxfp4"])
+def test_each_euler_step_vs_oracle(backend):
+    """Teacher-forced: every Euler step of the GPU rollout recomputed by the
+    oracle from the GPU's latents before that step, so a difference cannot
+    compound across steps.  One step is two blocks (eight linears) plus the
+    update x + (1/T)(blocks(x) - x); bar 2e-2 relative for the FP4 formats
+    (code flips inside one step only), 1e-2 for BF16."""
+    from paper_2604_06916_amd import stage1 as G
+    cfg = tiny()
+    dev = device()
+    model = G.make_weights(cfg, dev)
+    runner = G.Runner(cfg, model, backend, dev)
+    runner.step_trace = []
+    x0 = G.initial_latents(cfg, dev)
+    runner.rollout(x0)
+    torch.cuda.synchronize()
+    xs = [f64(x0)] + [f64(x) for x in runner.step_trace]
+    weights = [{n: (bf16_from_dev(w), bf16_from_dev(b)) for n, (w, b) in blk.items()} for blk in model]
+    layers = [{n: (S.prepare(backend, w), b) for n, (w, b) in blk.items()} for blk in weights]
+    dt = 1.0 / cfg.steps
+    for t in range(cfg.steps):
+        y = S.blocks(backend, xs[t], layers, cfg)
+        want = S.bf16_round(xs[t] + dt * (y - xs[t]))
+        err = rel(xs[t + 1], want)
+        say(f"{backend} step {t}: rel {err:.3e}")
+        assert err <= (1e-2 if backend == "bf16" else 2e-2)
