@@ -143,7 +143,7 @@ class Runner:
         self.linear_events = None
         self.op_events = None    # dict: op kind -> [(start, end)] of HIP events, when timing
         self.trace = None        # list: (stage name, tensor copy) of every block stage
-        self.step_trace = None   # list: latents after each Euler step (copies)
+        self.step_trace = None   # list: {"y": blocks output, "x": latents after} per Euler step
 
     def _op(self, kind):
         """A (start, end) event pair for one op of this kind, or None."""
@@ -227,7 +227,7 @@ class Runner:
             if ev is not None:
                 ev[1].record()
             if self.step_trace is not None:
-                self.step_trace.append(x.clone())
+                self.step_trace.append({"y": y.clone(), "x": x.clone()})
         return x
 
 
