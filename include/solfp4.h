@@ -98,6 +98,27 @@ SOLFP4_API int nvfp4_quantize(const uint16_t* x, int64_t rows, int64_t K,
                    void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * nvfp4_quantize without a workspace, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  Same arguments, kernels and results
+ * as nvfp4_quantize (bit-identical codes, scales and alpha); the amax
+ * pass's partial maxima go to a fixed 4 KiB device array of the library
+ * instead (one per device, held until the process ends; looked up on the
+ * first call on each device).  Allocates nothing, for any size: the amax
+ * pass never runs more workgroups than the array has words, and a size
+ * that needed more would be refused with SOLFP4_EWORKSPACE.
+ *
+ * Every call on one device shares that device's array: two calls that may
+ * run at the same time on one device (on different streams, or from
+ * different threads without ordering) race on it and may write a wrong
+ * alpha.  Calls ordered on one stream, or separated by synchronisation, are
+ * safe; the array's contents are rewritten by every call before they are
+ * read, so nothing needs clearing.
+ */
+SOLFP4_API int nvfp4_quantize_noalloc(const uint16_t* x, int64_t rows, int64_t K,
+                   uint8_t* codes, uint8_t* scales, float* global_scale, void* stream);
+
+/*
  * Block-scaled NVFP4 GEMM with BF16 output (the "NVFP4 dense operations" of
  * Sec. 3.4, Stage 1):
  *

@@ -180,6 +180,26 @@ int nvfp4_quantize(const uint16_t* x, int64_t rows, int64_t K, uint8_t* codes, u
   return e == hipSuccess ? SOLFP4_OK : SOLFP4_EHIP;
 }
 
+int nvfp4_quantize_noalloc(const uint16_t* x, int64_t rows, int64_t K, uint8_t* codes,
+                           uint8_t* scales, float* global_scale, void* stream) {
+  int rc = check_dims(rows, K);
+  if (rc) return rc;
+  if (K % 16) return SOLFP4_ESHAPE;
+  const bool data = rows > 0 && K > 0;
+  if (!global_scale || (data && (!x || !codes || !scales))) return SOLFP4_EINVAL;
+  if (!aligned16(global_scale) ||
+      (data && (!aligned16(x) || !aligned16(codes) || !aligned16(scales))))
+    return SOLFP4_EALIGN;
+  // the partial maxima must fit the fixed scratch (they always do: the amax
+  // pass never runs more than kMaxPartials workgroups)
+  if (solfp4::amax_partial_count(rows * K) > solfp4::kScratchWords) return SOLFP4_EWORKSPACE;
+  uint32_t* partial = nullptr;
+  if (solfp4::scratch_address(&partial) != hipSuccess) return SOLFP4_EHIP;
+  const hipError_t e = solfp4::launch_quantize(x, rows, K, codes, scales, global_scale, partial,
+                                               static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? SOLFP4_OK : SOLFP4_EHIP;
+}
+
 int nvfp4_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_global_scale,
                const uint8_t* b_codes, const uint8_t* b_scales, const float* b_global_scale,
                const uint16_t* bias, uint16_t* out, void* workspace, size_t workspace_bytes,

@@ -38,6 +38,13 @@ constexpr int64_t kMxQuantMaxGrid = 8192;
 
 int amax_partial_count(int64_t n_elems);
 
+// The allocation-free quantize's scratch: a file-scope device array of
+// kScratchWords words (the amax pass's partial maxima), one per device.
+constexpr int kScratchWords = kMaxPartials;
+static_assert(kScratchWords * 4 <= 4096, "scratch stays at 4 KiB");
+// Device address of this device's scratch (looked up once per device).
+hipError_t scratch_address(uint32_t** out);
+
 hipError_t launch_quantize(const uint16_t* x, int64_t rows, int64_t K, uint8_t* codes,
                            uint8_t* scales, float* global_scale, uint32_t* partial,
                            hipStream_t stream);

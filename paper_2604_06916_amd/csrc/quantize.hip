@@ -20,6 +20,8 @@
 //   alpha = amax_g / 2688; t = alpha * 6; s_f = amax_b / t; s = E4M3(s_f);
 //   d = s * alpha; r = 1 / d; y = x * r; q = E2M1(y)
 // with correctly rounded division (hipcc's default) and no contraction.
+#include <mutex>
+
 #include "device_common.h"
 #include "kernels.h"
 
@@ -165,6 +167,34 @@ __global__ __launch_bounds__(kQuantThreads) void nvfp4_encode_kernel(
     else
       encode_iter<true>(x, npieces, base, t, zero_tensor, rtab, codes, scales);
   }
+}
+
+// Scratch of the allocation-free quantize: the amax pass's partial maxima,
+// one word per workgroup of that pass, at most kMaxPartials (4 KiB).  Each
+// device the library runs on holds its own copy until the process ends.
+// Host code never passes `scratch` itself to a kernel (on the host the name
+// stands for a host-side shadow, not a device address): the address comes
+// from hipGetSymbolAddress, once per device.
+static __device__ __align__(256) uint32_t scratch[kScratchWords];
+
+hipError_t scratch_address(uint32_t** out) {
+  constexpr int kMaxDevices = 64;
+  static uint32_t* cached[kMaxDevices];
+  static std::mutex mu;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!cached[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    cached[dev] = static_cast<uint32_t*>(p);
+  }
+  *out = cached[dev];
+  return hipSuccess;
 }
 
 int amax_partial_count(int64_t n_elems) {
