@@ -191,11 +191,15 @@ SOLFP4_API size_t nvfp4_linear_workspace_bytes(int64_t M, int64_t N, int64_t K);
  *            holds the activation codes at offset 0, then their scales and
  *            alpha (offsets are an implementation detail).
  *
- * The result is bit-identical to nvfp4_quantize followed by nvfp4_gemm
- * with a workspace of at least nvfp4_gemm_workspace_bytes(M, N, K) (the
- * linear always splits the last round where the GEMM would; nvfp4_gemm
- * without a workspace runs every tile whole, which may change the last bits
- * of the affected outputs).
+ * Launches: the amax pass, the encode pass and the GEMM; or, for few
+ * tokens (the 64 x 64-tile GEMM) with K <= 512, the amax pass and one GEMM
+ * kernel that quantizes the activations itself.  Either way the workspace
+ * ends up holding the same codes, scales and alpha, and the result is
+ * bit-identical to nvfp4_quantize followed by nvfp4_gemm with a workspace of
+ * at least nvfp4_gemm_workspace_bytes(M, N, K) (the linear always splits
+ * the last round where the GEMM would; nvfp4_gemm without a workspace runs
+ * every tile whole, which may change the last bits of the affected
+ * outputs).
  */
 SOLFP4_API int nvfp4_linear(const uint16_t* x, const uint8_t* w_codes, const uint8_t* w_scales,
                  const float* w_global_scale, const uint16_t* bias, uint16_t* out,
@@ -214,7 +218,7 @@ SOLFP4_API int nvfp4_linear(const uint16_t* x, const uint8_t* w_codes, const uin
  *   with_workspace  nonzero: nvfp4_gemm gets a workspace of at least
  *                   nvfp4_gemm_workspace_bytes(M, N, K) (ignored for MXFP4)
  *   kernel          written: one of the SOLFP4_KERNEL_* ids below
- *   tile            written: output tile edge, 256 or 128
+ *   tile            written: output tile edge, 256, 128 or 64
  *   workgroups      written: workgroups of the launch
  *   splits          written: K ranges per tile of the last round (1: none)
  *
@@ -227,6 +231,9 @@ SOLFP4_API int nvfp4_linear(const uint16_t* x, const uint8_t* w_codes, const uin
 #define SOLFP4_KERNEL_NVFP4_LANE 1     /* codes to LDS by DMA, per-wave dequantization */
 #define SOLFP4_KERNEL_NVFP4_SHARED 2   /* workgroup-shared dequantization into LDS */
 #define SOLFP4_KERNEL_MXFP4 3          /* scaled FP4 matrix instructions */
+#define SOLFP4_KERNEL_NVFP4_SMALL 4    /* 64 x 64 tiles for few tokens (K % 128 == 0); in
+                                          nvfp4_linear with K <= 512 it also quantizes the
+                                          activations itself */
 SOLFP4_API int solfp4_gemm_plan(int format, int64_t M, int64_t N, int64_t K, int with_workspace,
                      int* kernel, int* tile, int64_t* workgroups, int* splits);
 

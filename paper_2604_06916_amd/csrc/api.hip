@@ -251,6 +251,23 @@ int nvfp4_linear(const uint16_t* x, const uint8_t* w_codes, const uint8_t* w_sca
                    N, K);
   if (rc) return rc;
   const hipStream_t s = static_cast<hipStream_t>(stream);
+  if (K <= solfp4::kFusedMaxK && solfp4::use_small_gemm(M, N, K)) {
+    // few tokens and a short K: the amax pass, then the small-tile GEMM
+    // quantizing the activations itself (leaving codes, scales and alpha in
+    // the workspace)
+    solfp4::SmallFuse fuse;
+    fuse.x = x;
+    fuse.partial = partial;
+    fuse.npartial = solfp4::amax_partial_count(M * K);
+    fuse.codes_out = xc;
+    fuse.scales_out = xs;
+    fuse.alpha_out = xa;
+    hipError_t e = solfp4::launch_amax(x, M * K, partial, s);
+    if (e != hipSuccess) return SOLFP4_EHIP;
+    e = solfp4::launch_gemm_small(nullptr, nullptr, nullptr, w_codes, w_scales, w_global_scale, bias,
+                                  out, M, N, K, &fuse, s);
+    return e == hipSuccess ? SOLFP4_OK : SOLFP4_EHIP;
+  }
   hipError_t e = solfp4::launch_quantize(x, M, K, xc, xs, xa, partial, s);
   if (e != hipSuccess) return SOLFP4_EHIP;
   if (M == 0 || N == 0) return SOLFP4_OK;

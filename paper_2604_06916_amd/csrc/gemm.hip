@@ -34,18 +34,11 @@
 #include <type_traits>
 
 #include "device_common.h"
+#include "nvfp4_gemm_common.h"
 #include "solfp4.h"
 #include "kernels.h"
 
 namespace solfp4 {
-
-typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
-typedef float floatx2_t __attribute__((ext_vector_type(2)));
-
-// Two FP32 values to a BF16 pair (round to nearest even), first in the low half.
-__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
-  return __builtin_bit_cast(uint32_t, __builtin_convertvector((floatx2_t{lo, hi}), bf16x2_t));
-}
 
 // ---------------------------------------------------------------------------
 // nvfp4_gemm_kernel: workgroup-shared dequantization, any K % 16 == 0.
@@ -433,32 +426,6 @@ __global__ __launch_bounds__(kGemmThreads, 1) void nvfp4_gemm_kernel(
 // the word of its row and piece and a packed multiply with the half selected
 // by op_sel applies the block scale.  Per K-step a kWT = 128 wave converts 8
 // fragments (64 VALU instructions) under 16 MFMAs.
-
-constexpr int kLBK = 128;                       // K elements per stage
-constexpr int kLRowBytes = kLBK / 2;            // code bytes per row per stage
-constexpr int kLThreads = 256;
-constexpr int kLBufs = 4;                       // LDS stage buffers (loads run 3 stages ahead)
-constexpr int kLScaleStride = 5;                // words per row in LDS (4 + 1 pad)
-
-// The 8 elements of one K-step (codes of word w, element j in nibble j)
-// times the scale pattern s (s * 2^-8 in both halves): 256 q from the
-// converter, then one exact packed multiply per pair.
-__device__ __forceinline__ half8_t dequant_step(uint32_t w, half2_t s) {
-  const half2_t d0 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 256.0f, 0) * s;
-  const half2_t d1 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 256.0f, 1) * s;
-  const half2_t d2 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 256.0f, 2) * s;
-  const half2_t d3 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, 256.0f, 3) * s;
-  typedef _Float16 half4_t __attribute__((ext_vector_type(4)));
-  const half4_t lo = __builtin_shufflevector(d0, d1, 0, 1, 2, 3);
-  const half4_t hi = __builtin_shufflevector(d2, d3, 0, 1, 2, 3);
-  return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-}
-
-// Scale bytes b0 (low) and b1 of a word's byte pair, as the FP16 patterns
-// b << 7 (s * 2^-8) in the low and high half.
-__device__ __forceinline__ uint32_t scale_patterns(uint32_t w, bool high_pair) {
-  return __builtin_amdgcn_perm(0u, w, high_pair ? 0x0C030C02u : 0x0C010C00u) << 7;
-}
 
 // kFull: K % 128 == 0, every stage lies inside the rows and a stage's 8
 // scale bytes per row are one aligned 8-byte load.  Otherwise (K % 32 == 0)
@@ -1065,12 +1032,19 @@ static SplitPlan gemm_plan(int64_t M, int64_t N, int64_t K, bool* small_out) {
 }
 
 size_t gemm_workspace_bytes(int64_t M, int64_t N, int64_t K) {
-  if (M <= 0 || N <= 0 || K <= 0) return 0;
+  if (M <= 0 || N <= 0 || K <= 0 || use_small_gemm(M, N, K)) return 0;
   return gemm_plan(M, N, K, nullptr).bytes;
 }
 
 void describe_gemm(int64_t M, int64_t N, int64_t K, bool with_workspace, int* kernel, int* tile,
                    int64_t* workgroups, int* splits) {
+  if (use_small_gemm(M, N, K)) {
+    *kernel = SOLFP4_KERNEL_NVFP4_SMALL;
+    *tile = 64;
+    *splits = 1;
+    *workgroups = ((M + 63) / 64) * ((N + 63) / 64);
+    return;
+  }
   bool small = false;
   SplitPlan plan = gemm_plan(M, N, K, &small);
   const bool split = plan.active() && with_workspace;
@@ -1083,10 +1057,34 @@ void describe_gemm(int64_t M, int64_t N, int64_t K, bool with_workspace, int* ke
   *workgroups = split ? plan.dp_tiles + plan.rem_tiles * plan.splits : tiles;
 }
 
+// The small-tile kernel takes the shapes whose 64 x 64 tiles fit in one
+// round (one workgroup per CU).  Measured against the 128 x 128 / 256 x 256
+// kernels, graph-replayed: 128 x 1152 x 1152 6.96 vs 11.46 us, 128 x 3072 x
+// 3072 13.3 vs 17.8, 768 x 1152 x 1152 7.4 vs 11.6; past one round it loses
+// (384 x 3072 x 3072 0.96x, 1024 x 3072 x 3072 0.85x, 128 x 9216 x 3072
+// 0.95x) or gains little (1024 x 1152 x 1152 1.16x at 288 tiles).
+bool use_small_gemm(int64_t M, int64_t N, int64_t K) {
+  if (K % kLBK != 0 || M <= 0 || N <= 0 || K <= 0) return false;
+  const int64_t t64 = ((M + 63) / 64) * ((N + 63) / 64);
+  return t64 <= device_cus();
+}
+
 hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_gs,
                        const uint8_t* b_codes, const uint8_t* b_scales, const float* b_gs,
                        const uint16_t* bias, uint16_t* out, int64_t M, int64_t N, int64_t K,
                        void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (M == 0 || N == 0) return hipSuccess;
+  if (use_small_gemm(M, N, K))
+    return launch_gemm_small(a_codes, a_scales, a_gs, b_codes, b_scales, b_gs, bias, out, M, N, K,
+                             nullptr, stream);
+  return launch_gemm_regular(a_codes, a_scales, a_gs, b_codes, b_scales, b_gs, bias, out, M, N, K,
+                             workspace, workspace_bytes, stream);
+}
+
+hipError_t launch_gemm_regular(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_gs,
+                               const uint8_t* b_codes, const uint8_t* b_scales, const float* b_gs,
+                               const uint16_t* bias, uint16_t* out, int64_t M, int64_t N, int64_t K,
+                               void* workspace, size_t workspace_bytes, hipStream_t stream) {
   if (M == 0 || N == 0) return hipSuccess;
   const int64_t tiles = ((M + kBM - 1) / kBM) * ((N + kBN - 1) / kBN);
   const dim3 grid((unsigned)tiles);

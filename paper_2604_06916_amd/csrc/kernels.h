@@ -104,6 +104,40 @@ void describe_gemm(int64_t M, int64_t N, int64_t K, bool with_workspace, int* ke
                    int64_t* workgroups, int* splits);
 void describe_mx_gemm(int64_t M, int64_t N, int64_t K, int* kernel, int* tile, int64_t* workgroups);
 
+// The small-tile GEMM (64 x 64 output tiles, K % 128 == 0) and its fused
+// variant, whose activations arrive as BF16 and are quantized in the kernel
+// (bit-identical to nvfp4_quantize) after the amax pass has written its
+// partial maxima.
+struct SmallFuse {
+  const uint16_t* x = nullptr;          // [M][K] BF16 activations
+  const uint32_t* partial = nullptr;    // the amax pass's partial maxima
+  int npartial = 0;
+  uint8_t* codes_out = nullptr;         // [M][K/2], the activations' codes
+  uint8_t* scales_out = nullptr;        // [M][K/16], their E4M3 scales
+  float* alpha_out = nullptr;           // their alpha
+};
+// Whether a GEMM of this shape runs on the small-tile kernel (host only):
+// K % 128 == 0 and its 64 x 64 tiles fit in one round on the device.
+bool use_small_gemm(int64_t M, int64_t N, int64_t K);
+// nvfp4_linear quantizes the activations inside the small-tile kernel up to
+// this K; beyond it the amax and encode passes followed by the small-tile
+// GEMM are faster (the in-kernel quantization costs as much VALU time as the
+// encode pass, and saves only its launch).
+constexpr int64_t kFusedMaxK = 512;
+hipError_t launch_gemm_small(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_gs,
+                             const uint8_t* b_codes, const uint8_t* b_scales, const float* b_gs,
+                             const uint16_t* bias, uint16_t* out, int64_t M, int64_t N, int64_t K,
+                             const SmallFuse* fuse, hipStream_t stream);
+// The amax pass alone (the first kernel of launch_quantize).
+hipError_t launch_amax(const uint16_t* x, int64_t n_elems, uint32_t* partial, hipStream_t stream);
+
+// launch_gemm without the small-tile route (the 256 x 256 / 128 x 128 lane
+// kernel or the workgroup-shared kernel, as gemm_plan chooses).
+hipError_t launch_gemm_regular(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_gs,
+                               const uint8_t* b_codes, const uint8_t* b_scales, const float* b_gs,
+                               const uint16_t* bias, uint16_t* out, int64_t M, int64_t N, int64_t K,
+                               void* workspace, size_t workspace_bytes, hipStream_t stream);
+
 hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_gs,
                        const uint8_t* b_codes, const uint8_t* b_scales, const float* b_gs,
                        const uint16_t* bias, uint16_t* out, int64_t M, int64_t N, int64_t K,

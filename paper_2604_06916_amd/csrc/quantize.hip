@@ -33,7 +33,8 @@ constexpr int kQuantThreads = 256;
 __device__ __forceinline__ u32x4_t stream_load(const uint4* p) {
   return __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
 }
-constexpr int kEncodeUnroll = 8;   // pieces per lane per iteration
+constexpr int kEncodeUnroll = 8;   // pieces per lane per iteration (large tensors)
+constexpr int kEncodeUnrollSmall = 2;   // for small tensors: four times the workgroups
 
 __global__ __launch_bounds__(kQuantThreads) void amax_partial_kernel(
     const uint4* __restrict__ x, int64_t n_vec, uint32_t* __restrict__ partial) {
@@ -87,20 +88,20 @@ __device__ __forceinline__ uint32_t pair_max(uint32_t v) {
 // code words.  rtab[c] = 1 / (value(c) * alpha) (0 for c == 0, so a
 // zero-scale block becomes signed zeros: x * 0 keeps the sign).  kGuard: the
 // iteration reaches past the last piece (uniform choice per iteration).
-template <bool kGuard>
+template <bool kGuard, int kU>
 __device__ __forceinline__ void encode_iter(const u32x4_t* __restrict__ x, int64_t npieces,
                                             int64_t base, float t, bool zero_tensor,
                                             const float* rtab, uint32_t* __restrict__ codes,
                                             uint8_t* __restrict__ scales) {
   const int lane = threadIdx.x & (kWave - 1);
-  u32x4_t v[kEncodeUnroll];
+  u32x4_t v[kU];
 #pragma unroll
-  for (int u = 0; u < kEncodeUnroll; ++u) {
+  for (int u = 0; u < kU; ++u) {
     const int64_t p = base + u * kQuantThreads + threadIdx.x;
     v[u] = (!kGuard || p < npieces) ? __builtin_nontemporal_load(&x[p]) : u32x4_t{0, 0, 0, 0};
   }
 #pragma unroll
-  for (int u = 0; u < kEncodeUnroll; ++u) {
+  for (int u = 0; u < kU; ++u) {
     const int64_t p = base + u * kQuantThreads + threadIdx.x;
     const uint32_t w[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
     ushort2_t m = as_us2(w[0] & 0x7FFF7FFFu);
@@ -128,6 +129,7 @@ __device__ __forceinline__ void encode_iter(const u32x4_t* __restrict__ x, int64
   }
 }
 
+template <int kU>
 __global__ __launch_bounds__(kQuantThreads) void nvfp4_encode_kernel(
     const u32x4_t* __restrict__ x, int64_t npieces, const uint32_t* __restrict__ partial,
     int npartial, uint32_t* __restrict__ codes, uint8_t* __restrict__ scales,
@@ -159,13 +161,13 @@ __global__ __launch_bounds__(kQuantThreads) void nvfp4_encode_kernel(
   }
   __syncthreads();
 
-  const int64_t per_iter = (int64_t)kQuantThreads * kEncodeUnroll;
+  const int64_t per_iter = (int64_t)kQuantThreads * kU;
   for (int64_t base = (int64_t)blockIdx.x * per_iter; base < npieces;
        base += (int64_t)gridDim.x * per_iter) {
     if (base + per_iter <= npieces)
-      encode_iter<false>(x, npieces, base, t, zero_tensor, rtab, codes, scales);
+      encode_iter<false, kU>(x, npieces, base, t, zero_tensor, rtab, codes, scales);
     else
-      encode_iter<true>(x, npieces, base, t, zero_tensor, rtab, codes, scales);
+      encode_iter<true, kU>(x, npieces, base, t, zero_tensor, rtab, codes, scales);
   }
 }
 
@@ -198,15 +200,22 @@ hipError_t scratch_address(uint32_t** out) {
 }
 
 int amax_partial_count(int64_t n_elems) {
-  // one workgroup per 64 Ki elements, rounded up to a whole number of
+  // one workgroup per 64 Ki elements (down to 4 Ki for small tensors, so
+  // that they still spread over many CUs), rounded up to a whole number of
   // workgroups per compute unit (256 of them) so that every CU streams the
   // same amount, at most kMaxPartials
-  const int64_t per_wg = 64 * 1024;
+  int64_t per_wg = n_elems / 256;
+  per_wg = per_wg < 4096 ? 4096 : per_wg > 65536 ? 65536 : per_wg;
   int64_t p = (n_elems + per_wg - 1) / per_wg;
   if (p > 256) p = (p + 255) / 256 * 256;
   if (p < 1) p = 1;
   if (p > kMaxPartials) p = kMaxPartials;
   return (int)p;
+}
+
+hipError_t launch_amax(const uint16_t* x, int64_t n, uint32_t* partial, hipStream_t stream) {
+  return launch_kernel(amax_partial_kernel, dim3(amax_partial_count(n)), dim3(kQuantThreads), stream,
+                       reinterpret_cast<const uint4*>(x), n / 8, partial);
 }
 
 hipError_t launch_quantize(const uint16_t* x, int64_t rows, int64_t K, uint8_t* codes,
@@ -215,14 +224,18 @@ hipError_t launch_quantize(const uint16_t* x, int64_t rows, int64_t K, uint8_t* 
   const int64_t n = rows * K;
   const int64_t npieces = n / 8;           // 8 elements per lane, 2 lanes per block
   const int npartial = amax_partial_count(n);
-  hipError_t e = launch_kernel(amax_partial_kernel, dim3(npartial), dim3(kQuantThreads), stream,
-                               reinterpret_cast<const uint4*>(x), n / 8, partial);
+  hipError_t e = launch_amax(x, n, partial, stream);
   if (e != hipSuccess) return e;
-  const int64_t per_wg = (int64_t)kQuantThreads * kEncodeUnroll;
+  // small tensors (under 64 workgroups of the large unroll) take the small
+  // unroll, so that they spread over four times as many CUs; the arithmetic
+  // per piece is the same
+  const bool small = npieces < 64 * (int64_t)kQuantThreads * kEncodeUnroll;
+  const int64_t per_wg = (int64_t)kQuantThreads * (small ? kEncodeUnrollSmall : kEncodeUnroll);
   int64_t grid = (npieces + per_wg - 1) / per_wg;
   if (grid > kEncodeMaxGrid) grid = kEncodeMaxGrid;
   if (grid < 1) grid = 1;
-  return launch_kernel(nvfp4_encode_kernel, dim3((unsigned)grid), dim3(kQuantThreads), stream,
+  return launch_kernel(small ? nvfp4_encode_kernel<kEncodeUnrollSmall> : nvfp4_encode_kernel<kEncodeUnroll>,
+                       dim3((unsigned)grid), dim3(kQuantThreads), stream,
                        reinterpret_cast<const u32x4_t*>(x), npieces, partial, npartial,
                        reinterpret_cast<uint32_t*>(codes), scales, global_scale);
 }

@@ -98,13 +98,13 @@ def test_gemm_workspace_plan():
     # K % 128 == 64 (a half last stage) splits too: the split is what makes
     # the lane kernel worth taking over the shared one there
     assert G(8192, 6720, 2240) == bytes_for(864 % 256)
-    # 128 x 128 tiles split as well, given enough K stages: 24 tiles of 24
-    # stages, 9 of 36 and 72 of 18 do; the 128-token 1152 -> 1152 layer's 9
-    # tiles of 9 stages gain nothing
-    assert G(128, 3072, 3072) == small_bytes_for(24)
-    assert G(128, 1152, 4608) == small_bytes_for(9)
+    # 128 x 128 tiles split as well, given enough K stages: 72 tiles of 24
+    # and of 36 stages, and 72 of 18 (a half last stage) do
+    assert G(384, 3072, 3072) == small_bytes_for(72)
+    assert G(256, 4608, 4608) == small_bytes_for(72)
     assert G(512, 2240, 2240) == small_bytes_for(72)
-    assert G(128, 1152, 1152) == 0
+    # fewer tokens with K % 128 == 0 run on 64 x 64 tiles, which never split
+    assert G(128, 1152, 1152) == 0 and G(128, 3072, 3072) == 0 and G(128, 1152, 4608) == 0
     assert G(0, 3072, 3072) == 0 and G(18432, 0, 3072) == 0
 
 

@@ -66,9 +66,10 @@ def test_golden_gemms():
 # 272, 289, 306 and 272 tiles, the second with a partial last stage, the
 # third with N % 8 != 0, the fourth with a half last stage).
 SPLIT_SHAPES = [(4352, 4096, 1536), (4352, 4200, 1440), (4353, 4100, 1536), (4352, 4096, 1600)]
-# 128 x 128 tiles split too when K is long: 24 tiles of 24 stages, 9 of 36,
-# 72 of 18 (a half last stage), and a ragged 3 x 7 tiles with N % 8 != 0
-SMALL_SPLIT_SHAPES = [(128, 3072, 3072), (128, 1152, 4608), (512, 2240, 2240), (300, 836, 4096)]
+# 128 x 128 tiles split too when K is long: 72 tiles of 24 and of 36
+# stages, 72 of 18 (a half last stage), and a ragged 3 x 29 tiles with
+# N % 8 != 0 (shapes whose 64 x 64 tiles fit in one round take the small kernel)
+SMALL_SPLIT_SHAPES = [(384, 3072, 3072), (256, 4608, 4608), (512, 2240, 2240), (300, 3604, 4096)]
 
 
 @pytest.mark.parametrize("M,N,K", [(1, 1, 16), (3, 5, 32), (37, 70, 64), (300, 260, 48),
@@ -166,9 +167,11 @@ def test_wide_dynamic_range_vs_oracle(kind):
     check_elements(got, a, b, ref)
 
 
+# (64, 64, 128), (128, 1152, 1152), (96, 300, 3072), (1, 9, 128),
+# (65, 130, 1152) and (200, 3000, 256) take the 64 x 64 kernel
 SHAPES = [(1, 1, 16), (5, 7, 32), (64, 64, 128), (255, 257, 48), (300, 520, 272),
           (257, 129, 2240), (128, 1152, 1152), (513, 260, 5600), (96, 300, 3072),
-          (260, 2049, 256), (513, 777, 640), (1, 9, 128),
+          (260, 2049, 256), (513, 777, 640), (1, 9, 128), (65, 130, 1152), (200, 3000, 256),
           (2100, 9000, 3072)]   # 256 x 256 tiles
 
 
@@ -277,3 +280,27 @@ def test_deterministic():
     r1 = gpu_gemm(ac, as_, aa, bc, bs, ba)
     r2 = gpu_gemm(ac, as_, aa, bc, bs, ba)
     assert np.array_equal(r1, r2)
+
+
+@pytest.mark.parametrize("M,N,K", [(128, 1152, 1152), (65, 130, 1152), (200, 3000, 256)])
+def test_small_tiles_match_the_lane_kernel(M, N, K):
+    """The 64 x 64 kernel uses the lane kernel's dequantization, K order and
+    epilogue, so it must give the lane kernel's output bit for bit.  The
+    lane kernel is reached with the same operands padded by 64 zero
+    elements along K (codes 0 under scale 0): K % 128 == 64 does not take
+    the small kernel, and the padding adds only exact zeros to every sum."""
+    import paper_2604_06916_amd as sol2
+    assert sol2.gemm_plan(M, N, K)["kernel"] == "nvfp4_gemm_small_kernel"
+    assert sol2.gemm_plan(M, N, K + 64, with_workspace=False)["kernel"] == "nvfp4_gemm_lane_kernel"
+    ac, as_, aa = quantized("normal", M, K, 13)
+    bc, bs, ba = quantized(None, N, K, 14, sigma=0.02)
+    small = gpu_gemm(ac, as_, aa, bc, bs, ba)
+
+    def pad(c, sc):
+        return np.pad(c, ((0, 0), (0, 32))), np.pad(sc, ((0, 0), (0, 4)))
+    (acp, asp), (bcp, bsp) = pad(ac, as_), pad(bc, bs)
+    lane = gpu_gemm(acp, asp, aa, bcp, bsp, ba, split=False)
+    assert np.array_equal(small, lane)
+    ref = O.nvfp4_gemm_ref(ac, as_, aa, bc, bs, ba)
+    assert rel_fro(small, ref) <= TOL
+    check_elements(small, (ac, as_, aa), (bc, bs, ba), ref)
