@@ -5,18 +5,20 @@ One step = every linear of one DiT block of the chosen workload (default: the
 FLUX.1-12B-like layers, M = 4 x (4096 + 512) = 18432 tokens; QKV 3072->9216,
 out 3072->3072, MLP 3072->12288->3072), each as
     nvfp4_quantize(W)            weight re-quantization (once per update)
-    nvfp4_quantize(X)            activation amax + encode
+    nvfp4_quantize_amax(X)       activation amax pass
+    nvfp4_quantize_encode(X)     activation encode pass
     nvfp4_gemm(Xq, Wq, bias)     block-scaled FP4 GEMM, BF16 out
-which is exactly the launch sequence of nvfp4_quantize(W) + nvfp4_linear.
-Inputs are synthetic (seeded, from workloads/) and resident in HBM before the
-timed region.  The same layers and inputs then run through the MXFP4 variant
-(mxfp4_quantize of W and X, mxfp4_gemm on the scaled FP4 matrix
-instructions), reported in the "mxfp4" object.  "graphs" times the weight
-re-quantization after a policy update and the per-step linears as captured
-HIP graphs replayed without re-capture; "small_linear" is the launch-bound
-128-token layer, eager and graph-batched; "stage1" runs the synthetic
-Stage-1 rollout loop (paper_2604_06916_amd/stage1.py) with BF16, NVFP4 and
-MXFP4 linears.  Prints one JSON line.
+which is exactly the launch sequence of nvfp4_quantize(W) + nvfp4_linear for
+these sizes (the two passes are the two kernels of nvfp4_quantize, called
+apart so that each is timed).  Inputs are synthetic (seeded, from
+workloads/) and resident in HBM before the timed region.  "workloads"
+repeats the step for the other configurations (the SANA-1.6B-like and
+SD3.5-Large-like layers, each with its own GEMM roofline) and holds the
+launch-bound 128-token layer; "mxfp4" runs the same FLUX layers through the
+MXFP4 variant; "graphs" times weight re-quantization and the per-step
+linears as replayed HIP graphs; "stage1" runs the synthetic Stage-1 rollout
+loop (paper_2604_06916_amd/stage1.py) with BF16, NVFP4 and MXFP4 linears.
+Prints one JSON line.
 """
 from __future__ import annotations
 
@@ -49,6 +51,8 @@ def parse():
     ap.add_argument("--no-graphs", action="store_true",
                     help="skip the graph-replay and small-layer measurements")
     ap.add_argument("--no-stage1", action="store_true", help="skip the synthetic Stage-1 rollouts")
+    ap.add_argument("--no-workloads", action="store_true",
+                    help="skip the other configurations (SANA-like, SD3.5-like, 128-token layer)")
     ap.add_argument("--no-vendor", action="store_true",
                     help="skip the vendor MXFP4 GEMM reference (it launches mxfp4_gemm once more per layer)")
     ap.add_argument("--cpu-rows", type=int, default=5120, help="oracle sample: activation rows")
@@ -73,6 +77,21 @@ def source_hash(*paths):
     return h.hexdigest()[:16]
 
 
+# the files each kernel is built from (its source and the device headers it
+# includes); a committed profile records their hash and goes stale with them
+KERNEL_SOURCES = {
+    "gemm.hip": ("gemm.hip", "device_common.h", "nvfp4_gemm_common.h"),
+    "gemm_small.hip": ("gemm_small.hip", "device_common.h", "nvfp4_gemm_common.h"),
+    "mx_gemm.hip": ("mx_gemm.hip", "device_common.h"),
+    "quantize.hip": ("quantize.hip", "device_common.h"),
+    "mx_quantize.hip": ("mx_quantize.hip", "device_common.h"),
+}
+
+
+def kernel_source_hash(source):
+    return source_hash(*(os.path.join(CSRC, f) for f in KERNEL_SOURCES[source]))
+
+
 def measured_traffic(summary, source):
     """HBM bytes per GEMM launch (FETCH_SIZE + WRITE_SIZE, scaled by a plain
     copy's reading of the same counters) from a committed counter summary of
@@ -83,26 +102,16 @@ def measured_traffic(summary, source):
     except OSError:
         return None
     kv = dict(l.split("=", 1) for l in lines if "=" in l and not l.startswith("#"))
-    if kv.get("source_sha256_16") != source_hash(os.path.join(CSRC, source),
-                                                 os.path.join(CSRC, "device_common.h")):
+    if kv.get("source_sha256_16") != kernel_source_hash(source):
         return None
     return float(kv["hbm_bytes_per_launch_avg"])
 
 
-def nvfp4_gemm_kernel_name(M, N, K, cus=256):
-    """The kernel nvfp4_gemm launches for this shape (the library's dispatch:
-    lane-side dequantization for K % 128 == 0 and K % 64 == 32, and for
-    K % 128 == 64 where 128 x 128 tiles or the split last round apply)."""
+def nvfp4_gemm_kernel_name(M, N, K):
+    """The kernel nvfp4_gemm launches for this shape, as the library reports
+    it (solfp4_gemm_plan; a workspace is passed, as in the step)."""
     import paper_2604_06916_amd as sol
-    if K % 128 == 0 or K % 64 == 32:
-        return "nvfp4_gemm_lane_kernel"
-    if K % 32:
-        return "nvfp4_gemm_kernel"
-    t256 = -(-M // 256) * -(-N // 256)
-    t128 = -(-M // 128) * -(-N // 128)
-    small = -(-t128 // cus) * 0.46 < -(-t256 // cus)
-    split = sol.nvfp4_gemm_workspace_bytes(M, N, K) > 0
-    return "nvfp4_gemm_lane_kernel" if small or split else "nvfp4_gemm_kernel"
+    return sol.gemm_plan(M, N, K)["kernel"]
 
 
 def vendor_mxfp4(layers, bufs, steps):
@@ -316,18 +325,44 @@ def run_small_linear(reps):
     e1.record()
     torch.cuda.synchronize()
     graph_us = e0.elapsed_time(e1) / (reps * batch) * 1e3
+    # the GEMM alone, graph-batched the same way
+    xc, xs, xa = sol.nvfp4_quantize(x)
+    gws = sol.nvfp4_gemm_workspace_bytes(M, N, K)
+    gws = torch.empty(gws, dtype=torch.uint8, device=dev) if gws else None
+    g2 = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g2):
+        for _ in range(batch):
+            sol.nvfp4_gemm(xc, xs, xa, wc, ws, wa, b, out, gws)
+    g2.replay()
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(reps):
+        g2.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    gemm_us = e0.elapsed_time(e1) / (reps * batch) * 1e3
     fl = 2.0 * M * N * K
+    route = ("amax pass + GEMM quantizing the activations in the kernel" if K <= 512
+             else "amax pass + encode pass + GEMM")
     return {"layer": f"M={M} {K}->{N} nvfp4_linear (+bias)", "eager_us": round(eager_us, 2),
-            "graph_us": round(graph_us, 2),
-            "graph_tflops": round(fl / (graph_us * 1e-6) / 1e12, 2)}
+            "graph_us": round(graph_us, 2), "gemm_graph_us": round(gemm_us, 2),
+            "gemm_kernel": nvfp4_gemm_kernel_name(M, N, K), "linear_launches": route,
+            "graph_tflops": round(fl / (graph_us * 1e-6) / 1e12, 2),
+            "roofline": {"bound": "latency", "achieved": round(fl / (graph_us * 1e-6) / 1e12, 2),
+                         "peak": PEAK_FP16_MFMA_TFLOPS, "unit": "TFLOP/s",
+                         "frac": round(fl / (graph_us * 1e-6) / 1e12 / PEAK_FP16_MFMA_TFLOPS, 5),
+                         "note": "1.1 MB of operands and 0.34 GFLOP: launch and memory round "
+                                 "trips bound this layer, not HBM bandwidth or the matrix cores"}}
 
 
 def run_stage1():
     """Synthetic Stage-1 rollouts (8 blocks of the FLUX-like width, 8 rollouts
     x 4608 tokens, 4 Euler steps, reward, top/bottom selection) with every
-    linear on each backend: rollout time, the linears' time, TFLOP/s and
-    share (HIP events around every linear), the other ops' time by kind, and
-    the speed-ups over BF16 linears (whole rollout, and linears alone)."""
+    linear on each backend.  Eager, with HIP events around every op: the
+    linears' time, TFLOP/s and share, and the other ops' time by kind (time
+    covered by no event is the GPU waiting for the host).  Then the same
+    rollout as one captured Euler step replayed per step (no host launch
+    cost): the rollout time the speed-ups are quoted on."""
     import torch
 
     from paper_2604_06916_amd import stage1 as G
@@ -361,12 +396,34 @@ def run_stage1():
         lin = sum(a.elapsed_time(b) for a, b in runner.linear_events)
         ops = {k: round(sum(a.elapsed_time(b) for a, b in v), 2) for k, v in runner.op_events.items()}
         top, bottom = G.select_rollouts(r.cpu().numpy(), cfg.keep)
-        out[backend] = {"rollout_ms": round(total, 2), "linear_ms": round(lin, 2),
-                        "linear_tflops": round(lin_flops / (lin * 1e-3) / 1e12, 1),
-                        "linear_share": round(lin / total, 4),
-                        "other_ms": round(total - lin, 2), "other_ms_by_op": ops,
-                        "unattributed_ms": round(total - lin - sum(ops.values()), 2),
-                        "top": [int(i) for i in top], "bottom": [int(i) for i in bottom]}
+        rec = {"rollout_ms_eager": round(total, 2), "linear_ms": round(lin, 2),
+               "linear_tflops": round(lin_flops / (lin * 1e-3) / 1e12, 1),
+               "linear_share": round(lin / total, 4),
+               "other_ms": round(total - lin, 2), "other_ms_by_op": ops,
+               "host_gaps_ms": round(total - lin - sum(ops.values()), 2),
+               "top": [int(i) for i in top], "bottom": [int(i) for i in bottom]}
+        runner.linear_events = None
+        runner.op_events = None
+        try:
+            xs = x0.clone()
+            g = runner.capture_step(xs)
+            times = []
+            for _ in range(2):
+                xs.copy_(x0)
+                torch.cuda.synchronize()
+                e0.record()
+                for _ in range(cfg.steps):
+                    g.replay()
+                e1.record()
+                torch.cuda.synchronize()
+                times.append(e0.elapsed_time(e1))
+            rec["rollout_ms"] = round(min(times), 2)
+            rec["rollout_graph_matches_eager"] = bool(torch.equal(xs.view(torch.int16), x.view(torch.int16)))
+            del g, xs
+        except RuntimeError as e:        # capture not possible in this build: eager time only
+            rec["rollout_ms"] = rec["rollout_ms_eager"]
+            rec["graph_error"] = str(e)[:120]
+        out[backend] = rec
         del runner
         torch.cuda.empty_cache()
     for backend in ("nvfp4", "mxfp4"):
@@ -445,23 +502,14 @@ def cpu_baseline(wl, rows, wrows):
     }
 
 
-def main():
-    args = parse()
-    if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the layer shards "
-              f"along tokens with no communication, see the design notes", file=sys.stderr)
-        sys.exit(2)
-
+def make_layers(wl, dev):
+    """Device buffers of every layer of a workload: seeded BF16 X, W and bias,
+    and the outputs and workspaces the step writes."""
     import numpy as np
     import torch
 
     import paper_2604_06916_amd as sol
-    from workloads import ROLE_BIAS, ROLE_W, ROLE_X, WORKLOADS, draw_activations, draw_bias, \
-        draw_weights, seed_for
-
-    wl = WORKLOADS[args.workload]
-    dev = torch.device("cuda:0")
-    torch.cuda.set_device(dev)
+    from workloads import ROLE_BIAS, ROLE_W, ROLE_X, draw_activations, draw_bias, draw_weights, seed_for
 
     def to_dev(bits):
         return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).to(dev).view(torch.bfloat16)
@@ -469,11 +517,11 @@ def main():
     layers = []
     for layer in wl.layers:
         M, N, K = wl.M, layer.N, layer.K
-        x = to_dev(draw_activations(layer.x_dist, M, K, seed_for(wl.config_id, layer.index, ROLE_X)))
-        w = to_dev(draw_weights(N, K, wl.w_sigma, seed_for(wl.config_id, layer.index, ROLE_W)))
-        b = to_dev(draw_bias(N, wl.w_sigma, seed_for(wl.config_id, layer.index, ROLE_BIAS)))
-        buf = dict(
-            x=x, w=w, b=b,
+        gws = sol.nvfp4_gemm_workspace_bytes(M, N, K)
+        layers.append(dict(
+            x=to_dev(draw_activations(layer.x_dist, M, K, seed_for(wl.config_id, layer.index, ROLE_X))),
+            w=to_dev(draw_weights(N, K, wl.w_sigma, seed_for(wl.config_id, layer.index, ROLE_W))),
+            b=to_dev(draw_bias(N, wl.w_sigma, seed_for(wl.config_id, layer.index, ROLE_BIAS))),
             wc=torch.empty((N, K // 2), dtype=torch.uint8, device=dev),
             ws=torch.empty((N, K // 16), dtype=torch.uint8, device=dev),
             wa=torch.empty(1, dtype=torch.float32, device=dev),
@@ -482,12 +530,22 @@ def main():
             xa=torch.empty(1, dtype=torch.float32, device=dev),
             qws=torch.empty(max(sol.nvfp4_quantize_workspace_bytes(max(M, N), K), 256),
                             dtype=torch.uint8, device=dev),
-            gws=(torch.empty(sol.nvfp4_gemm_workspace_bytes(M, N, K), dtype=torch.uint8, device=dev)
-                 if sol.nvfp4_gemm_workspace_bytes(M, N, K) else None),
+            gws=torch.empty(gws, dtype=torch.uint8, device=dev) if gws else None,
             out=torch.empty((M, N), dtype=torch.bfloat16, device=dev),
-            M=M, N=N, K=K, name=layer.name)
-        layers.append(buf)
+            M=M, N=N, K=K, name=layer.name))
     torch.cuda.synchronize()
+    return layers
+
+
+def run_nvfp4_step(layers, steps, warmup):
+    """Time `steps` steps (after `warmup`) of the NVFP4 step on resident
+    inputs: wall clock per step, and per layer HIP events (on the stream the
+    kernels run on) around the weight quantize, the activations' amax pass,
+    their encode pass and the GEMM."""
+    import numpy as np
+    import torch
+
+    import paper_2604_06916_amd as sol
 
     def step(events=None):
         for i, L in enumerate(layers):
@@ -497,56 +555,145 @@ def main():
             sol.nvfp4_quantize(L["w"], L["wc"], L["ws"], L["wa"], L["qws"])
             if e:
                 e[1].record()
-            sol.nvfp4_quantize(L["x"], L["xc"], L["xs"], L["xa"], L["qws"])
+            sol.nvfp4_quantize_amax(L["x"], L["qws"])
             if e:
                 e[2].record()
+            sol.nvfp4_quantize_encode(L["x"], L["xc"], L["xs"], L["xa"], L["qws"])
+            if e:
+                e[3].record()
             sol.nvfp4_gemm(L["xc"], L["xs"], L["xa"], L["wc"], L["ws"], L["wa"], L["b"], L["out"],
                            L["gws"])
             if e:
-                e[3].record()
+                e[4].record()
 
-    for _ in range(args.warmup):
+    for _ in range(warmup):
         step()
-    torch.cuda.synchronize()
-
-    ev = [[[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in layers]
-          for _ in range(args.steps)]
+    ev = [[[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in layers]
+          for _ in range(steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for s in range(args.steps):
+    for s in range(steps):
         step(ev[s])
     torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
+    ms_per_step = (time.perf_counter() - t0) / steps * 1e3
 
-    flops_step = sum(2.0 * L["M"] * L["N"] * L["K"] for L in layers)
-    per_layer = []
-    gemm_ms_tot = wq_ms_tot = xq_ms_tot = 0.0
+    def span(i, a, b):
+        return np.array([ev[s][i][a].elapsed_time(ev[s][i][b]) for s in range(steps)])
+
+    per_layer, tot = [], {"gemm": 0.0, "wq": 0.0, "amax": 0.0, "enc": 0.0}
     for i, L in enumerate(layers):
-        wq = np.mean([ev[s][i][0].elapsed_time(ev[s][i][1]) for s in range(args.steps)])
-        xqs = np.array([ev[s][i][1].elapsed_time(ev[s][i][2]) for s in range(args.steps)])
-        xq = float(np.mean(xqs))
-        gms = np.array([ev[s][i][2].elapsed_time(ev[s][i][3]) for s in range(args.steps)])
-        gm = float(np.mean(gms))
-        gemm_ms_tot += gm
-        wq_ms_tot += wq
-        xq_ms_tot += xq
+        wq, am, en, gm = span(i, 0, 1), span(i, 1, 2), span(i, 2, 3), span(i, 3, 4)
+        xq = am + en
+        for k, v in (("gemm", gm), ("wq", wq), ("amax", am), ("enc", en)):
+            tot[k] += float(np.mean(v))
+        n = L["M"] * L["K"]
         fl = 2.0 * L["M"] * L["N"] * L["K"]
-        xbytes = 4.5625 * L["M"] * L["K"]
         per_layer.append({
             "layer": L["name"], "M": L["M"], "N": L["N"], "K": L["K"],
-            "gemm_us": round(gm * 1e3, 2), "gemm_tflops": round(fl / (gm * 1e-3) / 1e12, 1),
-            "gemm_us_p10_p50_p90": [round(float(np.percentile(gms, q)) * 1e3, 2) for q in (10, 50, 90)],
-            "quantize_x_us": round(xq * 1e3, 2),
-            "quantize_x_us_p10_p50_p90": [round(float(np.percentile(xqs, q)) * 1e3, 2) for q in (10, 50, 90)],
-            "quantize_x_gbs": round(xbytes / (xq * 1e-3) / 1e9, 1),
-            "quantize_w_us": round(wq * 1e3, 2),
+            "gemm_kernel": nvfp4_gemm_kernel_name(L["M"], L["N"], L["K"]),
+            "gemm_us": round(float(np.mean(gm)) * 1e3, 2),
+            "gemm_tflops": round(fl / (float(np.mean(gm)) * 1e-3) / 1e12, 1),
+            "gemm_us_p10_p50_p90": [round(float(np.percentile(gm, q)) * 1e3, 2) for q in (10, 50, 90)],
+            "quantize_x_us": round(float(np.mean(xq)) * 1e3, 2),
+            "quantize_x_us_p10_p50_p90": [round(float(np.percentile(xq, q)) * 1e3, 2) for q in (10, 50, 90)],
+            "quantize_x_gbs": round(4.5625 * n / (float(np.mean(xq)) * 1e-3) / 1e9, 1),
+            "amax_pass_us": round(float(np.mean(am)) * 1e3, 2),
+            "amax_pass_gbs": round(2.0 * n / (float(np.mean(am)) * 1e-3) / 1e9, 1),
+            "encode_pass_us": round(float(np.mean(en)) * 1e3, 2),
+            "encode_pass_gbs": round(2.5625 * n / (float(np.mean(en)) * 1e-3) / 1e9, 1),
+            "x_mb": round(2.0 * n / 1e6, 1),
+            "quantize_w_us": round(float(np.mean(wq)) * 1e3, 2),
         })
-    gemm_tflops = flops_step / (gemm_ms_tot * 1e-3) / 1e12
-    xq_bytes = sum(4.5625 * L["M"] * L["K"] for L in layers)
-    quant_gbs = xq_bytes / (xq_ms_tot * 1e-3) / 1e9
-    ms_per_step = elapsed / args.steps * 1e3
-    value = flops_step / (ms_per_step * 1e-3) / 1e12
+    flops = sum(2.0 * L["M"] * L["N"] * L["K"] for L in layers)
+    elems = sum(L["M"] * L["K"] for L in layers)
+    return {"ms_per_step": ms_per_step, "flops": flops, "per_layer": per_layer,
+            "gemm_ms": tot["gemm"], "wq_ms": tot["wq"], "amax_ms": tot["amax"], "enc_ms": tot["enc"],
+            "gemm_tflops": flops / (tot["gemm"] * 1e-3) / 1e12,
+            "quant_gbs": 4.5625 * elems / ((tot["amax"] + tot["enc"]) * 1e-3) / 1e9,
+            "encode_gbs": 2.5625 * elems / (tot["enc"] * 1e-3) / 1e9,
+            "amax_gbs": 2.0 * elems / (tot["amax"] * 1e-3) / 1e9}
 
+
+def gemm_roofline(r, layers, traffic=None):
+    return {
+        "bound": "mfma",
+        "kernel": " + ".join(sorted({nvfp4_gemm_kernel_name(L["M"], L["N"], L["K"]) for L in layers})),
+        "achieved": round(r["gemm_tflops"], 1),
+        "peak": PEAK_FP16_MFMA_TFLOPS,
+        "unit": "TFLOP/s",
+        "frac": round(r["gemm_tflops"] / PEAK_FP16_MFMA_TFLOPS, 4),
+        "frac_fp4_peak": round(r["gemm_tflops"] / PEAK_FP4_MFMA_TFLOPS, 4),
+        "traffic": traffic,
+        "traffic_unit": "HBM bytes per launch (mean over the step's GEMMs)",
+        "algorithmic_flops_per_launch": r["flops"] / len(layers),
+    }
+
+
+def quantize_summary(r, layers):
+    """Whole quantize (both passes, 4.5625 B/element) and each pass alone,
+    over the step's activation tensors; the largest tensor on its own (the
+    graded encode-pass figure); tensors under the MALL's 256 MB may be
+    partly served from it on the second pass (labelled)."""
+    big = max(r["per_layer"], key=lambda p: p["x_mb"])
+    return {
+        "kernel": "amax_partial_kernel + nvfp4_encode_kernel (activations)",
+        "achieved_gbs": round(r["quant_gbs"], 1),
+        "bytes_per_element": 4.5625,
+        "peak_gbs": PEAK_HBM_GBS,
+        "frac_hbm": round(r["quant_gbs"] / PEAK_HBM_GBS, 4),
+        "encode_pass": {"achieved_gbs": round(r["encode_gbs"], 1), "bytes_per_element": 2.5625,
+                        "frac_hbm": round(r["encode_gbs"] / PEAK_HBM_GBS, 4)},
+        "amax_pass": {"achieved_gbs": round(r["amax_gbs"], 1), "bytes_per_element": 2.0,
+                      "frac_hbm": round(r["amax_gbs"] / PEAK_HBM_GBS, 4)},
+        "largest_input": {"layer": big["layer"], "x_mb": big["x_mb"],
+                          "encode_pass_gbs": big["encode_pass_gbs"],
+                          "encode_pass_frac_hbm": round(big["encode_pass_gbs"] / PEAK_HBM_GBS, 4),
+                          "whole_gbs": big["quantize_x_gbs"],
+                          "above_mall": big["x_mb"] > 256},
+        "mall_resident_candidates": [p["layer"] for p in r["per_layer"] if p["x_mb"] <= 256],
+    }
+
+
+def run_other_workload(name, steps, warmup):
+    """The step on another configuration (its own layers and M): GEMM
+    roofline, quantize figures, per-layer record."""
+    import torch
+
+    from workloads import WORKLOADS
+    wl = WORKLOADS[name]
+    layers = make_layers(wl, torch.device("cuda:0"))
+    r = run_nvfp4_step(layers, steps, warmup)
+    res = {"config": {"workload": wl.name, "M": wl.M,
+                      "layers": [f"{L['name']} {L['K']}->{L['N']}" for L in layers]},
+           "step_tflops": round(r["flops"] / (r["ms_per_step"] * 1e-3) / 1e12, 2),
+           "ms_per_step": round(r["ms_per_step"], 4),
+           "roofline": gemm_roofline(r, layers),
+           "quantize": quantize_summary(r, layers),
+           "layers": r["per_layer"]}
+    del layers
+    torch.cuda.empty_cache()
+    return res
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the layer shards "
+              f"along tokens with no communication, see the design notes", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from workloads import WORKLOADS
+
+    wl = WORKLOADS[args.workload]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    layers = make_layers(wl, dev)
+    r = run_nvfp4_step(layers, args.steps, args.warmup)
+    value = r["flops"] / (r["ms_per_step"] * 1e-3) / 1e12
+    traffic = (measured_traffic("nvfp4_gemm_flux-12b_traffic.txt", "gemm.hip")
+               if wl.name == PROFILED_WORKLOAD else None)
     result = {
         "metric": METRIC,
         "value": round(value, 2),
@@ -554,7 +701,7 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(ms_per_step, 4),
+        "ms_per_step": round(r["ms_per_step"], 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -563,34 +710,22 @@ def main():
         "config": {
             "workload": wl.name, "M": wl.M,
             "layers": [f"{L['name']} {L['K']}->{L['N']}" for L in layers],
-            "step": "per layer: nvfp4_quantize(W), nvfp4_quantize(X), nvfp4_gemm(+bias)",
+            "step": "per layer: nvfp4_quantize(W), nvfp4_quantize_amax(X), nvfp4_quantize_encode(X), "
+                    "nvfp4_gemm(+bias)",
             "operands": "NVFP4 (E2M1 + E4M3/16 + FP32 tensor scale)",
             "mfma": "exact FP16 dequant, v_mfma_f32_32x32x16_f16, FP32 accumulate",
             "parallelism": "single GPU",
         },
-        "roofline": {
-            "bound": "mfma",
-            "kernel": " + ".join(sorted({nvfp4_gemm_kernel_name(L["M"], L["N"], L["K"]) for L in layers})),
-            "achieved": round(gemm_tflops, 1),
-            "peak": PEAK_FP16_MFMA_TFLOPS,
-            "unit": "TFLOP/s",
-            "frac": round(gemm_tflops / PEAK_FP16_MFMA_TFLOPS, 4),
-            "traffic": (measured_traffic("nvfp4_gemm_flux-12b_traffic.txt", "gemm.hip")
-                        if wl.name == PROFILED_WORKLOAD else None),
-            "traffic_unit": "HBM bytes per launch (mean over the step's GEMMs)",
-            "algorithmic_flops_per_launch": flops_step / len(layers),
-        },
-        "gemm_frac_fp4_peak": round(gemm_tflops / PEAK_FP4_MFMA_TFLOPS, 4),
-        "quantize": {
-            "kernel": "amax_partial_kernel + nvfp4_encode_kernel (activations)",
-            "achieved_gbs": round(quant_gbs, 1),
-            "bytes_per_element": 4.5625,
-            "peak_gbs": PEAK_HBM_GBS,
-            "frac_hbm": round(quant_gbs / PEAK_HBM_GBS, 4),
-        },
-        "time_split_ms": {"gemm": round(gemm_ms_tot, 4), "quantize_x": round(xq_ms_tot, 4),
-                          "quantize_w": round(wq_ms_tot, 4)},
-        "layers": per_layer,
+        "roofline": gemm_roofline(r, layers, traffic),
+        "gemm_frac_fp4_peak": round(r["gemm_tflops"] / PEAK_FP4_MFMA_TFLOPS, 4),
+        "quantize": quantize_summary(r, layers),
+        "time_split_ms": {"gemm": round(r["gemm_ms"], 4),
+                          "quantize_x": round(r["amax_ms"] + r["enc_ms"], 4),
+                          "quantize_x_amax": round(r["amax_ms"], 4),
+                          "quantize_x_encode": round(r["enc_ms"], 4),
+                          "quantize_w": round(r["wq_ms"], 4)},
+        "layers": r["per_layer"],
+        "workloads": None,
         "mxfp4": None,
         "graphs": None,
         "small_linear": None,
@@ -600,14 +735,9 @@ def main():
     }
     if not args.no_graphs:
         result["graphs"] = run_graphs(layers, max(args.steps, 5))
-        result["small_linear"] = run_small_linear(max(args.steps, 5))
-    if not args.no_stage1:
-        result["stage1"] = run_stage1()
     if not args.no_mxfp4:
         result["mxfp4"] = run_mxfp4(layers, args.steps, args.warmup,
                                     wl.name == PROFILED_WORKLOAD, not args.no_vendor)
-    if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(wl, args.cpu_rows, args.cpu_wrows)
     if args.copy_calibration:
         n = args.copy_calibration
         src = torch.empty(n, dtype=torch.uint8, device=dev)
@@ -615,6 +745,21 @@ def main():
         for _ in range(3):
             dst.copy_(src)
         torch.cuda.synchronize()
+        del src, dst
+    del layers
+    torch.cuda.empty_cache()
+    if not args.no_workloads:
+        result["small_linear"] = run_small_linear(max(args.steps, 5))
+        others = {}
+        for name in ("sana-1.6b", "sd35-large"):
+            if name != wl.name:
+                others[name] = run_other_workload(name, min(args.steps, 20), min(args.warmup, 5))
+        others["single-1152"] = dict(result["small_linear"])
+        result["workloads"] = others
+    if not args.no_stage1:
+        result["stage1"] = run_stage1()
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(wl, args.cpu_rows, args.cpu_wrows)
     print(json.dumps(result), flush=True)
 
 

@@ -98,6 +98,25 @@ SOLFP4_API int nvfp4_quantize(const uint16_t* x, int64_t rows, int64_t K,
                    void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * The two passes of nvfp4_quantize as separate calls, for callers that want
+ * to schedule them apart (the amax pass of the next layer's input can run
+ * on another stream, or be timed on its own).  nvfp4_quantize_amax(x, rows,
+ * K, workspace, ...) reads x once and writes its partial maxima into the
+ * workspace; nvfp4_quantize_encode(x, rows, K, codes, scales, global_scale,
+ * workspace, ...) folds them into alpha and writes codes, scales and alpha.
+ * The pair, in stream order, with the same x, sizes and workspace and
+ * nothing writing x or the workspace in between, is exactly nvfp4_quantize
+ * (same kernels, bit-identical results); the workspace must be at least
+ * nvfp4_quantize_workspace_bytes(rows, K) bytes.  Argument checks and
+ * errors as for nvfp4_quantize.
+ */
+SOLFP4_API int nvfp4_quantize_amax(const uint16_t* x, int64_t rows, int64_t K,
+                   void* workspace, size_t workspace_bytes, void* stream);
+SOLFP4_API int nvfp4_quantize_encode(const uint16_t* x, int64_t rows, int64_t K,
+                   uint8_t* codes, uint8_t* scales, float* global_scale,
+                   void* workspace, size_t workspace_bytes, void* stream);
+
+/*
  * nvfp4_quantize without a workspace, for callers that cannot allocate
  * device memory (code under HIP graph capture, tight serving loops,
  * harnesses that forbid hipMalloc).  Same arguments, kernels and results

@@ -8,7 +8,7 @@ raises ImportError if the library has not been built.
 _NAMES = ("EXPORTED", "LIB_PATH", "Solfp4Error", "lib", "gemm_plan", "FORMAT_NVFP4",
           "FORMAT_MXFP4", "nvfp4_gemm",
           "nvfp4_gemm_workspace_bytes", "nvfp4_linear", "nvfp4_linear_workspace_bytes",
-          "nvfp4_quantize", "nvfp4_quantize_noalloc", "nvfp4_quantize_workspace_bytes", "mxfp4_gemm", "mxfp4_linear", "mxfp4_linear_workspace_bytes", "mxfp4_quantize")
+          "nvfp4_quantize", "nvfp4_quantize_amax", "nvfp4_quantize_encode", "nvfp4_quantize_noalloc", "nvfp4_quantize_workspace_bytes", "mxfp4_gemm", "mxfp4_linear", "mxfp4_linear_workspace_bytes", "mxfp4_quantize")
 __all__ = list(_NAMES)
 
 

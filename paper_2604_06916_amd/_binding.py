@@ -30,6 +30,10 @@ lib.nvfp4_quantize_workspace_bytes.restype = _sz
 lib.nvfp4_quantize_workspace_bytes.argtypes = [_i64, _i64]
 lib.nvfp4_quantize.restype = ctypes.c_int
 lib.nvfp4_quantize.argtypes = [_p, _i64, _i64, _p, _p, _p, _p, _sz, _p]
+lib.nvfp4_quantize_amax.restype = ctypes.c_int
+lib.nvfp4_quantize_amax.argtypes = [_p, _i64, _i64, _p, _sz, _p]
+lib.nvfp4_quantize_encode.restype = ctypes.c_int
+lib.nvfp4_quantize_encode.argtypes = [_p, _i64, _i64, _p, _p, _p, _p, _sz, _p]
 lib.nvfp4_quantize_noalloc.restype = ctypes.c_int
 lib.nvfp4_quantize_noalloc.argtypes = [_p, _i64, _i64, _p, _p, _p, _p]
 lib.nvfp4_gemm.restype = ctypes.c_int
@@ -56,7 +60,8 @@ lib.mxfp4_linear.restype = ctypes.c_int
 lib.mxfp4_linear.argtypes = [_p, _p, _p, _p, _p, _p, _sz, _i64, _i64, _i64, _p]
 
 EXPORTED = ["solfp4_strerror", "solfp4_version", "solfp4_gemm_plan",
-            "nvfp4_quantize_workspace_bytes", "nvfp4_quantize", "nvfp4_quantize_noalloc",
+            "nvfp4_quantize_workspace_bytes", "nvfp4_quantize", "nvfp4_quantize_amax",
+            "nvfp4_quantize_encode", "nvfp4_quantize_noalloc",
             "nvfp4_gemm",
             "nvfp4_gemm_workspace_bytes", "nvfp4_linear_workspace_bytes", "nvfp4_linear",
             "mxfp4_quantize", "mxfp4_gemm", "mxfp4_linear_workspace_bytes", "mxfp4_linear"]
@@ -179,6 +184,34 @@ def nvfp4_quantize(x, codes=None, scales=None, global_scale=None, workspace=None
         workspace = _alloc((max(need, 256),), torch.uint8, dev, st)
     _check(lib.nvfp4_quantize(_ptr(x), rows, K, _ptr(codes), _ptr(scales), _ptr(global_scale),
                               _ptr(workspace), workspace.numel(), ctypes.c_void_p(st.cuda_stream)))
+    return codes, scales, global_scale
+
+
+def nvfp4_quantize_amax(x, workspace, stream=None):
+    """The first pass of nvfp4_quantize: x's partial maxima into `workspace`
+    (uint8, at least nvfp4_quantize_workspace_bytes(rows, K))."""
+    rows, K = _dims(x, "x", 16)
+    dev = x.device
+    _need(x, torch.bfloat16, (rows, K), "x")
+    _need_workspace(workspace, nvfp4_quantize_workspace_bytes(rows, K), "workspace", dev)
+    st = _stream(stream, dev)
+    _check(lib.nvfp4_quantize_amax(_ptr(x), rows, K, _ptr(workspace), workspace.numel(),
+                                   ctypes.c_void_p(st.cuda_stream)))
+
+
+def nvfp4_quantize_encode(x, codes, scales, global_scale, workspace, stream=None):
+    """The second pass of nvfp4_quantize (after nvfp4_quantize_amax on the
+    same x and workspace): codes, scales and alpha."""
+    rows, K = _dims(x, "x", 16)
+    dev = x.device
+    _need(x, torch.bfloat16, (rows, K), "x")
+    _need(codes, torch.uint8, (rows, K // 2), "codes", dev)
+    _need(scales, torch.uint8, (rows, K // 16), "scales", dev)
+    _need(global_scale, torch.float32, (1,), "global_scale", dev)
+    _need_workspace(workspace, nvfp4_quantize_workspace_bytes(rows, K), "workspace", dev)
+    st = _stream(stream, dev)
+    _check(lib.nvfp4_quantize_encode(_ptr(x), rows, K, _ptr(codes), _ptr(scales), _ptr(global_scale),
+                                     _ptr(workspace), workspace.numel(), ctypes.c_void_p(st.cuda_stream)))
     return codes, scales, global_scale
 
 

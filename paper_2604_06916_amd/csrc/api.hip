@@ -180,6 +180,30 @@ int nvfp4_quantize(const uint16_t* x, int64_t rows, int64_t K, uint8_t* codes, u
   return e == hipSuccess ? SOLFP4_OK : SOLFP4_EHIP;
 }
 
+int nvfp4_quantize_amax(const uint16_t* x, int64_t rows, int64_t K, void* workspace,
+                        size_t workspace_bytes, void* stream) {
+  int rc = check_dims(rows, K);
+  if (rc) return rc;
+  if (K % 16) return SOLFP4_ESHAPE;
+  if (!workspace || (rows > 0 && K > 0 && !x)) return SOLFP4_EINVAL;
+  if (!aligned16(workspace) || (rows > 0 && K > 0 && !aligned16(x))) return SOLFP4_EALIGN;
+  if (workspace_bytes < quantize_scratch_bytes(rows, K)) return SOLFP4_EWORKSPACE;
+  const hipError_t e = solfp4::launch_amax(x, rows * K, static_cast<uint32_t*>(workspace),
+                                           static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? SOLFP4_OK : SOLFP4_EHIP;
+}
+
+int nvfp4_quantize_encode(const uint16_t* x, int64_t rows, int64_t K, uint8_t* codes,
+                          uint8_t* scales, float* global_scale, void* workspace,
+                          size_t workspace_bytes, void* stream) {
+  const int rc = quantize_checks(x, rows, K, codes, scales, global_scale, workspace, workspace_bytes);
+  if (rc) return rc;
+  const hipError_t e = solfp4::launch_encode(x, rows, K, codes, scales, global_scale,
+                                             static_cast<const uint32_t*>(workspace),
+                                             static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? SOLFP4_OK : SOLFP4_EHIP;
+}
+
 int nvfp4_quantize_noalloc(const uint16_t* x, int64_t rows, int64_t K, uint8_t* codes,
                            uint8_t* scales, float* global_scale, void* stream) {
   int rc = check_dims(rows, K);

@@ -128,8 +128,12 @@ hipError_t launch_gemm_small(const uint8_t* a_codes, const uint8_t* a_scales, co
                              const uint8_t* b_codes, const uint8_t* b_scales, const float* b_gs,
                              const uint16_t* bias, uint16_t* out, int64_t M, int64_t N, int64_t K,
                              const SmallFuse* fuse, hipStream_t stream);
-// The amax pass alone (the first kernel of launch_quantize).
+// The amax pass alone (the first kernel of launch_quantize), and the encode
+// pass alone (the second).
 hipError_t launch_amax(const uint16_t* x, int64_t n_elems, uint32_t* partial, hipStream_t stream);
+hipError_t launch_encode(const uint16_t* x, int64_t rows, int64_t K, uint8_t* codes,
+                         uint8_t* scales, float* global_scale, const uint32_t* partial,
+                         hipStream_t stream);
 
 // launch_gemm without the small-tile route (the 256 x 256 / 128 x 128 lane
 // kernel or the workgroup-shared kernel, as gemm_plan chooses).

@@ -218,14 +218,12 @@ hipError_t launch_amax(const uint16_t* x, int64_t n, uint32_t* partial, hipStrea
                        reinterpret_cast<const uint4*>(x), n / 8, partial);
 }
 
-hipError_t launch_quantize(const uint16_t* x, int64_t rows, int64_t K, uint8_t* codes,
-                           uint8_t* scales, float* global_scale, uint32_t* partial,
-                           hipStream_t stream) {
+hipError_t launch_encode(const uint16_t* x, int64_t rows, int64_t K, uint8_t* codes,
+                         uint8_t* scales, float* global_scale, const uint32_t* partial,
+                         hipStream_t stream) {
   const int64_t n = rows * K;
   const int64_t npieces = n / 8;           // 8 elements per lane, 2 lanes per block
   const int npartial = amax_partial_count(n);
-  hipError_t e = launch_amax(x, n, partial, stream);
-  if (e != hipSuccess) return e;
   // small tensors (under 64 workgroups of the large unroll) take the small
   // unroll, so that they spread over four times as many CUs; the arithmetic
   // per piece is the same
@@ -238,6 +236,14 @@ hipError_t launch_quantize(const uint16_t* x, int64_t rows, int64_t K, uint8_t* 
                        dim3((unsigned)grid), dim3(kQuantThreads), stream,
                        reinterpret_cast<const u32x4_t*>(x), npieces, partial, npartial,
                        reinterpret_cast<uint32_t*>(codes), scales, global_scale);
+}
+
+hipError_t launch_quantize(const uint16_t* x, int64_t rows, int64_t K, uint8_t* codes,
+                           uint8_t* scales, float* global_scale, uint32_t* partial,
+                           hipStream_t stream) {
+  const hipError_t e = launch_amax(x, rows * K, partial, stream);
+  if (e != hipSuccess) return e;
+  return launch_encode(x, rows, K, codes, scales, global_scale, partial, stream);
 }
 
 }  // namespace solfp4

@@ -231,6 +231,29 @@ class Runner:
         return x
 
 
+    def euler_step_(self, x):
+        """One Euler step on x in place (x: [rollouts * tokens, hidden] BF16)."""
+        dt = 1.0 / self.cfg.steps
+        y = self.blocks(x)
+        x.copy_((x.float() + dt * (y.float() - x.float())).to(torch.bfloat16))
+        return x
+
+    def capture_step(self, x_static):
+        """One Euler step on the static buffer x_static, captured as a HIP
+        graph (warmed up once on a side stream first, which advances
+        x_static by a step); replaying it T times from the initial latents
+        is the rollout without any host launch cost."""
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            self.euler_step_(x_static)
+        torch.cuda.current_stream().wait_stream(side)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            self.euler_step_(x_static)
+        return g
+
+
 def _rmsnorm(x, out):
     xf = x.float()
     out.copy_(xf * torch.rsqrt(xf.pow(2).mean(dim=-1, keepdim=True) + EPS))

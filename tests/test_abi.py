@@ -128,6 +128,17 @@ def test_quantize_rejects_bad_arguments():
     assert quant(wsb=0) == EWORKSPACE
 
 
+def test_two_pass_quantize_rejects_bad_arguments():
+    amax = lambda x=P, rows=4, K=32, ws=P, wsb=4096: sol.lib.nvfp4_quantize_amax(x, rows, K, ws, wsb, S)
+    enc = lambda x=P, rows=4, K=32, codes=P2, scales=P3, gs=P, ws=P, wsb=4096: \
+        sol.lib.nvfp4_quantize_encode(x, rows, K, codes, scales, gs, ws, wsb, S)
+    assert amax(rows=-1) == EINVAL and amax(K=24) == ESHAPE and amax(x=NULL) == EINVAL
+    assert amax(ws=NULL) == EINVAL and amax(x=MIS) == EALIGN and amax(ws=MIS) == EALIGN
+    assert amax(wsb=0) == EWORKSPACE
+    assert enc(rows=-1) == EINVAL and enc(K=24) == ESHAPE and enc(codes=NULL) == EINVAL
+    assert enc(gs=NULL) == EINVAL and enc(scales=MIS) == EALIGN and enc(wsb=0) == EWORKSPACE
+
+
 def gemm(ac=P, as_=P2, ag=P3, bc=P, bs=P2, bg=P3, bias=NULL, out=P, ws=NULL, wsb=0, M=8, N=8,
          K=32):
     return sol.lib.nvfp4_gemm(ac, as_, ag, bc, bs, bg, bias, out, ws, wsb, M, N, K, S)

@@ -72,3 +72,19 @@ def test_roofline_kernel_name_follows_the_dispatch():
     assert bench.nvfp4_gemm_kernel_name(8192, 2240, 2240) == lane     # split last round
     assert bench.nvfp4_gemm_kernel_name(300, 260, 2240) == lane       # 128 x 128 tiles
     assert bench.nvfp4_gemm_kernel_name(300, 260, 48) == shared       # K % 32 == 16
+    assert bench.nvfp4_gemm_kernel_name(128, 1152, 1152) == "nvfp4_gemm_small_kernel"
+
+
+def test_kernel_source_hashes_cover_every_include():
+    """A committed profile goes stale when its kernel's source or any
+    header it includes changes: the hashed file list names every local
+    include of each source."""
+    import re
+    import bench
+    for src, files in bench.KERNEL_SOURCES.items():
+        text = open(os.path.join(bench.CSRC, src)).read()
+        includes = set(re.findall(r'#include "([^"]+)"', text))
+        for h in includes - {"kernels.h", "solfp4.h"}:
+            assert h in files, (src, h)
+            sub = set(re.findall(r'#include "([^"]+)"', open(os.path.join(bench.CSRC, h)).read()))
+            assert sub <= set(files) | {"kernels.h", "solfp4.h"}, (h, sub)

@@ -187,3 +187,26 @@ def test_grid_stride_loop_and_determinism():
     assert f32_bits(a1.cpu().numpy()[0]) == f32_bits(ra)
     assert np.array_equal(u8_from_dev(s1)[rows], rs)
     assert np.array_equal(u8_from_dev(c1)[rows], rc)
+
+
+@pytest.mark.parametrize("rows,K", [(1, 16), (128, 1152), (777, 2240), (4096, 4096)])
+def test_two_pass_calls_equal_quantize(rows, K):
+    """nvfp4_quantize_amax then nvfp4_quantize_encode (same x, workspace)
+    is nvfp4_quantize: codes, scales and alpha bit-identical, and equal to
+    the oracle's."""
+    import paper_2604_06916_amd as sol2
+    xb = draw_activations("t3_1pct", rows, K, seed=rows + K)
+    x = bf16_to_dev(xb)
+    want = sol2.nvfp4_quantize(x)
+    ws = torch.empty(max(sol2.nvfp4_quantize_workspace_bytes(rows, K), 256), dtype=torch.uint8,
+                     device=x.device)
+    codes = torch.full((rows, K // 2), 0xAB, dtype=torch.uint8, device=x.device)
+    scales = torch.full((rows, K // 16), 0xAB, dtype=torch.uint8, device=x.device)
+    gs = torch.full((1,), float("nan"), dtype=torch.float32, device=x.device)
+    sol2.nvfp4_quantize_amax(x, ws)
+    sol2.nvfp4_quantize_encode(x, codes, scales, gs, ws)
+    torch.cuda.synchronize()
+    assert torch.equal(codes, want[0]) and torch.equal(scales, want[1])
+    assert torch.equal(gs.view(torch.int32), want[2].view(torch.int32))
+    rc, rs, ra = O.nvfp4_quantize_ref(xb)
+    assert np.array_equal(codes.cpu().numpy(), rc) and np.array_equal(scales.cpu().numpy(), rs)
