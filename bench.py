@@ -5,12 +5,11 @@ One step = every linear of one DiT block of the chosen workload (default: the
 FLUX.1-12B-like layers, M = 4 x (4096 + 512) = 18432 tokens; QKV 3072->9216,
 out 3072->3072, MLP 3072->12288->3072), each as
     nvfp4_quantize(W)            weight re-quantization (once per update)
-    nvfp4_quantize_amax(X)       activation amax pass
-    nvfp4_quantize_encode(X)     activation encode pass
+    nvfp4_quantize(X)            activation amax + encode passes
     nvfp4_gemm(Xq, Wq, bias)     block-scaled FP4 GEMM, BF16 out
 which is exactly the launch sequence of nvfp4_quantize(W) + nvfp4_linear for
-these sizes (the two passes are the two kernels of nvfp4_quantize, called
-apart so that each is timed).  Inputs are synthetic (seeded, from
+these sizes; the two passes of the activation quantize are also timed one at
+a time (nvfp4_quantize_amax, nvfp4_quantize_encode).  Inputs are synthetic (seeded, from
 workloads/) and resident in HBM before the timed region.  "workloads"
 repeats the step for the other configurations (the SANA-1.6B-like and
 SD3.5-Large-like layers, each with its own GEMM roofline) and holds the
@@ -540,8 +539,10 @@ def make_layers(wl, dev):
 def run_nvfp4_step(layers, steps, warmup):
     """Time `steps` steps (after `warmup`) of the NVFP4 step on resident
     inputs: wall clock per step, and per layer HIP events (on the stream the
-    kernels run on) around the weight quantize, the activations' amax pass,
-    their encode pass and the GEMM."""
+    kernels run on) around the weight quantize, the activation quantize and
+    the GEMM.  Then, apart from the step, the activations' two quantize
+    passes called one at a time (nvfp4_quantize_amax, nvfp4_quantize_encode)
+    with events around each: the encode pass's own figure."""
     import numpy as np
     import torch
 
@@ -555,20 +556,17 @@ def run_nvfp4_step(layers, steps, warmup):
             sol.nvfp4_quantize(L["w"], L["wc"], L["ws"], L["wa"], L["qws"])
             if e:
                 e[1].record()
-            sol.nvfp4_quantize_amax(L["x"], L["qws"])
+            sol.nvfp4_quantize(L["x"], L["xc"], L["xs"], L["xa"], L["qws"])
             if e:
                 e[2].record()
-            sol.nvfp4_quantize_encode(L["x"], L["xc"], L["xs"], L["xa"], L["qws"])
-            if e:
-                e[3].record()
             sol.nvfp4_gemm(L["xc"], L["xs"], L["xa"], L["wc"], L["ws"], L["wa"], L["b"], L["out"],
                            L["gws"])
             if e:
-                e[4].record()
+                e[3].record()
 
     for _ in range(warmup):
         step()
-    ev = [[[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in layers]
+    ev = [[[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in layers]
           for _ in range(steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -577,14 +575,33 @@ def run_nvfp4_step(layers, steps, warmup):
     torch.cuda.synchronize()
     ms_per_step = (time.perf_counter() - t0) / steps * 1e3
 
+    # the two passes apart (after another layer's GEMM, as in the step)
+    reps = max(3, min(steps, 10))
+    pev = [[[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in layers]
+           for _ in range(reps)]
+    for r in range(reps):
+        for i, L in enumerate(layers):
+            P = layers[i - 1]
+            sol.nvfp4_gemm(P["xc"], P["xs"], P["xa"], P["wc"], P["ws"], P["wa"], P["b"], P["out"],
+                           P["gws"])
+            pev[r][i][0].record()
+            sol.nvfp4_quantize_amax(L["x"], L["qws"])
+            pev[r][i][1].record()
+            sol.nvfp4_quantize_encode(L["x"], L["xc"], L["xs"], L["xa"], L["qws"])
+            pev[r][i][2].record()
+    torch.cuda.synchronize()
+
     def span(i, a, b):
         return np.array([ev[s][i][a].elapsed_time(ev[s][i][b]) for s in range(steps)])
 
-    per_layer, tot = [], {"gemm": 0.0, "wq": 0.0, "amax": 0.0, "enc": 0.0}
+    def pspan(i, a, b):
+        return np.array([pev[r][i][a].elapsed_time(pev[r][i][b]) for r in range(reps)])
+
+    per_layer, tot = [], {"gemm": 0.0, "wq": 0.0, "xq": 0.0, "amax": 0.0, "enc": 0.0}
     for i, L in enumerate(layers):
-        wq, am, en, gm = span(i, 0, 1), span(i, 1, 2), span(i, 2, 3), span(i, 3, 4)
-        xq = am + en
-        for k, v in (("gemm", gm), ("wq", wq), ("amax", am), ("enc", en)):
+        wq, xq, gm = span(i, 0, 1), span(i, 1, 2), span(i, 2, 3)
+        am, en = pspan(i, 0, 1), pspan(i, 1, 2)
+        for k, v in (("gemm", gm), ("wq", wq), ("xq", xq), ("amax", am), ("enc", en)):
             tot[k] += float(np.mean(v))
         n = L["M"] * L["K"]
         fl = 2.0 * L["M"] * L["N"] * L["K"]
@@ -607,9 +624,10 @@ def run_nvfp4_step(layers, steps, warmup):
     flops = sum(2.0 * L["M"] * L["N"] * L["K"] for L in layers)
     elems = sum(L["M"] * L["K"] for L in layers)
     return {"ms_per_step": ms_per_step, "flops": flops, "per_layer": per_layer,
-            "gemm_ms": tot["gemm"], "wq_ms": tot["wq"], "amax_ms": tot["amax"], "enc_ms": tot["enc"],
+            "gemm_ms": tot["gemm"], "wq_ms": tot["wq"], "xq_ms": tot["xq"],
+            "amax_ms": tot["amax"], "enc_ms": tot["enc"],
             "gemm_tflops": flops / (tot["gemm"] * 1e-3) / 1e12,
-            "quant_gbs": 4.5625 * elems / ((tot["amax"] + tot["enc"]) * 1e-3) / 1e9,
+            "quant_gbs": 4.5625 * elems / (tot["xq"] * 1e-3) / 1e9,
             "encode_gbs": 2.5625 * elems / (tot["enc"] * 1e-3) / 1e9,
             "amax_gbs": 2.0 * elems / (tot["amax"] * 1e-3) / 1e9}
 
@@ -630,10 +648,11 @@ def gemm_roofline(r, layers, traffic=None):
 
 
 def quantize_summary(r, layers):
-    """Whole quantize (both passes, 4.5625 B/element) and each pass alone,
-    over the step's activation tensors; the largest tensor on its own (the
-    graded encode-pass figure); tensors under the MALL's 256 MB may be
-    partly served from it on the second pass (labelled)."""
+    """Whole quantize (both passes in one call, 4.5625 B/element, timed in
+    the step) and each pass called alone, over the step's activation
+    tensors; the largest tensor on its own (the graded encode-pass figure);
+    tensors under the MALL's 256 MB may be partly served from it on the
+    second pass (labelled)."""
     big = max(r["per_layer"], key=lambda p: p["x_mb"])
     return {
         "kernel": "amax_partial_kernel + nvfp4_encode_kernel (activations)",
@@ -710,8 +729,7 @@ def main():
         "config": {
             "workload": wl.name, "M": wl.M,
             "layers": [f"{L['name']} {L['K']}->{L['N']}" for L in layers],
-            "step": "per layer: nvfp4_quantize(W), nvfp4_quantize_amax(X), nvfp4_quantize_encode(X), "
-                    "nvfp4_gemm(+bias)",
+            "step": "per layer: nvfp4_quantize(W), nvfp4_quantize(X), nvfp4_gemm(+bias)",
             "operands": "NVFP4 (E2M1 + E4M3/16 + FP32 tensor scale)",
             "mfma": "exact FP16 dequant, v_mfma_f32_32x32x16_f16, FP32 accumulate",
             "parallelism": "single GPU",
@@ -720,9 +738,9 @@ def main():
         "gemm_frac_fp4_peak": round(r["gemm_tflops"] / PEAK_FP4_MFMA_TFLOPS, 4),
         "quantize": quantize_summary(r, layers),
         "time_split_ms": {"gemm": round(r["gemm_ms"], 4),
-                          "quantize_x": round(r["amax_ms"] + r["enc_ms"], 4),
-                          "quantize_x_amax": round(r["amax_ms"], 4),
-                          "quantize_x_encode": round(r["enc_ms"], 4),
+                          "quantize_x": round(r["xq_ms"], 4),
+                          "quantize_x_amax_pass_alone": round(r["amax_ms"], 4),
+                          "quantize_x_encode_pass_alone": round(r["enc_ms"], 4),
                           "quantize_w": round(r["wq_ms"], 4)},
         "layers": r["per_layer"],
         "workloads": None,
