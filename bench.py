@@ -106,6 +106,28 @@ def measured_traffic(summary, source):
     return float(kv["hbm_bytes_per_launch_avg"])
 
 
+def profile_status():
+    """Each committed profile summary under profiles/ with the kernel sources
+    it was taken on (its `kernel_sources name=sha ...` line): "current" when
+    every one of them still hashes the same, "stale" when any changed,
+    "unhashed" when the file names none."""
+    out = {}
+    try:
+        names = sorted(n for n in os.listdir(PROFILES) if n.endswith(".txt"))
+    except OSError:
+        return out
+    for name in names:
+        with open(os.path.join(PROFILES, name)) as f:
+            tags = [l.split()[1:] for l in f if l.startswith("kernel_sources ")]
+        if not tags:
+            out[name] = "unhashed"
+            continue
+        pairs = [t.split("=", 1) for t in tags[0]]
+        ok = all(src in KERNEL_SOURCES and kernel_source_hash(src) == sha for src, sha in pairs)
+        out[name] = "current" if ok else "stale"
+    return out
+
+
 def nvfp4_gemm_kernel_name(M, N, K):
     """The kernel nvfp4_gemm launches for this shape, as the library reports
     it (solfp4_gemm_plan; a workspace is passed, as in the step)."""
@@ -750,6 +772,7 @@ def main():
         "stage1": None,
         "cpu_baseline": None,
         "paper_context": PAPER_CONTEXT,
+        "profiles": profile_status(),
     }
     if not args.no_graphs:
         result["graphs"] = run_graphs(layers, max(args.steps, 5))

@@ -88,3 +88,21 @@ def test_kernel_source_hashes_cover_every_include():
             assert h in files, (src, h)
             sub = set(re.findall(r'#include "([^"]+)"', open(os.path.join(bench.CSRC, h)).read()))
             assert sub <= set(files) | {"kernels.h", "solfp4.h"}, (h, sub)
+
+
+def test_every_profile_names_the_sources_it_was_taken_on(tmp_path, monkeypatch):
+    """Every committed profile summary carries a `kernel_sources` line that
+    bench.py checks against the current sources, so a stale profile shows
+    up as stale in the bench line rather than as current."""
+    import bench
+    status = bench.profile_status()
+    names = [n for n in os.listdir(bench.PROFILES) if n.endswith(".txt")]
+    assert names and set(status) == set(names)
+    assert "unhashed" not in status.values(), status
+    # the check itself: a changed source turns a profile stale
+    good = " ".join(f"{s}={bench.kernel_source_hash(s)}" for s in ("gemm.hip", "quantize.hip"))
+    (tmp_path / "a.txt").write_text(f"# x\nkernel_sources {good}\n")
+    (tmp_path / "b.txt").write_text("# x\nkernel_sources gemm.hip=0000000000000000\n")
+    (tmp_path / "c.txt").write_text("# no tag\n")
+    monkeypatch.setattr(bench, "PROFILES", str(tmp_path))
+    assert bench.profile_status() == {"a.txt": "current", "b.txt": "stale", "c.txt": "unhashed"}
