@@ -217,14 +217,19 @@ def run_mxfp4(layers, steps, warmup, profiled, vendor=True):
     gemm_ms = xq_ms = 0.0
     per_layer = []
     for i, L in enumerate(layers):
-        xq = np.mean([ev[s][i][1].elapsed_time(ev[s][i][2]) for s in range(steps)])
-        gm = np.mean([ev[s][i][2].elapsed_time(ev[s][i][3]) for s in range(steps)])
+        xqs = np.array([ev[s][i][1].elapsed_time(ev[s][i][2]) for s in range(steps)])
+        gms = np.array([ev[s][i][2].elapsed_time(ev[s][i][3]) for s in range(steps)])
+        xq, gm = float(np.mean(xqs)), float(np.mean(gms))
         gemm_ms += gm
         xq_ms += xq
         fl = 2.0 * L["M"] * L["N"] * L["K"]
         per_layer.append({"layer": L["name"], "gemm_us": round(gm * 1e3, 2),
                           "gemm_tflops": round(fl / (gm * 1e-3) / 1e12, 1),
-                          "quantize_x_us": round(xq * 1e3, 2)})
+                          "gemm_us_p10_p50_p90": [round(float(np.percentile(gms, q)) * 1e3, 2)
+                                                  for q in (10, 50, 90)],
+                          "quantize_x_us": round(xq * 1e3, 2),
+                          "quantize_x_us_p10_p50_p90": [round(float(np.percentile(xqs, q)) * 1e3, 2)
+                                                        for q in (10, 50, 90)]})
     flops = sum(2.0 * L["M"] * L["N"] * L["K"] for L in layers)
     gemm_tflops = flops / (gemm_ms * 1e-3) / 1e12
     vendor = vendor_mxfp4(layers, bufs, steps) if vendor else None
