@@ -1,5 +1,5 @@
-"""GPU parity at sizes past 32-bit byte offsets: the NVFP4 quantize on a
-tensor of more than 2^31 BF16 elements (over 4 GiB), and both GEMMs with an
+"""GPU parity at sizes past 32-bit byte offsets: both quantizers on a tensor
+of more than 2^31 BF16 elements (over 4 GiB), and both GEMMs with an
 output of more than 4 GiB.  The whole tensors are far beyond what the CPU
 oracle can take, so the check runs on sampled rows: the first and last rows
 and the rows on both sides of every 4 GiB boundary of each buffer.  Codes,
@@ -43,7 +43,7 @@ def bits_rows(t, rows):
 
 
 def test_quantize_past_4gib():
-    rows, K = (1 << 20) + 5, 2064          # 2.16e9 elements, 4.3 GB of BF16, 129 blocks per row
+    rows, K = (1 << 20) + 5, 2080          # 2.18e9 elements, 4.4 GB of BF16, 130 blocks of 16 per row
     x = torch.randn((rows, K), dtype=torch.float32, device=device(), generator=seeded(11))
     x = x.to(torch.bfloat16)
     planted = rows - 3
@@ -63,7 +63,17 @@ def test_quantize_past_4gib():
     assert np.array_equal(u8_from_dev(scales[idx]), rs)
     assert np.array_equal(u8_from_dev(codes[idx]), rc)
     say(f"  {len(sample)} sampled rows bit-exact, alpha {a!r}")
-    del x, codes, scales
+    del codes, scales
+    # the MXFP4 quantize on the same tensor (its blocks are independent)
+    mcodes = poison_u8((rows, K // 2))
+    mscales = poison_u8((rows, K // 32))
+    sol.mxfp4_quantize(x, mcodes, mscales)
+    torch.cuda.synchronize()
+    mc, ms = O.mxfp4_quantize_ref(xb)
+    assert np.array_equal(u8_from_dev(mscales[idx]), ms)
+    assert np.array_equal(u8_from_dev(mcodes[idx]), mc)
+    say(f"  MXFP4: {len(sample)} sampled rows bit-exact")
+    del x, mcodes, mscales
     torch.cuda.empty_cache()
 
 
@@ -74,7 +84,7 @@ def test_gemm_output_past_4gib(fmt):
     g = seeded(12)
     ac = torch.randint(0, 256, (M, K // 2), dtype=torch.uint8, device=device(), generator=g)
     bc = torch.randint(0, 256, (N, K // 2), dtype=torch.uint8, device=device(), generator=g)
-    if fmt == "nvfp4":      # E4M3 scales 0.5 .. 0.9375
+    if fmt == "nvfp4":      # E4M3 scales 0.5 .. 1.75
         lo, hi = 0x30, 0x3F
     else:                   # E8M0 scales 2^-4 .. 2^3
         lo, hi = 123, 131
