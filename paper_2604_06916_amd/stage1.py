@@ -207,7 +207,7 @@ class Runner:
             end(ev)
             u = self._t("up", self.linear(h, L["up"], B["u"]))
             ev = self._op("gelu")
-            B["u"].copy_(F.gelu(u, approximate="tanh"))
+            torch.ops.aten.gelu_(u, approximate="tanh")     # in place: one kernel, no copy
             end(ev)
             self._t("g", B["u"])
             d = self._t("d", self.linear(B["u"], L["down"], B["d"]))
