@@ -616,7 +616,22 @@ def run_nvfp4_step(layers, steps, warmup):
             pev[r][i][1].record()
             sol.nvfp4_quantize_encode(L["x"], L["xc"], L["xs"], L["xa"], L["qws"])
             pev[r][i][2].record()
+    # a plain device-to-device copy of the largest activation on the same
+    # box (reads 2 B and writes 2 B per element), after a GEMM like the passes
+    big = max(range(len(layers)), key=lambda i: layers[i]["M"] * layers[i]["K"])
+    dst = torch.empty_like(layers[big]["x"])
+    cev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(reps)]
+    for r in range(reps):
+        P = layers[big - 1]
+        sol.nvfp4_gemm(P["xc"], P["xs"], P["xa"], P["wc"], P["ws"], P["wa"], P["b"], P["out"],
+                       P["gws"])
+        cev[r][0].record()
+        dst.copy_(layers[big]["x"])
+        cev[r][1].record()
     torch.cuda.synchronize()
+    copy_ms = float(np.mean([cev[r][0].elapsed_time(cev[r][1]) for r in range(reps)]))
+    copy_gbs = 4.0 * layers[big]["M"] * layers[big]["K"] / (copy_ms * 1e-3) / 1e9
+    del dst
 
     def span(i, a, b):
         return np.array([ev[s][i][a].elapsed_time(ev[s][i][b]) for s in range(steps)])
@@ -652,7 +667,7 @@ def run_nvfp4_step(layers, steps, warmup):
     elems = sum(L["M"] * L["K"] for L in layers)
     return {"ms_per_step": ms_per_step, "flops": flops, "per_layer": per_layer,
             "gemm_ms": tot["gemm"], "wq_ms": tot["wq"], "xq_ms": tot["xq"],
-            "amax_ms": tot["amax"], "enc_ms": tot["enc"],
+            "amax_ms": tot["amax"], "enc_ms": tot["enc"], "copy_gbs": copy_gbs,
             "gemm_tflops": flops / (tot["gemm"] * 1e-3) / 1e12,
             "quant_gbs": 4.5625 * elems / (tot["xq"] * 1e-3) / 1e9,
             "encode_gbs": 2.5625 * elems / (tot["enc"] * 1e-3) / 1e9,
@@ -679,7 +694,9 @@ def quantize_summary(r, layers):
     the step) and each pass called alone, over the step's activation
     tensors; the largest tensor on its own (the graded encode-pass figure);
     tensors under the MALL's 256 MB may be partly served from it on the
-    second pass (labelled)."""
+    second pass (labelled).  Beside the largest tensor: a plain
+    device-to-device copy of it on the same box (2 B read + 2 B written per
+    element), the memory system's own rate for a read-and-write stream."""
     big = max(r["per_layer"], key=lambda p: p["x_mb"])
     return {
         "kernel": "amax_partial_kernel + nvfp4_encode_kernel (activations)",
@@ -695,7 +712,9 @@ def quantize_summary(r, layers):
                           "encode_pass_gbs": big["encode_pass_gbs"],
                           "encode_pass_frac_hbm": round(big["encode_pass_gbs"] / PEAK_HBM_GBS, 4),
                           "whole_gbs": big["quantize_x_gbs"],
-                          "above_mall": big["x_mb"] > 256},
+                          "above_mall": big["x_mb"] > 256,
+                          "plain_copy_gbs": round(r["copy_gbs"], 1),
+                          "encode_pass_vs_plain_copy": round(big["encode_pass_gbs"] / r["copy_gbs"], 3)},
         "mall_resident_candidates": [p["layer"] for p in r["per_layer"] if p["x_mb"] <= 256],
     }
 
