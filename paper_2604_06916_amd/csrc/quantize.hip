@@ -4,8 +4,8 @@
 //
 // The tensor is a flat run of 16-element blocks (K % 16 == 0, row-major), so
 // both kernels treat it as one-dimensional:
-//   1. amax_partial_kernel  streams x once, one contiguous chunk per
-//      workgroup, and writes one partial |x| maximum (as a 15-bit BF16
+//   1. amax_partial_kernel  streams x once (nontemporal loads, grid-stride
+//      loop) and writes one partial |x| maximum (as a 15-bit BF16
 //      magnitude) per workgroup;
 //   2. nvfp4_encode_kernel  folds the partials into alpha, tabulates
 //      r(s) = 1 / (s * alpha) for the 126 nonzero finite E4M3 scales in LDS,
@@ -29,41 +29,43 @@ namespace solfp4 {
 
 constexpr int kQuantThreads = 256;
 
-// 16-byte streaming load (each input byte is read exactly once per pass).
-__device__ __forceinline__ u32x4_t stream_load(const uint4* p) {
-  return __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
-}
 constexpr int kEncodeUnroll = 8;   // pieces per lane per iteration (large tensors)
 constexpr int kEncodeUnrollSmall = 2;   // for small tensors: four times the workgroups
+constexpr int kAmaxUnroll = 8;     // amax pass, pieces per lane per iteration (large tensors)
+constexpr int kAmaxUnrollSmall = 2;
 
+// Whether the amax pass takes the large unroll: every one of its kMaxPartials
+// workgroups then runs at least one whole iteration.
+static bool amax_large(int64_t n_vec) {
+  return n_vec >= (int64_t)kMaxPartials * kQuantThreads * kAmaxUnroll;
+}
+
+__device__ __forceinline__ ushort2_t absmax_piece(ushort2_t m, u32x4_t v) {
+  m = absmax_pair(m, v.x);
+  m = absmax_pair(m, v.y);
+  m = absmax_pair(m, v.z);
+  return absmax_pair(m, v.w);
+}
+
+template <int kU>
 __global__ __launch_bounds__(kQuantThreads) void amax_partial_kernel(
-    const uint4* __restrict__ x, int64_t n_vec, uint32_t* __restrict__ partial) {
-  // each workgroup streams one contiguous chunk, 8 x 4 KiB per iteration
-  // (long sequential runs keep HBM pages open)
-  constexpr int kU = 8;
+    const u32x4_t* __restrict__ x, int64_t n_vec, uint32_t* __restrict__ partial) {
+  // grid-stride loop: an iteration covers kU * 256 consecutive 16-byte
+  // pieces of the workgroup, kU loads in flight per lane
   ushort2_t m = {0, 0};
-  const int64_t per = (n_vec + gridDim.x - 1) / gridDim.x;
-  const int64_t lo = (int64_t)blockIdx.x * per;
-  const int64_t hi = min(n_vec, lo + per);
-  int64_t i = lo + threadIdx.x;
-  for (; i + (kU - 1) * kQuantThreads < hi; i += kU * kQuantThreads) {
+  const int64_t per_iter = (int64_t)kU * kQuantThreads;
+  int64_t base = (int64_t)blockIdx.x * per_iter;
+  const int64_t stride = (int64_t)gridDim.x * per_iter;
+  for (; base + per_iter <= n_vec; base += stride) {
     u32x4_t v[kU];
 #pragma unroll
-    for (int u = 0; u < kU; ++u) v[u] = stream_load(&x[i + u * kQuantThreads]);
+    for (int u = 0; u < kU; ++u) v[u] = __builtin_nontemporal_load(&x[base + u * kQuantThreads + threadIdx.x]);
 #pragma unroll
-    for (int u = 0; u < kU; ++u) {
-      m = absmax_pair(m, v[u].x);
-      m = absmax_pair(m, v[u].y);
-      m = absmax_pair(m, v[u].z);
-      m = absmax_pair(m, v[u].w);
-    }
+    for (int u = 0; u < kU; ++u) m = absmax_piece(m, v[u]);
   }
-  for (; i < hi; i += kQuantThreads) {
-    const uint4 v = x[i];
-    m = absmax_pair(m, v.x);
-    m = absmax_pair(m, v.y);
-    m = absmax_pair(m, v.z);
-    m = absmax_pair(m, v.w);
+  // the one iteration that reaches past the end (at most one workgroup)
+  if (base < n_vec) {
+    for (int64_t i = base + threadIdx.x; i < n_vec; i += kQuantThreads) m = absmax_piece(m, x[i]);
   }
   uint32_t r = wave_max_u32(max((uint32_t)m.x, (uint32_t)m.y));
   __shared__ uint32_t red[kQuantThreads / kWave];
@@ -200,22 +202,23 @@ hipError_t scratch_address(uint32_t** out) {
 }
 
 int amax_partial_count(int64_t n_elems) {
-  // one workgroup per 64 Ki elements (down to 4 Ki for small tensors, so
-  // that they still spread over many CUs), rounded up to a whole number of
-  // workgroups per compute unit (256 of them) so that every CU streams the
-  // same amount, at most kMaxPartials
-  int64_t per_wg = n_elems / 256;
-  per_wg = per_wg < 4096 ? 4096 : per_wg > 65536 ? 65536 : per_wg;
-  int64_t p = (n_elems + per_wg - 1) / per_wg;
-  if (p > 256) p = (p + 255) / 256 * 256;
+  // the grid of the amax pass, one partial maximum per workgroup: all
+  // kMaxPartials once each runs a whole iteration of the large unroll;
+  // below that one workgroup per iteration of the small unroll (4 Ki
+  // elements), so that small tensors still spread over many CUs
+  const int64_t n_vec = n_elems / 8;
+  if (amax_large(n_vec)) return kMaxPartials;
+  int64_t p = (n_vec + kQuantThreads * kAmaxUnrollSmall - 1) / (kQuantThreads * kAmaxUnrollSmall);
   if (p < 1) p = 1;
   if (p > kMaxPartials) p = kMaxPartials;
   return (int)p;
 }
 
 hipError_t launch_amax(const uint16_t* x, int64_t n, uint32_t* partial, hipStream_t stream) {
-  return launch_kernel(amax_partial_kernel, dim3(amax_partial_count(n)), dim3(kQuantThreads), stream,
-                       reinterpret_cast<const uint4*>(x), n / 8, partial);
+  const int64_t n_vec = n / 8;
+  return launch_kernel(amax_large(n_vec) ? amax_partial_kernel<kAmaxUnroll> : amax_partial_kernel<kAmaxUnrollSmall>,
+                       dim3(amax_partial_count(n)), dim3(kQuantThreads), stream,
+                       reinterpret_cast<const u32x4_t*>(x), n_vec, partial);
 }
 
 hipError_t launch_encode(const uint16_t* x, int64_t rows, int64_t K, uint8_t* codes,
