@@ -528,6 +528,40 @@ def cpu_baseline(wl, rows, wrows):
     }
 
 
+def gpu_state():
+    """Socket power and clocks of GPU 0 as amd-smi reports them (a child
+    process, 30 s limit); None where amd-smi is missing or says nothing.
+    amd-smi samples are coarse: they do not show the clock of a kernel of a
+    few hundred microseconds (the counter profile records that)."""
+    import shutil
+    import subprocess
+    exe = shutil.which("amd-smi") or "/opt/rocm/bin/amd-smi"
+    try:
+        p = subprocess.run([exe, "metric", "-g", "0", "-p", "-c", "--json"], capture_output=True,
+                           text=True, timeout=30)
+        data = json.loads(p.stdout)
+    except (OSError, subprocess.SubprocessError, ValueError):
+        return None
+    gpus = data.get("gpu_data", data) if isinstance(data, dict) else data
+    if not isinstance(gpus, list) or not gpus or not isinstance(gpus[0], dict):
+        return None
+
+    def num(v):
+        v = v.get("value") if isinstance(v, dict) else v
+        return v if isinstance(v, (int, float)) else None
+
+    g = gpus[0]
+    power = num((g.get("power") or {}).get("socket_power"))
+    clocks = g.get("clock") or {}
+    gfx = [num((c or {}).get("clk")) for k, c in clocks.items() if k.startswith("gfx_")]
+    gfx = [v for v in gfx if v is not None]
+    mem = [num((c or {}).get("clk")) for k, c in clocks.items() if k.startswith("mem_")]
+    mem = [v for v in mem if v is not None]
+    return {"socket_power_w": power,
+            "gfx_clk_mhz": [min(gfx), round(sum(gfx) / len(gfx)), max(gfx)] if gfx else None,
+            "mem_clk_mhz": mem[0] if mem else None}
+
+
 def make_layers(wl, dev):
     """Device buffers of every layer of a workload: seeded BF16 X, W and bias,
     and the outputs and workspaces the step writes."""
@@ -755,7 +789,9 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     layers = make_layers(wl, dev)
+    state_before = gpu_state()
     r = run_nvfp4_step(layers, args.steps, args.warmup)
+    state_after = gpu_state()
     value = r["flops"] / (r["ms_per_step"] * 1e-3) / 1e12
     traffic = (measured_traffic("nvfp4_gemm_flux-12b_traffic.txt", "gemm.hip")
                if wl.name == PROFILED_WORKLOAD else None)
@@ -797,6 +833,9 @@ def main():
         "cpu_baseline": None,
         "paper_context": PAPER_CONTEXT,
         "profiles": profile_status(),
+        "gpu_state": {"source": "amd-smi metric -p -c, before and after the NVFP4 step timing "
+                                "(gfx_clk_mhz: min, mean, max over the XCDs)",
+                      "before": state_before, "after": state_after},
     }
     if not args.no_graphs:
         result["graphs"] = run_graphs(layers, max(args.steps, 5))

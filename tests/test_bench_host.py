@@ -106,3 +106,31 @@ def test_every_profile_names_the_sources_it_was_taken_on(tmp_path, monkeypatch):
     (tmp_path / "c.txt").write_text("# no tag\n")
     monkeypatch.setattr(bench, "PROFILES", str(tmp_path))
     assert bench.profile_status() == {"a.txt": "current", "b.txt": "stale", "c.txt": "unhashed"}
+
+
+def test_gpu_state_reads_power_and_clocks(monkeypatch):
+    # an amd-smi reply of the shape `amd-smi metric -p -c --json` prints
+    # (values made up), and replies it cannot use
+    sys.path.insert(0, ROOT)
+    import json
+    import types
+
+    import bench
+    reply = {"gpu_data": [{"gpu": 0,
+                           "power": {"socket_power": {"value": 700, "unit": "W"}, "gfx_voltage": "N/A"},
+                           "clock": {"gfx_0": {"clk": {"value": 2100, "unit": "MHz"}},
+                                     "gfx_1": {"clk": {"value": 2300, "unit": "MHz"}},
+                                     "gfx_2": {"clk": "N/A"},
+                                     "mem_0": {"clk": {"value": 2000, "unit": "MHz"}}}}]}
+    monkeypatch.setattr(subprocess, "run",
+                        lambda *a, **k: types.SimpleNamespace(stdout=json.dumps(reply), returncode=0))
+    assert bench.gpu_state() == {"socket_power_w": 700, "gfx_clk_mhz": [2100, 2200, 2300],
+                                 "mem_clk_mhz": 2000}
+    monkeypatch.setattr(subprocess, "run",
+                        lambda *a, **k: types.SimpleNamespace(stdout="not json", returncode=1))
+    assert bench.gpu_state() is None
+
+    def missing(*a, **k):
+        raise FileNotFoundError("amd-smi")
+    monkeypatch.setattr(subprocess, "run", missing)
+    assert bench.gpu_state() is None
