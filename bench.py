@@ -305,7 +305,8 @@ def run_graphs(layers, reps):
 
 def run_small_linear(reps):
     """The 128-token 1152 -> 1152 layer, launch-bound: nvfp4_linear per call,
-    eager launches against one graph holding `batch` linears."""
+    eager launches against one graph holding `batch` linears; the GEMM alone;
+    the MXFP4 linear and GEMM graph-replayed the same way."""
     import numpy as np
     import torch
 
@@ -367,6 +368,26 @@ def run_small_linear(reps):
     e1.record()
     torch.cuda.synchronize()
     gemm_us = e0.elapsed_time(e1) / (reps * batch) * 1e3
+    # the MXFP4 linear (quantize + GEMM) and its GEMM alone, graph-batched alike
+    mwc, mws = sol.mxfp4_quantize(w)
+    mlws = torch.empty(sol.mxfp4_linear_workspace_bytes(M, K), dtype=torch.uint8, device=dev)
+    mxc, mxs = sol.mxfp4_quantize(x)
+
+    def graph_time(fn):
+        gr = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(gr):
+            for _ in range(batch):
+                fn()
+        gr.replay()
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(reps):
+            gr.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / (reps * batch) * 1e3
+    mx_lin_us = graph_time(lambda: sol.mxfp4_linear(x, mwc, mws, b, out, mlws))
+    mx_gemm_us = graph_time(lambda: sol.mxfp4_gemm(mxc, mxs, mwc, mws, b, out))
     fl = 2.0 * M * N * K
     route = ("amax pass + GEMM quantizing the activations in the kernel" if K <= 512
              else "amax pass + encode pass + GEMM")
@@ -374,6 +395,8 @@ def run_small_linear(reps):
             "graph_us": round(graph_us, 2), "gemm_graph_us": round(gemm_us, 2),
             "gemm_kernel": nvfp4_gemm_kernel_name(M, N, K), "linear_launches": route,
             "graph_tflops": round(fl / (graph_us * 1e-6) / 1e12, 2),
+            "mxfp4": {"linear_graph_us": round(mx_lin_us, 2), "gemm_graph_us": round(mx_gemm_us, 2),
+                      "linear_launches": "mxfp4_quantize + mxfp4_gemm"},
             "roofline": {"bound": "latency", "achieved": round(fl / (graph_us * 1e-6) / 1e12, 2),
                          "peak": PEAK_FP16_MFMA_TFLOPS, "unit": "TFLOP/s",
                          "frac": round(fl / (graph_us * 1e-6) / 1e12 / PEAK_FP16_MFMA_TFLOPS, 5),
