@@ -249,7 +249,8 @@ SOLFP4_API int nvfp4_linear(const uint16_t* x, const uint8_t* w_codes, const uin
 #define SOLFP4_FORMAT_MXFP4 1
 #define SOLFP4_KERNEL_NVFP4_LANE 1     /* codes to LDS by DMA, per-wave dequantization */
 #define SOLFP4_KERNEL_NVFP4_SHARED 2   /* workgroup-shared dequantization into LDS */
-#define SOLFP4_KERNEL_MXFP4 3          /* scaled FP4 matrix instructions */
+#define SOLFP4_KERNEL_MXFP4 3          /* scaled FP4 matrix instructions (256 x 256,
+                                          128 x 128 or, for few tokens, 64 x 64 tiles) */
 #define SOLFP4_KERNEL_NVFP4_SMALL 4    /* 64 x 64 tiles for few tokens (K % 128 == 0); in
                                           nvfp4_linear with K <= 512 it also quantizes the
                                           activations itself */

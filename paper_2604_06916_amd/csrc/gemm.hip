@@ -925,7 +925,7 @@ __global__ __launch_bounds__(kLThreads, 1) void nvfp4_gemm_lane_kernel(
 
 // Compute units of the current device (256 on MI355X), queried once per
 // device.
-static int device_cus() {
+int device_cu_count() {
   constexpr int kMaxDevices = 64;
   static int cached[kMaxDevices];
   int dev = 0;
@@ -947,7 +947,7 @@ bool small_tiles_pay(int64_t tiles256, int64_t tiles128) {
 #ifndef SOLFP4_SMALL_TILE_COST
 #define SOLFP4_SMALL_TILE_COST 0.46
 #endif
-  const int64_t cus = device_cus();
+  const int64_t cus = device_cu_count();
   const double big = (double)((tiles256 + cus - 1) / cus);
   const double small = (double)((tiles128 + cus - 1) / cus) * SOLFP4_SMALL_TILE_COST;
   return small < big;
@@ -958,7 +958,7 @@ SplitPlan plan_split(int64_t tiles, int64_t nstages, double fixed_cost, double p
   SplitPlan plan;
   plan.dp_tiles = tiles;
   plan.stages = nstages;
-  const int64_t cus = device_cus();
+  const int64_t cus = device_cu_count();
   const int64_t rem = tiles % cus;
   if (rem == 0 || nstages < 2) return plan;
   // two K halves per remainder tile (the kernels add exactly two), when
@@ -1066,7 +1066,7 @@ void describe_gemm(int64_t M, int64_t N, int64_t K, bool with_workspace, int* ke
 bool use_small_gemm(int64_t M, int64_t N, int64_t K) {
   if (K % kLBK != 0 || M <= 0 || N <= 0 || K <= 0) return false;
   const int64_t t64 = ((M + 63) / 64) * ((N + 63) / 64);
-  return t64 <= device_cus();
+  return t64 <= device_cu_count();
 }
 
 hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_gs,

@@ -49,9 +49,15 @@ hipError_t launch_quantize(const uint16_t* x, int64_t rows, int64_t K, uint8_t* 
                            uint8_t* scales, float* global_scale, uint32_t* partial,
                            hipStream_t stream);
 
+// Compute units of the current device, queried once per device (host only).
+int device_cu_count();
+
 // Whether a GEMM should run on 128 x 128 output tiles rather than 256 x 256
 // ones, given the tile counts of both (host only).
 bool small_tiles_pay(int64_t tiles256, int64_t tiles128);
+
+// Output tile edge (256, 128 or 64) of an MXFP4 GEMM (host only).
+int mx_tile_edge(int64_t M, int64_t N);
 
 // Split-K for the last, partial round of 256 x 256 tiles.  A GEMM with T
 // tiles on C compute units runs about ceil(T / C) rounds of one tile's time;

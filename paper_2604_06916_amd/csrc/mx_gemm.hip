@@ -13,7 +13,10 @@
 // Tiling: a 256 x 256 output tile per workgroup of 4 waves (one per SIMD),
 // each wave owning 128 x 128 (4 x 4 MFMA tiles of 32 x 32, 256 FP32
 // accumulators per lane in AGPRs); or, for GEMMs with too few such tiles to
-// fill the chip, 128 x 128 tiles with 64 x 64 per wave.  K advances 128
+// fill the chip, 128 x 128 tiles with 64 x 64 per wave, and for few tokens
+// 64 x 64 tiles with one 32 x 32 MFMA tile per wave (mx_tile_edge chooses;
+// every size runs the same sequence of MFMAs per output element, so the
+// results are bit-identical across sizes).  K advances 128
 // elements (64 code bytes per row) per stage.  Codes go from global memory straight into LDS by
 // buffer loads with the LDS-destination bit (no register staging), into four
 // stage buffers: the loads for stage s+3 are issued while stage s computes,
@@ -113,7 +116,7 @@ __global__ __launch_bounds__(kMxThreads, 1) void mxfp4_gemm_kernel(
     const uint8_t* __restrict__ b_codes, const uint8_t* __restrict__ b_scales,
     const uint16_t* __restrict__ bias, uint16_t* __restrict__ out, int64_t M, int64_t N,
     int64_t K) {
-  static_assert(kWT == 128 || kWT == 64, "wave tile edge");
+  static_assert(kWT == 128 || kWT == 64 || kWT == 32, "wave tile edge");
   constexpr int kT = 2 * kWT;                // output tile edge (M and N)
   constexpr int kFr = kWT / 32;              // 32 x 32 MFMA tiles per wave edge
   constexpr int kStage = kT * kMxRowBytes;   // one operand, one stage
@@ -211,10 +214,19 @@ __global__ __launch_bounds__(kMxThreads, 1) void mxfp4_gemm_kernel(
           rcb, (lds_ptr_t)(bbuf[buf] + (kGw * wave + j) * 1024), 16, off, 0, 0, 1);
     }
   };
-  // half h of the DMA of `stage` (kGw / 2 groups, kDma / 2 instructions)
+  // half h of the DMA of `stage` (kGw / 2 groups, kDma / 2 instructions; with
+  // one group per wave, the A group in half 0 and the B group in half 1)
   auto dma_half = [&](int buf, int stage, int h) {
     const bool ok = kFast || (int64_t)stage * kMxBK + 32 * piece < K;
     const uint32_t base = dma_off + (uint32_t)stage * kMxRowBytes;
+    if constexpr (kGw == 1) {
+      const uint32_t off = ok ? base : kDrop;
+      if (h == 0)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rca, (lds_ptr_t)(abuf[buf] + wave * 1024), 16, off, 0, 0, 1);
+      else
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rcb, (lds_ptr_t)(bbuf[buf] + wave * 1024), 16, off, 0, 0, 1);
+      return;
+    }
 #pragma unroll
     for (int jj = 0; jj < kGw / 2; ++jj) {
       const int j = h * (kGw / 2) + jj;
@@ -432,31 +444,51 @@ __global__ __launch_bounds__(kMxThreads, 1) void mxfp4_gemm_kernel(
   }
 }
 
-void describe_mx_gemm(int64_t M, int64_t N, int64_t K, int* kernel, int* tile, int64_t* workgroups) {
+// The output tile edge: one workgroup holds one tile at a time on its CU, so
+// a launch takes about ceil(tiles / CUs) rounds of one tile's time.  Between
+// 256 x 256 and 128 x 128 tiles small_tiles_pay decides; a 64 x 64 tile costs
+// SOLFP4_MX_TINY_TILE_COST of a 128 x 128 one (measured on 64 to 512 tokens:
+// 64 x 64 tiles 1.13-1.61x faster where they take at most two rounds and
+// 128 x 128 tiles one, 0.80x at three rounds against one).  Where 256 x 256
+// tiles win, 64 x 64 ones cannot: that takes three or more rounds of
+// 128 x 128 tiles, and 64 x 64 tiles then need about four times as many.
+int mx_tile_edge(int64_t M, int64_t N) {
+#ifndef SOLFP4_MX_TINY_TILE_COST
+#define SOLFP4_MX_TINY_TILE_COST 0.46
+#endif
   const int64_t t256 = ((M + 255) / 256) * ((N + 255) / 256);
   const int64_t t128 = ((M + 127) / 128) * ((N + 127) / 128);
-  const bool small = small_tiles_pay(t256, t128);
+  if (!small_tiles_pay(t256, t128)) return 256;
+  const int64_t t64 = ((M + 63) / 64) * ((N + 63) / 64);
+  const int64_t cus = device_cu_count();
+  const double r128 = (double)((t128 + cus - 1) / cus);
+  const double r64 = (double)((t64 + cus - 1) / cus);
+  return r64 * SOLFP4_MX_TINY_TILE_COST < r128 ? 64 : 128;
+}
+
+void describe_mx_gemm(int64_t M, int64_t N, int64_t K, int* kernel, int* tile, int64_t* workgroups) {
+  const int edge = mx_tile_edge(M, N);
   (void)K;
   *kernel = SOLFP4_KERNEL_MXFP4;
-  *tile = small ? 128 : 256;
-  *workgroups = small ? t128 : t256;
+  *tile = edge;
+  *workgroups = ((M + edge - 1) / edge) * ((N + edge - 1) / edge);
 }
 
 hipError_t launch_mx_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const uint8_t* b_codes,
                           const uint8_t* b_scales, const uint16_t* bias, uint16_t* out, int64_t M,
                           int64_t N, int64_t K, hipStream_t stream) {
   if (M == 0 || N == 0) return hipSuccess;
-  const int64_t t256 = ((M + 255) / 256) * ((N + 255) / 256);
-  const int64_t t128 = ((M + 127) / 128) * ((N + 127) / 128);
-  const bool small = small_tiles_pay(t256, t128);
-  const dim3 grid((unsigned)(small ? t128 : t256)), block(kMxThreads);
+  const int edge = mx_tile_edge(M, N);
+  const dim3 grid((unsigned)(((M + edge - 1) / edge) * ((N + edge - 1) / edge))), block(kMxThreads);
   const bool fast = K % kMxBK == 0;
   const bool vec = N % 8 == 0;
-#define SOLFP4_MX_LAUNCH(F, V)                                                                 \
-  (small ? launch_kernel(mxfp4_gemm_kernel<F, V, 64>, grid, block, stream, a_codes, a_scales,  \
-                         b_codes, b_scales, bias, out, M, N, K)                                \
-         : launch_kernel(mxfp4_gemm_kernel<F, V, 128>, grid, block, stream, a_codes, a_scales, \
-                         b_codes, b_scales, bias, out, M, N, K))
+#define SOLFP4_MX_LAUNCH(F, V)                                                                   \
+  (edge == 64 ? launch_kernel(mxfp4_gemm_kernel<F, V, 32>, grid, block, stream, a_codes, a_scales, \
+                              b_codes, b_scales, bias, out, M, N, K)                             \
+   : edge == 128 ? launch_kernel(mxfp4_gemm_kernel<F, V, 64>, grid, block, stream, a_codes,      \
+                                 a_scales, b_codes, b_scales, bias, out, M, N, K)                \
+                 : launch_kernel(mxfp4_gemm_kernel<F, V, 128>, grid, block, stream, a_codes,     \
+                                 a_scales, b_codes, b_scales, bias, out, M, N, K))
   hipError_t e;
   if (fast) e = vec ? SOLFP4_MX_LAUNCH(true, true) : SOLFP4_MX_LAUNCH(true, false);
   else e = vec ? SOLFP4_MX_LAUNCH(false, true) : SOLFP4_MX_LAUNCH(false, false);

@@ -120,7 +120,17 @@ def test_gemm_plan_names_the_kernels():
                                             "workgroups": 36, "splits": 1}
     assert B.gemm_plan(128, 1152, 1120)["tile"] == 128      # K % 128 != 0
     assert B.gemm_plan(4096, 4096, 320)["kernel"] == "nvfp4_gemm_kernel"
-    assert B.gemm_plan(18432, 9216, 3072, B.FORMAT_MXFP4)["kernel"] == "mxfp4_gemm_kernel"
+    assert B.gemm_plan(18432, 9216, 3072, B.FORMAT_MXFP4) == {"kernel": "mxfp4_gemm_kernel",
+                                                              "tile": 256, "workgroups": 2592,
+                                                              "splits": 1}
+    # MXFP4 tiles by token count (on a host without a device the library
+    # plans for 256 CUs): 64 x 64 while they take at most two rounds and
+    # 128 x 128 tiles one, 128 x 128 beyond
+    mx = lambda M, N, K: B.gemm_plan(M, N, K, B.FORMAT_MXFP4)
+    assert (mx(128, 1152, 1152)["tile"], mx(128, 1152, 1152)["workgroups"]) == (64, 36)
+    assert mx(384, 3072, 3072)["tile"] == 64 and mx(512, 2240, 2240)["workgroups"] == 280
+    assert mx(1024, 3072, 3072)["tile"] == 128 and mx(1000, 3000, 256)["tile"] == 128
+    assert mx(2100, 9000, 3072)["tile"] == 256
     assert B.gemm_plan(0, 16, 16)["kernel"] is None
     with pytest.raises(B.Solfp4Error):
         B.gemm_plan(16, 16, 24)

@@ -155,16 +155,18 @@ def test_golden_gemm():
         assert int(got[0, 0]) == c["bf16"], name
 
 
-# The small shapes run on 128 x 128 tiles, (4200, 4360, K) and (6000, 6152,
-# 1024) on 256 x 256 ones (ragged M and N).  Scale groups (16 bytes of a row)
-# are one 16-byte load; with K % 128 != 0 (K = 96, 2240) rows start at any
-# byte offset and the lane of an operand's last row whose group reaches past
-# the range loads bytes instead, on both tile sizes.  K = 1152 (K % 512 !=
+# The small shapes run on 64 x 64 tiles, (1000, 3000, K) and (1024, 3072, K)
+# on 128 x 128 ones, (4200, 4360, K) and (6000, 6152, 1024) on 256 x 256 ones
+# (ragged M and N).  Scale groups (16 bytes of a row) are one 16-byte load;
+# with K % 128 != 0 (K = 96, 2240) rows start at any byte offset and the lane
+# of an operand's last row whose group reaches past the range loads bytes
+# instead, on every tile size.  K = 1152 (K % 512 !=
 # 0) once fetched groups as four 4-byte loads that the compiler merged (a
 # stage-end wait that counted them as four let the previous stage's loads
 # still be in flight).
 @pytest.mark.parametrize("M,N,K", [(1, 1, 32), (3, 5, 64), (37, 70, 128), (300, 260, 96),
                                    (257, 513, 32), (64, 96, 512), (260, 300, 1152),
+                                   (1000, 3000, 128), (1024, 3072, 96),
                                    (4200, 4360, 1024), (6000, 6152, 1024), (4200, 4360, 1152),
                                    (300, 260, 2240), (4200, 4360, 2240), (4201, 4359, 96)])
 def test_exact_sums_are_bit_exact(M, N, K):
@@ -207,7 +209,9 @@ def test_every_scale_code_bit_exact(side):
 SHAPES = [(1, 1, 32), (5, 7, 64), (64, 64, 128), (255, 257, 96), (300, 520, 288),
           (257, 129, 2240), (128, 1152, 1152), (513, 260, 5600), (96, 300, 3072),
           (260, 2049, 256), (600, 700, 2432),
-          # persistent kernel (more tiles than compute units, K % 512 == 0)
+          # 128 x 128 tiles (the shapes above take 64 x 64 ones)
+          (1000, 3000, 256), (1024, 3072, 160),
+          # 256 x 256 tiles, more tiles than compute units
           (4200, 4360, 1024), (2100, 9000, 3072)]
 
 
