@@ -210,3 +210,39 @@ def test_two_pass_calls_equal_quantize(rows, K):
     assert torch.equal(gs.view(torch.int32), want[2].view(torch.int32))
     rc, rs, ra = O.nvfp4_quantize_ref(xb)
     assert np.array_equal(codes.cpu().numpy(), rc) and np.array_equal(scales.cpu().numpy(), rs)
+
+
+# The amax pass is a grid-stride loop of whole iterations (256 threads times
+# 8 or 2 pieces of 8 elements); the one iteration that reaches past the end
+# is read element by element.  Shapes: the 2-piece unroll on 1024 workgroups
+# with three rounds, the last one partial (3001 x 4096); the 8-piece unroll
+# with a partial last iteration (4100 x 4112); a single row (2 x 16496).  The
+# tensor's largest magnitude is planted at the first element, the last one
+# and the middle of the partial iteration in turn, so alpha is right only if
+# every piece is read.
+@pytest.mark.parametrize("rows,K", [(3001, 4096), (4100, 4112), (2, 16 * 1031)])
+def test_amax_pass_reads_every_piece(rows, K):
+    xb = draw_activations("normal", rows, K, seed=rows + K)
+    n = rows * K
+    per_iter = 8 * 256 * (8 if n // 8 >= 1024 * 2048 else 2)   # elements per iteration
+    tail = n // per_iter * per_iter
+    places = [0, n - 1, (tail + n) // 2 if tail < n else n // 2]
+    x = bf16_to_dev(xb)
+    for p in places:
+        r, j = divmod(p, K)
+        saved = x[r, j].clone()
+        x[r, j] = -300.0                       # the largest magnitude; its sign must not matter
+        codes = poison_u8((rows, K // 2))
+        scales = poison_u8((rows, K // 16))
+        gs = torch.full((1,), float("nan"), dtype=torch.float32, device=device())
+        sol.nvfp4_quantize(x, codes, scales, gs)
+        torch.cuda.synchronize()
+        sample = sorted({0, r, rows - 1})
+        xs = x[torch.tensor(sample, device=device())].view(torch.int16).cpu().numpy().view(np.uint16)
+        rc, rs, ra = O.nvfp4_quantize_ref(xs)   # the planted row carries the global amax
+        a = np.float32(gs.cpu().numpy()[0])
+        assert f32_bits(a) == f32_bits(ra), (rows, K, p, a, ra)
+        idx = torch.tensor(sample, device=device())
+        assert np.array_equal(u8_from_dev(scales[idx]), rs), (rows, K, p)
+        assert np.array_equal(u8_from_dev(codes[idx]), rc), (rows, K, p)
+        x[r, j] = saved
