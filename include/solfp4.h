@@ -173,7 +173,11 @@ SOLFP4_API int nvfp4_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const
  * computed as two K halves by two workgroups, which add their FP32 partial
  * sums through this workspace (one partial tile per half: 256 KB, or 64 KB
  * for 128 x 128 tiles; plus an 8-byte slot per tile that tells the second
- * half to finish that it is second).  0 means the shape runs without it.
+ * half to finish that it is second).  0 means the shape runs without it,
+ * which includes few-token shapes (K % 128 == 0 with at most one 64 x 64
+ * tile per compute unit): they run on 64 x 64 tiles, or on 32 x 32 tiles
+ * whose K stages the four waves of a workgroup share (their partial sums
+ * added in LDS in wave order), whichever is estimated faster.
  *
  * nvfp4_gemm's workspace argument:
  *   NULL       no split (workspace_bytes is ignored)
@@ -237,9 +241,11 @@ SOLFP4_API int nvfp4_linear(const uint16_t* x, const uint8_t* w_codes, const uin
  *   with_workspace  nonzero: nvfp4_gemm gets a workspace of at least
  *                   nvfp4_gemm_workspace_bytes(M, N, K) (ignored for MXFP4)
  *   kernel          written: one of the SOLFP4_KERNEL_* ids below
- *   tile            written: output tile edge, 256, 128 or 64
+ *   tile            written: output tile edge, 256, 128, 64 or 32
  *   workgroups      written: workgroups of the launch
- *   splits          written: K ranges per tile of the last round (1: none)
+ *   splits          written: K ranges per tile of the last round, each on
+ *                   a workgroup of its own (1: none; the wave-K kernel's
+ *                   four K shares inside one workgroup are not counted)
  *
  * Returns SOLFP4_OK, SOLFP4_EINVAL for a null output pointer, a negative
  * size or an unknown format, or SOLFP4_ESHAPE for a shape the GEMM rejects.
@@ -254,6 +260,8 @@ SOLFP4_API int nvfp4_linear(const uint16_t* x, const uint8_t* w_codes, const uin
 #define SOLFP4_KERNEL_NVFP4_SMALL 4    /* 64 x 64 tiles for few tokens (K % 128 == 0); in
                                           nvfp4_linear with K <= 512 it also quantizes the
                                           activations itself */
+#define SOLFP4_KERNEL_NVFP4_WAVEK 5    /* 32 x 32 tiles for few tokens, each workgroup's
+                                          K stages dealt to its four waves (K % 128 == 0) */
 SOLFP4_API int solfp4_gemm_plan(int format, int64_t M, int64_t N, int64_t K, int with_workspace,
                      int* kernel, int* tile, int64_t* workgroups, int* splits);
 

@@ -15,7 +15,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 OBJ = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libsolfp4.so")
-SOURCES = ["api.hip", "quantize.hip", "gemm.hip", "gemm_small.hip", "mx_quantize.hip", "mx_gemm.hip"]
+SOURCES = ["api.hip", "quantize.hip", "gemm.hip", "gemm_small.hip", "gemm_wavek.hip", "mx_quantize.hip",
+           "mx_gemm.hip"]
 HEADERS = ["device_common.h", "kernels.h", "nvfp4_gemm_common.h"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

@@ -1038,6 +1038,13 @@ size_t gemm_workspace_bytes(int64_t M, int64_t N, int64_t K) {
 
 void describe_gemm(int64_t M, int64_t N, int64_t K, bool with_workspace, int* kernel, int* tile,
                    int64_t* workgroups, int* splits) {
+  if (use_wavek_gemm(M, N, K)) {
+    *kernel = SOLFP4_KERNEL_NVFP4_WAVEK;
+    *tile = 32;
+    *splits = 1;
+    *workgroups = ((M + 31) / 32) * ((N + 31) / 32);
+    return;
+  }
   if (use_small_gemm(M, N, K)) {
     *kernel = SOLFP4_KERNEL_NVFP4_SMALL;
     *tile = 64;
@@ -1069,11 +1076,36 @@ bool use_small_gemm(int64_t M, int64_t N, int64_t K) {
   return t64 <= device_cu_count();
 }
 
+// Among the shapes the small-tile kernel takes, the wave-K kernel (32 x 32
+// tiles, each workgroup's K stages dealt to its four waves) where its
+// estimated time is lower: a launch takes ceil(tiles / CUs) rounds, and a
+// round costs a fixed part plus one per stage a wave runs.  The costs, in
+// microseconds, are fitted to measurements on one box (graph-free, 50
+// launches): the 64 x 64 kernel 3.35 + 0.40 per stage, the wave-K kernel
+// 2.83 + 0.52 per stage of its longest wave (128 x 1152 x 1152: 6.98 ->
+// 4.40 us, 128 x 1152 x 4608: 17.85 -> 7.53, 128 x 3072 x 12288: 42.7 ->
+// 28.6; kept on 64 x 64 tiles: 300 x 1000 x 512, 5.6 on wave-K against 4.9,
+// 256 x 3072 x 3072, 16.8 against 14.4, 128 x 12288 x 3072, 31.3 against
+// 21.7).
+bool use_wavek_gemm(int64_t M, int64_t N, int64_t K) {
+  if (!use_small_gemm(M, N, K)) return false;
+  const int64_t cus = device_cu_count();
+  const int64_t t64 = ((M + 63) / 64) * ((N + 63) / 64);
+  const int64_t t32 = ((M + 31) / 32) * ((N + 31) / 32);
+  const int64_t stages = K / kLBK;
+  const double small = (double)((t64 + cus - 1) / cus) * (3.35 + 0.40 * (double)stages);
+  const double wavek = (double)((t32 + cus - 1) / cus) * (2.83 + 0.52 * (double)((stages + 3) / 4));
+  return wavek < small;
+}
+
 hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_gs,
                        const uint8_t* b_codes, const uint8_t* b_scales, const float* b_gs,
                        const uint16_t* bias, uint16_t* out, int64_t M, int64_t N, int64_t K,
                        void* workspace, size_t workspace_bytes, hipStream_t stream) {
   if (M == 0 || N == 0) return hipSuccess;
+  if (use_wavek_gemm(M, N, K))
+    return launch_gemm_wavek(a_codes, a_scales, a_gs, b_codes, b_scales, b_gs, bias, out, M, N, K,
+                             stream);
   if (use_small_gemm(M, N, K))
     return launch_gemm_small(a_codes, a_scales, a_gs, b_codes, b_scales, b_gs, bias, out, M, N, K,
                              nullptr, stream);

@@ -125,6 +125,14 @@ struct SmallFuse {
 // Whether a GEMM of this shape runs on the small-tile kernel (host only):
 // K % 128 == 0 and its 64 x 64 tiles fit in one round on the device.
 bool use_small_gemm(int64_t M, int64_t N, int64_t K);
+// Whether a GEMM the small-tile kernel would take runs faster on the wave-K
+// kernel (32 x 32 tiles, K dealt to the four waves of a workgroup; host
+// only).
+bool use_wavek_gemm(int64_t M, int64_t N, int64_t K);
+hipError_t launch_gemm_wavek(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_gs,
+                             const uint8_t* b_codes, const uint8_t* b_scales, const float* b_gs,
+                             const uint16_t* bias, uint16_t* out, int64_t M, int64_t N, int64_t K,
+                             hipStream_t stream);
 // nvfp4_linear quantizes the activations inside the small-tile kernel up to
 // this K; beyond it the amax and encode passes followed by the small-tile
 // GEMM are faster (the in-kernel quantization costs as much VALU time as the

@@ -72,7 +72,8 @@ def test_roofline_kernel_name_follows_the_dispatch():
     assert bench.nvfp4_gemm_kernel_name(8192, 2240, 2240) == lane     # split last round
     assert bench.nvfp4_gemm_kernel_name(300, 260, 2240) == lane       # 128 x 128 tiles
     assert bench.nvfp4_gemm_kernel_name(300, 260, 48) == shared       # K % 32 == 16
-    assert bench.nvfp4_gemm_kernel_name(128, 1152, 1152) == "nvfp4_gemm_small_kernel"
+    assert bench.nvfp4_gemm_kernel_name(128, 1152, 1152) == "nvfp4_gemm_wavek_kernel"
+    assert bench.nvfp4_gemm_kernel_name(256, 3072, 1152) == "nvfp4_gemm_small_kernel"
 
 
 def test_kernel_source_hashes_cover_every_include():

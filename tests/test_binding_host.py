@@ -116,8 +116,12 @@ def test_gemm_plan_names_the_kernels():
     assert p == {"kernel": "nvfp4_gemm_lane_kernel", "tile": 256, "workgroups": 2592 - 32 + 64,
                  "splits": 2}
     assert B.gemm_plan(18432, 9216, 3072, with_workspace=False)["splits"] == 1
-    assert B.gemm_plan(128, 1152, 1152) == {"kernel": "nvfp4_gemm_small_kernel", "tile": 64,
-                                            "workgroups": 36, "splits": 1}
+    assert B.gemm_plan(128, 1152, 1152) == {"kernel": "nvfp4_gemm_wavek_kernel", "tile": 32,
+                                            "workgroups": 144, "splits": 1}
+    assert B.gemm_plan(256, 3072, 1152) == {"kernel": "nvfp4_gemm_small_kernel", "tile": 64,
+                                            "workgroups": 192, "splits": 1}
+    assert B.gemm_plan(300, 1000, 512)["kernel"] == "nvfp4_gemm_small_kernel"
+    assert B.gemm_plan(128, 12288, 3072)["kernel"] == "nvfp4_gemm_lane_kernel"
     assert B.gemm_plan(128, 1152, 1120)["tile"] == 128      # K % 128 != 0
     assert B.gemm_plan(4096, 4096, 320)["kernel"] == "nvfp4_gemm_kernel"
     assert B.gemm_plan(18432, 9216, 3072, B.FORMAT_MXFP4) == {"kernel": "mxfp4_gemm_kernel",

@@ -282,7 +282,7 @@ def test_deterministic():
     assert np.array_equal(r1, r2)
 
 
-@pytest.mark.parametrize("M,N,K", [(128, 1152, 1152), (65, 130, 1152), (200, 3000, 256)])
+@pytest.mark.parametrize("M,N,K", [(256, 3072, 1152), (200, 2050, 640), (200, 3000, 256)])
 def test_small_tiles_match_the_lane_kernel(M, N, K):
     """The 64 x 64 kernel uses the lane kernel's dequantization, K order and
     epilogue, so it must give the lane kernel's output bit for bit.  The
@@ -304,3 +304,42 @@ def test_small_tiles_match_the_lane_kernel(M, N, K):
     ref = O.nvfp4_gemm_ref(ac, as_, aa, bc, bs, ba)
     assert rel_fro(small, ref) <= TOL
     check_elements(small, (ac, as_, aa), (bc, bs, ba), ref)
+
+
+# Few tokens on the wave-K kernel (32 x 32 tiles, the K stages of a
+# workgroup dealt to its four waves, their sums added in LDS in wave
+# order): 1 stage (three waves without one), 3, 5 (uneven shares), 9 and 36
+# stages; ragged M and N, N % 8 != 0.  The exact-sum shapes (64, 96, 128),
+# (300, 260, 256) and (64, 1000, 1280) above take this kernel too.
+WAVEK_SHAPES = [(7, 33, 128), (100, 200, 384), (33, 40, 640), (65, 130, 1152),
+                (128, 1152, 1152), (128, 1152, 4608)]
+
+
+@pytest.mark.parametrize("M,N,K", WAVEK_SHAPES)
+def test_wavek_kernel_vs_oracle(M, N, K):
+    assert sol.gemm_plan(M, N, K)["kernel"] == "nvfp4_gemm_wavek_kernel"
+    ac, as_, aa = quantized("outlier4x20", M, K, 21 * M + K)
+    bc, bs, ba = quantized(None, N, K, 23 * N + K, sigma=0.02)
+    bias = draw_bias(N, 0.02, N + 1)
+    got = gpu_gemm(ac, as_, aa, bc, bs, ba, bias)
+    assert np.array_equal(got, gpu_gemm(ac, as_, aa, bc, bs, ba, bias))   # fixed sum order
+    ref = O.nvfp4_gemm_ref(ac, as_, aa, bc, bs, ba, bias)
+    err = rel_fro(got, ref)
+    say(f"M={M} N={N} K={K}: rel_fro={err:.3e}")
+    assert err <= TOL
+    check_elements(got, (ac, as_, aa), (bc, bs, ba), ref, bias)
+
+
+@pytest.mark.parametrize("M,N,K", [(7, 33, 128), (33, 40, 640), (128, 1152, 4608)])
+def test_wavek_exact_sums_are_bit_exact(M, N, K):
+    """As test_exact_sums_are_bit_exact, on the wave-K kernel."""
+    assert sol.gemm_plan(M, N, K)["kernel"] == "nvfp4_gemm_wavek_kernel"
+    g = np.random.Generator(np.random.PCG64(M * 1000 + N + K))
+    ac = g.integers(0, 256, size=(M, K // 2), dtype=np.uint8)
+    bc = g.integers(0, 256, size=(N, K // 2), dtype=np.uint8)
+    as_ = np.full((M, K // 16), 0x38, np.uint8)
+    bs = np.full((N, K // 16), 0x38, np.uint8)
+    aa, ba = np.float32(2.0 ** -3), np.float32(2.0 ** 5)
+    ref = O.nvfp4_gemm_ref(ac, as_, aa, bc, bs, ba)
+    got = gpu_gemm(ac, as_, aa, bc, bs, ba)
+    assert np.array_equal(got, O.bf16_output(ref))

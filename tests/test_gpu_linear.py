@@ -70,11 +70,11 @@ def test_linear_workspace_holds_the_activation_codes():
                                    (128, 1152, 1152)])
 def test_fused_linear_leaves_codes_scales_and_alpha(M, N, K):
     """Both small-token routes (the fused one for K <= 512, amax + encode +
-    small-tile GEMM beyond) leave the activations' codes, scales and alpha
+    a few-token GEMM beyond) leave the activations' codes, scales and alpha
     in the workspace exactly as nvfp4_quantize would (codes at offset 0,
     then the scales and alpha, each region 256-byte aligned)."""
     import paper_2604_06916_amd as sol2
-    assert sol2.gemm_plan(M, N, K)["kernel"] == "nvfp4_gemm_small_kernel"
+    assert sol2.gemm_plan(M, N, K)["kernel"] in ("nvfp4_gemm_small_kernel", "nvfp4_gemm_wavek_kernel")
     xb = draw_activations("outlier4x20", M, K, seed=M + 5)
     wb = draw_weights(N, K, 0.02, seed=N + 6)
     x = bf16_to_dev(xb)
