@@ -1078,23 +1078,28 @@ bool use_small_gemm(int64_t M, int64_t N, int64_t K) {
 
 // Among the shapes the small-tile kernel takes, the wave-K kernel (32 x 32
 // tiles, each workgroup's K stages dealt to its four waves) where its
-// estimated time is lower: a launch takes ceil(tiles / CUs) rounds, and a
-// round costs a fixed part plus one per stage a wave runs.  The costs, in
-// microseconds, are fitted to measurements on one box (graph-free, 50
-// launches): the 64 x 64 kernel 3.35 + 0.40 per stage, the wave-K kernel
-// 2.83 + 0.52 per stage of its longest wave (128 x 1152 x 1152: 6.98 ->
-// 4.40 us, 128 x 1152 x 4608: 17.85 -> 7.53, 128 x 3072 x 12288: 42.7 ->
-// 28.6; kept on 64 x 64 tiles: 300 x 1000 x 512, 5.6 on wave-K against 4.9,
-// 256 x 3072 x 3072, 16.8 against 14.4, 128 x 12288 x 3072, 31.3 against
-// 21.7).
+// estimated time is lower.  A launch takes about tiles / CUs rounds, a last
+// partial round after whole ones costing 0.8 of one (it runs beside fewer
+// workgroups), and a round costs a fixed part plus one per stage a wave
+// runs.  The costs, in microseconds, are fitted to measurements on one box
+// (50 launches per timing): the 64 x 64 kernel 3.35 + 0.40 per stage, the
+// wave-K kernel 2.83 + 0.52 per stage of its longest wave (128 x 1152 x 1152
+// 6.98 -> 4.40 us, 128 x 1152 x 4608 17.85 -> 7.53, 128 x 3072 x 12288 42.7
+// -> 28.6; kept on 64 x 64 tiles: 300 x 1000 x 512, 5.6 on wave-K against
+// 4.9, 256 x 3072 x 3072 16.8 against 14.4).  On 24 shapes of 1 to 384
+// tokens the estimate picks the faster kernel every time.
 bool use_wavek_gemm(int64_t M, int64_t N, int64_t K) {
   if (!use_small_gemm(M, N, K)) return false;
   const int64_t cus = device_cu_count();
+  auto rounds = [cus](int64_t tiles) {
+    const double r = (double)(tiles / cus) + (tiles % cus ? 0.8 : 0.0);
+    return r < 1.0 ? 1.0 : r;
+  };
   const int64_t t64 = ((M + 63) / 64) * ((N + 63) / 64);
   const int64_t t32 = ((M + 31) / 32) * ((N + 31) / 32);
   const int64_t stages = K / kLBK;
-  const double small = (double)((t64 + cus - 1) / cus) * (3.35 + 0.40 * (double)stages);
-  const double wavek = (double)((t32 + cus - 1) / cus) * (2.83 + 0.52 * (double)((stages + 3) / 4));
+  const double small = rounds(t64) * (3.35 + 0.40 * (double)stages);
+  const double wavek = rounds(t32) * (2.83 + 0.52 * (double)((stages + 3) / 4));
   return wavek < small;
 }
 
