@@ -16,11 +16,10 @@
 // waits only for its own loads, so the main loop has no barrier.  At the
 // end waves 1-3 park their partial sums in LDS and wave 0 adds them in the
 // order 0 + 1, + 2, + 3 (so the result does not depend on timing) before
-// the epilogue: one FP32 fused
-// multiply-add of alpha and bias, then rounding to BF16.  The FP32 sums are
-// formed in a different order than in the other kernels, so results agree
-// with them to FP32 summation error, not bit for bit.  K must be a
-// multiple of 128 (whole stages).
+// the epilogue: one FP32 fused multiply-add of alpha and bias, then
+// rounding to BF16.  The FP32 sums are formed in a different order than in
+// the other kernels, so results agree with them to FP32 summation error,
+// not bit for bit.  K must be a multiple of 128 (whole stages).
 #include <type_traits>
 
 #include "device_common.h"
@@ -36,7 +35,7 @@ constexpr int kWKWaves = kLThreads / kWave;    // waves per workgroup, one K sha
 // scale bytes (A, then B: 64 words each, word l holding bytes 4 (l / 32) ..
 // +3 of row l % 32's 8 for the stage)
 constexpr int kWKCodes = kWKTile * kLRowBytes;       // 2 KB per operand
-constexpr int kWKBuf = 2 * kWKCodes + 1024;          // 5 KB, with room for the scales
+constexpr int kWKBuf = 2 * kWKCodes + 1024;          // 5 KB: the scales take 512 B of the last 1 KB
 constexpr int kWKScales = 2 * kWKCodes;
 
 template <bool kVecOut>
