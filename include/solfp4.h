@@ -215,8 +215,9 @@ SOLFP4_API size_t nvfp4_linear_workspace_bytes(int64_t M, int64_t N, int64_t K);
  *            alpha (offsets are an implementation detail).
  *
  * Launches: the amax pass, the encode pass and the GEMM; or, for few
- * tokens (the 64 x 64-tile GEMM) with K <= 512, the amax pass and one GEMM
- * kernel that quantizes the activations itself.  Either way the workspace
+ * tokens with K <= 512 where nvfp4_gemm runs on 64 x 64 tiles, the amax
+ * pass and one GEMM kernel that quantizes the activations itself (with the
+ * same tiles and summation order).  Either way the workspace
  * ends up holding the same codes, scales and alpha, and the result is
  * bit-identical to nvfp4_quantize followed by nvfp4_gemm with a workspace of
  * at least nvfp4_gemm_workspace_bytes(M, N, K) (the linear always splits

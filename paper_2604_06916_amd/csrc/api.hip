@@ -275,10 +275,12 @@ int nvfp4_linear(const uint16_t* x, const uint8_t* w_codes, const uint8_t* w_sca
                    N, K);
   if (rc) return rc;
   const hipStream_t s = static_cast<hipStream_t>(stream);
-  if (K <= solfp4::kFusedMaxK && solfp4::use_small_gemm(M, N, K)) {
-    // few tokens and a short K: the amax pass, then the small-tile GEMM
-    // quantizing the activations itself (leaving codes, scales and alpha in
-    // the workspace)
+  if (K <= solfp4::kFusedMaxK && solfp4::use_small_gemm(M, N, K) &&
+      !solfp4::use_wavek_gemm(M, N, K)) {
+    // few tokens and a short K, where nvfp4_gemm runs the small-tile kernel
+    // too (so the FP32 sums are formed in the same order): the amax pass,
+    // then the small-tile GEMM quantizing the activations itself (leaving
+    // codes, scales and alpha in the workspace)
     solfp4::SmallFuse fuse;
     fuse.x = x;
     fuse.partial = partial;

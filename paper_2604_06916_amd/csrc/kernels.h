@@ -134,9 +134,10 @@ hipError_t launch_gemm_wavek(const uint8_t* a_codes, const uint8_t* a_scales, co
                              const uint16_t* bias, uint16_t* out, int64_t M, int64_t N, int64_t K,
                              hipStream_t stream);
 // nvfp4_linear quantizes the activations inside the small-tile kernel up to
-// this K; beyond it the amax and encode passes followed by the small-tile
-// GEMM are faster (the in-kernel quantization costs as much VALU time as the
-// encode pass, and saves only its launch).
+// this K (where nvfp4_gemm takes that kernel, not the wave-K one); beyond it
+// the amax and encode passes followed by the GEMM are faster (the in-kernel
+// quantization costs as much VALU time as the encode pass, and saves only
+// its launch).
 constexpr int64_t kFusedMaxK = 512;
 hipError_t launch_gemm_small(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_gs,
                              const uint8_t* b_codes, const uint8_t* b_scales, const float* b_gs,

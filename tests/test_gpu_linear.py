@@ -16,16 +16,16 @@ pytestmark = pytest.mark.gpu
 # 4352 x 4096 x 1536 and 128 x 3072 x 3072: the GEMM's last round splits into
 # K halves (256 x 256 and 128 x 128 tiles), through the part of the linear's
 # workspace after the activation codes
-# Few tokens with K % 128 == 0 (128 x 1152 x 1152, 128 x 3072 x 3072,
-# 256 x 1152 x 1152) take the small-tile GEMM; with K <= 512 (ragged
-# 100 x 200 x 384, 65 x 130 x 256 with N % 8 != 0, 1 x 16 x 128, and
-# 300 x 1000 x 512) nvfp4_linear runs it with the activations quantized
-# inside the kernel: still bit-identical to nvfp4_quantize followed by
-# nvfp4_gemm
+# Few tokens with K % 128 == 0 take a few-token GEMM: the wave-K kernel
+# (128 x 1152 x 1152, 128 x 3072 x 3072, ragged 100 x 200 x 384, 65 x 130 x
+# 256 with N % 8 != 0, 1 x 16 x 128) or the 64 x 64 one (256 x 1152 x 1152,
+# 300 x 1000 x 512, 320 x 1024 x 256); where the latter runs with K <= 512
+# (the last two), nvfp4_linear quantizes the activations inside it: still
+# bit-identical to nvfp4_quantize followed by nvfp4_gemm
 @pytest.mark.parametrize("M,N,K", [(1, 16, 16), (7, 33, 48), (128, 1152, 1152), (300, 520, 2240),
                                    (517, 260, 5600), (1000, 3072, 3072), (4352, 4096, 1536),
                                    (128, 3072, 3072), (100, 200, 384), (65, 130, 256), (1, 16, 128),
-                                   (256, 1152, 1152), (300, 1000, 512)])
+                                   (256, 1152, 1152), (300, 1000, 512), (320, 1024, 256)])
 @pytest.mark.parametrize("with_bias", [False, True])
 def test_linear_matches_quantize_then_gemm_and_oracle(M, N, K, with_bias):
     xb = draw_activations("t3_1pct", M, K, seed=M + K)
@@ -67,12 +67,13 @@ def test_linear_workspace_holds_the_activation_codes():
 
 
 @pytest.mark.parametrize("M,N,K", [(64, 48, 256), (100, 200, 384), (300, 1000, 512),
-                                   (128, 1152, 1152)])
+                                   (320, 1024, 256), (128, 1152, 1152)])
 def test_fused_linear_leaves_codes_scales_and_alpha(M, N, K):
-    """Both small-token routes (the fused one for K <= 512, amax + encode +
-    a few-token GEMM beyond) leave the activations' codes, scales and alpha
-    in the workspace exactly as nvfp4_quantize would (codes at offset 0,
-    then the scales and alpha, each region 256-byte aligned)."""
+    """Every small-token route (the fused one, 300 x 1000 x 512 and
+    320 x 1024 x 256; amax + encode + a few-token GEMM otherwise) leaves the
+    activations' codes, scales and alpha in the workspace exactly as
+    nvfp4_quantize would (codes at offset 0, then the scales and alpha, each
+    region 256-byte aligned)."""
     import paper_2604_06916_amd as sol2
     assert sol2.gemm_plan(M, N, K)["kernel"] in ("nvfp4_gemm_small_kernel", "nvfp4_gemm_wavek_kernel")
     xb = draw_activations("outlier4x20", M, K, seed=M + 5)
@@ -94,9 +95,10 @@ def test_fused_linear_leaves_codes_scales_and_alpha(M, N, K):
 
 def test_fused_linear_zero_and_signed_zero_input():
     """All-zero activations (alpha = 0, every scale 0, codes keep the sign
-    of zero) through the fused path: the output is the bias, and the codes
-    in the workspace are the oracle's."""
-    M, N, K = 64, 64, 256
+    of zero) through the fused path (320 x 1024 x 256: the GEMM itself runs
+    on 64 x 64 tiles there): the output is the bias, and the codes in the
+    workspace are the oracle's."""
+    M, N, K = 320, 1024, 256
     xb = np.zeros((M, K), np.uint16)
     xb[::3, ::5] = 0x8000
     wb = draw_weights(N, K, 0.02, seed=9)
