@@ -31,6 +31,10 @@
 //     CUs' worth of tiles runs as two K halves per tile (SplitK);
 //   nvfp4_gemm_kernel (the other K % 16 == 0): the workgroup converts each
 //     stage once into FP16 tiles in LDS, which all waves read.
+// Few tokens (K % 128 == 0, at most one 64 x 64 tile per CU) take one of
+// two kernels of their own, chosen here by estimated time: 64 x 64 tiles
+// (gemm_small.hip) or 32 x 32 tiles with the K stages dealt to the four
+// waves of a workgroup (gemm_wavek.hip).
 #include <type_traits>
 
 #include "device_common.h"
