@@ -31,7 +31,7 @@ constexpr int kQuantThreads = 256;
 
 constexpr int kEncodeUnroll = 8;   // pieces per lane per iteration (large tensors)
 constexpr int kEncodeUnrollSmall = 2;   // for small tensors: four times the workgroups
-constexpr int kAmaxUnroll = 8;     // amax pass, pieces per lane per iteration (large tensors)
+constexpr int kAmaxUnroll = 4;     // amax pass, pieces per lane per iteration (large tensors)
 constexpr int kAmaxUnrollSmall = 2;
 
 // Whether the amax pass takes the large unroll: every one of its kMaxPartials

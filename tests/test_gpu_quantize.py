@@ -213,18 +213,18 @@ def test_two_pass_calls_equal_quantize(rows, K):
 
 
 # The amax pass is a grid-stride loop of whole iterations (256 threads times
-# 8 or 2 pieces of 8 elements); the one iteration that reaches past the end
+# 4 or 2 pieces of 8 elements); the one iteration that reaches past the end
 # is read element by element.  Shapes: the 2-piece unroll on 1024 workgroups
-# with three rounds, the last one partial (3001 x 4096); the 8-piece unroll
-# with a partial last iteration (4100 x 4112); a single row (2 x 16496).  The
-# tensor's largest magnitude is planted at the first element, the last one
-# and the middle of the partial iteration in turn, so alpha is right only if
-# every piece is read.
-@pytest.mark.parametrize("rows,K", [(3001, 4096), (4100, 4112), (2, 16 * 1031)])
+# with a partial second round (2000 x 3008); the 4-piece unroll with a
+# partial last iteration (3001 x 4096, 4100 x 4112); a single row
+# (2 x 16496).  The tensor's largest magnitude is planted at the first
+# element, the last one and the middle of the partial iteration in turn, so
+# alpha is right only if every piece is read.
+@pytest.mark.parametrize("rows,K", [(2000, 3008), (3001, 4096), (4100, 4112), (2, 16 * 1031)])
 def test_amax_pass_reads_every_piece(rows, K):
     xb = draw_activations("normal", rows, K, seed=rows + K)
     n = rows * K
-    per_iter = 8 * 256 * (8 if n // 8 >= 1024 * 2048 else 2)   # elements per iteration
+    per_iter = 8 * 256 * (4 if n // 8 >= 1024 * 1024 else 2)   # elements per iteration
     tail = n // per_iter * per_iter
     places = [0, n - 1, (tail + n) // 2 if tail < n else n // 2]
     x = bf16_to_dev(xb)
