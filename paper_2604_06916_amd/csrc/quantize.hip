@@ -31,6 +31,11 @@ constexpr int kQuantThreads = 256;
 
 constexpr int kEncodeUnroll = 8;   // pieces per lane per iteration (large tensors)
 constexpr int kEncodeUnrollSmall = 2;   // for small tensors: four times the workgroups
+// Tensors past the 256 MB memory-side cache: 4 pieces per lane on up to
+// 4096 workgroups (measured 2.6-3.8% faster there, 1-3% slower on 113 MB).
+constexpr int kEncodeUnrollHuge = 4;
+constexpr int64_t kEncodeHugePieces = (int64_t)1 << 24;   // 16 Mi pieces, 256 MB of BF16
+constexpr int64_t kEncodeMaxGridHuge = 4096;
 constexpr int kAmaxUnroll = 4;     // amax pass, pieces per lane per iteration (large tensors)
 constexpr int kAmaxUnrollSmall = 2;
 
@@ -231,11 +236,16 @@ hipError_t launch_encode(const uint16_t* x, int64_t rows, int64_t K, uint8_t* co
   // unroll, so that they spread over four times as many CUs; the arithmetic
   // per piece is the same
   const bool small = npieces < 64 * (int64_t)kQuantThreads * kEncodeUnroll;
-  const int64_t per_wg = (int64_t)kQuantThreads * (small ? kEncodeUnrollSmall : kEncodeUnroll);
+  const bool huge = npieces >= kEncodeHugePieces;
+  const int unroll = small ? kEncodeUnrollSmall : huge ? kEncodeUnrollHuge : kEncodeUnroll;
+  const int64_t per_wg = (int64_t)kQuantThreads * unroll;
   int64_t grid = (npieces + per_wg - 1) / per_wg;
-  if (grid > kEncodeMaxGrid) grid = kEncodeMaxGrid;
+  const int64_t cap = huge ? kEncodeMaxGridHuge : kEncodeMaxGrid;
+  if (grid > cap) grid = cap;
   if (grid < 1) grid = 1;
-  return launch_kernel(small ? nvfp4_encode_kernel<kEncodeUnrollSmall> : nvfp4_encode_kernel<kEncodeUnroll>,
+  return launch_kernel(small  ? nvfp4_encode_kernel<kEncodeUnrollSmall>
+                       : huge ? nvfp4_encode_kernel<kEncodeUnrollHuge>
+                              : nvfp4_encode_kernel<kEncodeUnroll>,
                        dim3((unsigned)grid), dim3(kQuantThreads), stream,
                        reinterpret_cast<const u32x4_t*>(x), npieces, partial, npartial,
                        reinterpret_cast<uint32_t*>(codes), scales, global_scale);
