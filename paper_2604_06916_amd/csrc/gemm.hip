@@ -1082,28 +1082,27 @@ bool use_small_gemm(int64_t M, int64_t N, int64_t K) {
 
 // Among the shapes the small-tile kernel takes, the wave-K kernel (32 x 32
 // tiles, each workgroup's K stages dealt to its four waves) where its
-// estimated time is lower.  A launch takes about tiles / CUs rounds, a last
-// partial round after whole ones costing 0.8 of one (it runs beside fewer
-// workgroups), and a round costs a fixed part plus one per stage a wave
-// runs.  The costs, in microseconds, are fitted to measurements on one box
-// (50 launches per timing): the 64 x 64 kernel 3.35 + 0.40 per stage, the
-// wave-K kernel 2.83 + 0.52 per stage of its longest wave (128 x 1152 x 1152
-// 6.98 -> 4.40 us, 128 x 1152 x 4608 17.85 -> 7.53, 128 x 3072 x 12288 42.7
-// -> 28.6; kept on 64 x 64 tiles: 300 x 1000 x 512, 5.6 on wave-K against
-// 4.9, 256 x 3072 x 3072 16.8 against 14.4).  On 24 shapes of 1 to 384
-// tokens the estimate picks the faster kernel every time.
+// estimated time is lower.  Its LDS lets two workgroups share a CU, so a
+// launch of t tiles puts ceil(t / CUs) of them on the busiest CU, and each
+// one past the first adds 0.52 of a lone workgroup's time (two at once run
+// 1.28-1.6x as long as one alone, longer K towards the top).  A lone
+// workgroup costs a fixed part plus one per stage of its longest wave; the
+// 64 x 64 kernel never takes more than one round here.  The costs, in
+// microseconds, are fitted to measurements on one box (50 launches per
+// timing): the 64 x 64 kernel 3.35 + 0.40 per stage, the wave-K kernel
+// 2.83 + 0.52 per stage (128 x 1152 x 1152 6.9 -> 4.4 us, 128 x 3072 x 12288
+// 42.4 -> 23.6 at 384 tiles, 256 x 3072 x 3072 13.7 -> 12.4 at 768; kept on
+// 64 x 64 tiles: 512 x 2048 x 2048, 10.6 against 11.9 at 1024 tiles).  On
+// 15 shapes of 7 to 512 tokens the estimate picks the faster kernel on all
+// but one, 128 x 6144 x 1536, where wave-K would be 3% faster.
 bool use_wavek_gemm(int64_t M, int64_t N, int64_t K) {
   if (!use_small_gemm(M, N, K)) return false;
   const int64_t cus = device_cu_count();
-  auto rounds = [cus](int64_t tiles) {
-    const double r = (double)(tiles / cus) + (tiles % cus ? 0.8 : 0.0);
-    return r < 1.0 ? 1.0 : r;
-  };
-  const int64_t t64 = ((M + 63) / 64) * ((N + 63) / 64);
   const int64_t t32 = ((M + 31) / 32) * ((N + 31) / 32);
   const int64_t stages = K / kLBK;
-  const double small = rounds(t64) * (3.35 + 0.40 * (double)stages);
-  const double wavek = rounds(t32) * (2.83 + 0.52 * (double)((stages + 3) / 4));
+  const double small = 3.35 + 0.40 * (double)stages;
+  const double per_cu = (double)((t32 + cus - 1) / cus);
+  const double wavek = (1.0 + 0.52 * (per_cu - 1.0)) * (2.83 + 0.52 * (double)((stages + 3) / 4));
   return wavek < small;
 }
 

