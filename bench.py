@@ -389,13 +389,15 @@ def run_small_linear(reps):
     mx_lin_us = graph_time(lambda: sol.mxfp4_linear(x, mwc, mws, b, out, mlws))
     mx_gemm_us = graph_time(lambda: sol.mxfp4_gemm(mxc, mxs, mwc, mws, b, out))
     fl = 2.0 * M * N * K
-    route = ("amax pass + GEMM quantizing the activations in the kernel" if K <= 512
+    fused = K <= 512 and nvfp4_gemm_kernel_name(M, N, K) == "nvfp4_gemm_small_kernel"
+    route = ("amax pass + GEMM quantizing the activations in the kernel" if fused
              else "amax pass + encode pass + GEMM")
     return {"layer": f"M={M} {K}->{N} nvfp4_linear (+bias)", "eager_us": round(eager_us, 2),
             "graph_us": round(graph_us, 2), "gemm_graph_us": round(gemm_us, 2),
             "gemm_kernel": nvfp4_gemm_kernel_name(M, N, K), "linear_launches": route,
             "graph_tflops": round(fl / (graph_us * 1e-6) / 1e12, 2),
             "mxfp4": {"linear_graph_us": round(mx_lin_us, 2), "gemm_graph_us": round(mx_gemm_us, 2),
+                      "gemm_kernel": sol.gemm_plan(M, N, K, sol.FORMAT_MXFP4)["kernel"],
                       "linear_launches": "mxfp4_quantize + mxfp4_gemm"},
             "roofline": {"bound": "latency", "achieved": round(fl / (graph_us * 1e-6) / 1e12, 2),
                          "peak": PEAK_FP16_MFMA_TFLOPS, "unit": "TFLOP/s",

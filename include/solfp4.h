@@ -263,6 +263,9 @@ SOLFP4_API int nvfp4_linear(const uint16_t* x, const uint8_t* w_codes, const uin
                                           activations itself */
 #define SOLFP4_KERNEL_NVFP4_WAVEK 5    /* 32 x 32 tiles for few tokens, each workgroup's
                                           K stages dealt to its four waves (K % 128 == 0) */
+#define SOLFP4_KERNEL_MXFP4_WAVEK 6    /* MXFP4, 32 x 32 tiles for few tokens, each
+                                          workgroup's K stages dealt to its four waves
+                                          (K % 128 == 0) */
 SOLFP4_API int solfp4_gemm_plan(int format, int64_t M, int64_t N, int64_t K, int with_workspace,
                      int* kernel, int* tile, int64_t* workgroups, int* splits);
 

@@ -68,7 +68,8 @@ EXPORTED = ["solfp4_strerror", "solfp4_version", "solfp4_gemm_plan",
 
 FORMAT_NVFP4, FORMAT_MXFP4 = 0, 1
 KERNEL_NAMES = {0: None, 1: "nvfp4_gemm_lane_kernel", 2: "nvfp4_gemm_kernel",
-                3: "mxfp4_gemm_kernel", 4: "nvfp4_gemm_small_kernel", 5: "nvfp4_gemm_wavek_kernel"}
+                3: "mxfp4_gemm_kernel", 4: "nvfp4_gemm_small_kernel", 5: "nvfp4_gemm_wavek_kernel",
+                6: "mxfp4_gemm_wavek_kernel"}
 
 
 class Solfp4Error(RuntimeError):

@@ -56,8 +56,12 @@ int device_cu_count();
 // ones, given the tile counts of both (host only).
 bool small_tiles_pay(int64_t tiles256, int64_t tiles128);
 
-// Output tile edge (256, 128 or 64) of an MXFP4 GEMM (host only).
+// Output tile edge (256, 128 or 64) of the tiled MXFP4 GEMM kernel (host only).
 int mx_tile_edge(int64_t M, int64_t N);
+
+// Whether an MXFP4 GEMM runs on the wave-K kernel (32 x 32 tiles, each
+// workgroup's K stages dealt to its four waves; host only).
+bool use_mx_wavek(int64_t M, int64_t N, int64_t K);
 
 // Split-K for the last, partial round of 256 x 256 tiles.  A GEMM with T
 // tiles on C compute units runs about ceil(T / C) rounds of one tile's time;
@@ -170,5 +174,12 @@ hipError_t launch_mx_quantize(const uint16_t* x, int64_t rows, int64_t K, uint8_
 hipError_t launch_mx_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const uint8_t* b_codes,
                           const uint8_t* b_scales, const uint16_t* bias, uint16_t* out, int64_t M,
                           int64_t N, int64_t K, hipStream_t stream);
+
+// The wave-K MXFP4 kernel alone (K % 128 == 0); launch_mx_gemm calls it
+// where use_mx_wavek holds.
+hipError_t launch_mx_gemm_wavek(const uint8_t* a_codes, const uint8_t* a_scales,
+                                const uint8_t* b_codes, const uint8_t* b_scales,
+                                const uint16_t* bias, uint16_t* out, int64_t M, int64_t N,
+                                int64_t K, hipStream_t stream);
 
 }  // namespace solfp4

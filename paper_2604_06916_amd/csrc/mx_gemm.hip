@@ -16,7 +16,8 @@
 // fill the chip, 128 x 128 tiles with 64 x 64 per wave, and for few tokens
 // 64 x 64 tiles with one 32 x 32 MFMA tile per wave (mx_tile_edge chooses;
 // every size runs the same sequence of MFMAs per output element, so the
-// results are bit-identical across sizes).  K advances 128
+// results are bit-identical across sizes; the wave-K kernel further down,
+// for few tokens, sums in another order).  K advances 128
 // elements (64 code bytes per row) per stage.  Codes go from global memory straight into LDS by
 // buffer loads with the LDS-destination bit (no register staging), into four
 // stage buffers: the loads for stage s+3 are issued while stage s computes,
@@ -444,6 +445,234 @@ __global__ __launch_bounds__(kMxThreads, 1) void mxfp4_gemm_kernel(
   }
 }
 
+// Few tokens, K a multiple of 128: one 32 x 32 output tile per workgroup
+// of four waves, wave w running stages w, w + 4, w + 8, ... of K, each wave
+// with a pipeline of its own (codes and scale bytes by DMA into four LDS
+// stage buffers of its own, three of its stages ahead, waiting on its own
+// loads only: no barrier in the main loop).  With 64 x 64 tiles one K loop
+// per wave runs on as many CUs as there are tiles; here four times as many
+// workgroups each run a quarter of it, and their 72 KB of LDS lets two
+// share a CU.  Waves 1-3 park their sums in their own stage buffers and
+// wave 0 adds them in wave order before the epilogue, so the FP32 sums are
+// formed in a different order than in the other tile sizes: results agree
+// with them to FP32 summation error, bit for bit where the sums are exact.
+constexpr int kMxWKTile = 32;
+constexpr int kMxWKWaves = kMxThreads / kWave;
+constexpr int kMxWKCodes = kMxWKTile * kMxRowBytes;   // 2 KB per operand and stage
+constexpr int kMxWKBuf = 2 * kMxWKCodes + 512;        // codes, then 256 B of scale words per operand
+constexpr int kMxWKScales = 2 * kMxWKCodes;
+static_assert(kMxWKWaves * kMxBufs * kMxWKBuf <= 80 * 1024 - 64, "two workgroups per CU");
+static_assert(4 * kWave * (int)sizeof(floatx4_t) <= kMxBufs * kMxWKBuf, "partial sums fit a wave's buffers");
+
+template <bool kVecOut>
+__global__ __launch_bounds__(kMxThreads, 2) void mxfp4_gemm_wavek_kernel(
+    const uint8_t* __restrict__ a_codes, const uint8_t* __restrict__ a_scales,
+    const uint8_t* __restrict__ b_codes, const uint8_t* __restrict__ b_scales,
+    const uint16_t* __restrict__ bias, uint16_t* __restrict__ out, int64_t M, int64_t N,
+    int64_t K) {
+  __shared__ __attribute__((aligned(1024))) uint8_t lbuf[kMxWKWaves][kMxBufs][kMxWKBuf];
+  __shared__ uint16_t lbias[kMxWKTile];
+
+  const int tiles_m = (int)((M + kMxWKTile - 1) / kMxWKTile);
+  const int tiles_n = (int)((N + kMxWKTile - 1) / kMxWKTile);
+  int tm, tn;
+  tile_coords(tiles_m, tiles_n, tm, tn);
+  const int64_t m0 = (int64_t)tm * kMxWKTile;
+  const int64_t n0 = (int64_t)tn * kMxWKTile;
+  const int nstages = (int)(K / kMxBK);
+
+  const int t = threadIdx.x;
+  const int lane = t & (kWave - 1);
+  const int wave = t / kWave;
+  const int li = lane & 31;
+  const int g = lane >> 5;
+
+  const int64_t row_bytes = K / 2;
+  const int64_t kgroups = K / 32;
+  const int64_t valid_a = min<int64_t>(M - m0, kMxWKTile);
+  const int64_t valid_b = min<int64_t>(N - n0, kMxWKTile);
+  const __amdgpu_buffer_rsrc_t rca = uniform_rsrc(a_codes + m0 * row_bytes, valid_a * row_bytes);
+  const __amdgpu_buffer_rsrc_t rcb = uniform_rsrc(b_codes + n0 * row_bytes, valid_b * row_bytes);
+  const __amdgpu_buffer_rsrc_t rsa = uniform_rsrc(a_scales + m0 * kgroups, valid_a * kgroups);
+  const __amdgpu_buffer_rsrc_t rsb = uniform_rsrc(b_scales + n0 * kgroups, valid_b * kgroups);
+
+  // this wave's stages: wave + 4 i for i < count
+  const int count = nstages > wave ? (nstages - wave + kMxWKWaves - 1) / kMxWKWaves : 0;
+
+  // code DMA as in the tiled kernel: lane quad l/4 reads the 64 bytes of row
+  // l/4 of a 16-row group (rows past the operand read zero), lane l's 16
+  // bytes land in slot l of the group's 1 KB, the piece order of row r
+  // swizzled by (r >> 2) & 3
+  const int dma_r = lane >> 2;
+  const int piece = (lane & 3) ^ ((dma_r >> 2) & 3);
+  const uint32_t dma_off = (uint32_t)(dma_r * row_bytes + 16 * piece);
+  const uint32_t group_stride = (uint32_t)(16 * row_bytes);
+  // operand slots of this lane (row li of A and of B): lane group g reads
+  // piece 2 st + g in K-step st
+  const int swz = ((li & 15) >> 2) & 3;
+  const int rd = (li >> 4) * 1024 + (li & 15) * 64;
+  const int q_off[2] = {16 * (g ^ swz), 16 * ((2 + g) ^ swz)};
+  // scale DMA: lane l fetches the 4 scale bytes of row l % 32 for the stage
+  // (kgroups 4 s .. 4 s + 3; lanes 32-63 repeat lanes 0-31), one
+  // instruction per operand; rows past the operand read zero
+  const uint32_t sc_off = (uint32_t)(li * kgroups);
+
+  if (t < kMxWKTile) lbias[t] = bias && n0 + t < N ? bias[n0 + t] : (uint16_t)0;
+
+  floatx16_t acc = floatx16_t{};
+
+  // the loads of this wave's i-th stage into buffer B (6 instructions)
+  auto issue = [&](auto buf, int i) {
+    constexpr int B = decltype(buf)::value;
+    const int stage = wave + kMxWKWaves * i;
+    uint8_t* base = &lbuf[wave][B][0];
+    const uint32_t off = dma_off + (uint32_t)stage * kMxRowBytes;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rca, (lds_ptr_t)(base), 16, off, 0, 0, 1);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rca, (lds_ptr_t)(base + 1024), 16, off + group_stride, 0, 0, 1);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rcb, (lds_ptr_t)(base + kMxWKCodes), 16, off, 0, 0, 1);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rcb, (lds_ptr_t)(base + kMxWKCodes + 1024), 16,
+                                             off + group_stride, 0, 0, 1);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsa, (lds_ptr_t)(base + kMxWKScales), 4,
+                                             sc_off + 4 * stage, 0, 0, 1);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsb, (lds_ptr_t)(base + kMxWKScales + 256), 4,
+                                             sc_off + 4 * stage, 0, 0, 1);
+  };
+  constexpr int kPerStage = 6;   // vector-memory instructions per stage
+
+  // one stage from buffer B: per K-step st the lane's code pieces of A and
+  // B and byte 2 st + g of its rows' scale words (brought to byte 2 st by a
+  // shift of 8 g, so the byte select is a constant), then one MFMA
+  auto compute = [&](auto buf) {
+    constexpr int B = decltype(buf)::value;
+    const uint8_t* base = &lbuf[wave][B][0];
+    const u32x4_t xa0 = *reinterpret_cast<const u32x4_t*>(base + rd + q_off[0]);
+    const u32x4_t xb0 = *reinterpret_cast<const u32x4_t*>(base + kMxWKCodes + rd + q_off[0]);
+    const u32x4_t xa1 = *reinterpret_cast<const u32x4_t*>(base + rd + q_off[1]);
+    const u32x4_t xb1 = *reinterpret_cast<const u32x4_t*>(base + kMxWKCodes + rd + q_off[1]);
+    const uint32_t* sw = reinterpret_cast<const uint32_t*>(base + kMxWKScales);
+    const int ssa = (int)(sw[li] >> (8 * g));
+    const int ssb = (int)(sw[64 + li] >> (8 * g));
+    acc = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fp4_operand(xb0), fp4_operand(xa0), acc,
+                                                          4, 4, 0, ssb, 0, ssa);
+    acc = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fp4_operand(xb1), fp4_operand(xa1), acc,
+                                                          4, 4, 2, ssb, 2, ssa);
+  };
+
+  // stage i (buffer i % 4): the loads of stage i+3 go into the buffer read
+  // in stage i-1, whose LDS reads the wait at the end of that stage
+  // completed; then wait until stage i's loads have landed
+  using B0 = std::integral_constant<int, 0>;
+  using B1 = std::integral_constant<int, 1>;
+  using B2 = std::integral_constant<int, 2>;
+  using B3 = std::integral_constant<int, 3>;
+  auto run = [&](auto buf, int i) {
+    constexpr int B = decltype(buf)::value;
+    if (i + 3 < count) {
+      issue(std::integral_constant<int, (B + 3) % kMxBufs>{}, i + 3);
+      wait_counts<3 * kPerStage, 0>();
+    } else if (i + 2 < count) {
+      wait_counts<2 * kPerStage, 0>();
+    } else if (i + 1 < count) {
+      wait_counts<kPerStage, 0>();
+    } else {
+      wait_counts<0, 0>();
+    }
+    compute(buf);
+    wait_counts<63, 0>();   // this stage's LDS reads done before its buffer is refilled
+  };
+
+  if (count > 0) issue(B0{}, 0);
+  if (count > 1) issue(B1{}, 1);
+  if (count > 2) issue(B2{}, 2);
+  int i = 0;
+  for (; i + 4 <= count; i += 4) {
+    run(B0{}, i);
+    run(B1{}, i + 1);
+    run(B2{}, i + 2);
+    run(B3{}, i + 3);
+  }
+  if (i < count) run(B0{}, i);
+  if (i + 1 < count) run(B1{}, i + 1);
+  if (i + 2 < count) run(B2{}, i + 2);
+  wait_counts<0, 0>();
+
+  // waves 1-3 park their sums in their own stage buffers (their loads and
+  // reads are complete), wave 0 adds them in wave order
+  if (wave > 0) {
+    floatx4_t* red = reinterpret_cast<floatx4_t*>(&lbuf[wave][0][0]);
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      red[q * kWave + lane] = floatx4_t{acc[4 * q], acc[4 * q + 1], acc[4 * q + 2], acc[4 * q + 3]};
+  }
+  __syncthreads();
+  if (wave != 0) return;
+#pragma unroll
+  for (int w = 1; w < kMxWKWaves; ++w)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const floatx4_t p = reinterpret_cast<const floatx4_t*>(&lbuf[w][0][0])[q * kWave + lane];
+      acc[4 * q] += p[0];
+      acc[4 * q + 1] += p[1];
+      acc[4 * q + 2] += p[2];
+      acc[4 * q + 3] += p[3];
+    }
+
+  // epilogue: out = bf16(fp32(acc + bias)), stored as in the tiled kernel
+  const __amdgpu_buffer_rsrc_t ro = uniform_rsrc(out + m0 * N, valid_a * N * 2);
+  constexpr uint32_t kDrop = 0x80000000u;   // beyond any output range (N < 2^22)
+  const uint32_t mrow = (uint32_t)(li * N);
+  float v[16];
+#pragma unroll
+  for (int q = 0; q < 16; ++q) v[q] = acc[q];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const uint2 b2 = *reinterpret_cast<const uint2*>(&lbias[8 * k + 4 * g]);
+    v[4 * k + 0] += __uint_as_float(b2.x << 16);
+    v[4 * k + 1] += __uint_as_float(b2.x & 0xFFFF0000u);
+    v[4 * k + 2] += __uint_as_float(b2.y << 16);
+    v[4 * k + 3] += __uint_as_float(b2.y & 0xFFFF0000u);
+  }
+  uint32_t p[4][2];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    p[k][0] = pack_bf16(v[4 * k], v[4 * k + 1]);
+    p[k][1] = pack_bf16(v[4 * k + 2], v[4 * k + 3]);
+  }
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    uint32_t r[4];   // 8 columns starting at 16 h + 8 g
+#pragma unroll
+    for (int d = 0; d < 2; ++d) {
+      const auto x = __builtin_amdgcn_permlane32_swap(p[2 * h][d], p[2 * h + 1][d], false, false);
+      r[d] = x[0];
+      r[2 + d] = x[1];
+    }
+    const int64_t n = n0 + 16 * h + 8 * g;
+    if (kVecOut) {
+      const uint32_t off = n < N ? (mrow + (uint32_t)n) * 2 : kDrop;
+      __builtin_amdgcn_raw_buffer_store_b128(u32x4_t{r[0], r[1], r[2], r[3]}, ro, off, 0, 0);
+    } else {
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const uint32_t off = n + q < N ? (mrow + (uint32_t)(n + q)) * 2 : kDrop;
+        __builtin_amdgcn_raw_buffer_store_b16((uint16_t)(r[q / 2] >> (16 * (q & 1))), ro, off, 0, 0);
+      }
+    }
+  }
+}
+
+hipError_t launch_mx_gemm_wavek(const uint8_t* a_codes, const uint8_t* a_scales,
+                                const uint8_t* b_codes, const uint8_t* b_scales,
+                                const uint16_t* bias, uint16_t* out, int64_t M, int64_t N,
+                                int64_t K, hipStream_t stream) {
+  const int64_t tiles = ((M + kMxWKTile - 1) / kMxWKTile) * ((N + kMxWKTile - 1) / kMxWKTile);
+  const dim3 grid((unsigned)tiles), block(kMxThreads);
+  return N % 8 == 0 ? launch_kernel(mxfp4_gemm_wavek_kernel<true>, grid, block, stream, a_codes,
+                                    a_scales, b_codes, b_scales, bias, out, M, N, K)
+                    : launch_kernel(mxfp4_gemm_wavek_kernel<false>, grid, block, stream, a_codes,
+                                    a_scales, b_codes, b_scales, bias, out, M, N, K);
+}
+
 // The output tile edge: one workgroup holds one tile at a time on its CU, so
 // a launch takes about ceil(tiles / CUs) rounds of one tile's time.  Between
 // 256 x 256 and 128 x 128 tiles small_tiles_pay decides; a 64 x 64 tile costs
@@ -466,9 +695,35 @@ int mx_tile_edge(int64_t M, int64_t N) {
   return r64 * SOLFP4_MX_TINY_TILE_COST < r128 ? 64 : 128;
 }
 
+// Few tokens: the wave-K kernel where its 32 x 32 tiles fit one workgroup
+// per CU and its estimated time is below the 64 x 64 kernel's (which then
+// runs one round).  Both are bound by how fast a CU moves codes into LDS:
+// a second workgroup on a CU nearly doubles the wave-K kernel's time on
+// long K, so past one tile per CU it lost to 64 x 64 tiles on most shapes
+// measured (0.62-0.91x at 384 to 1024 tiles; 1.03-1.14x at 280 to 350).
+// Costs in microseconds, fitted to measurements on one box (50 launches
+// per timing): 64 x 64 tiles 2.70 + 0.158 per stage, wave-K 2.64 + 0.28 per
+// stage of its longest wave (128 x 1152 x 1152 4.30 -> 3.43 us,
+// 16 x 3072 x 3072 6.09 -> 4.61, 128 x 1152 x 4608 8.26 -> 5.14; a single
+// stage, 7 x 33 x 128, stays on 64 x 64 tiles: 2.79 against 2.92).
+bool use_mx_wavek(int64_t M, int64_t N, int64_t K) {
+  if (K % kMxBK != 0 || K == 0 || M <= 0 || N <= 0 || mx_tile_edge(M, N) != 64) return false;
+  const int64_t t32 = ((M + kMxWKTile - 1) / kMxWKTile) * ((N + kMxWKTile - 1) / kMxWKTile);
+  if (t32 > device_cu_count()) return false;
+  const int64_t stages = K / kMxBK;
+  const double tiled = 2.70 + 0.158 * (double)stages;
+  const double wavek = 2.64 + 0.28 * (double)((stages + kMxWKWaves - 1) / kMxWKWaves);
+  return wavek < tiled;
+}
+
 void describe_mx_gemm(int64_t M, int64_t N, int64_t K, int* kernel, int* tile, int64_t* workgroups) {
+  if (use_mx_wavek(M, N, K)) {
+    *kernel = SOLFP4_KERNEL_MXFP4_WAVEK;
+    *tile = kMxWKTile;
+    *workgroups = ((M + kMxWKTile - 1) / kMxWKTile) * ((N + kMxWKTile - 1) / kMxWKTile);
+    return;
+  }
   const int edge = mx_tile_edge(M, N);
-  (void)K;
   *kernel = SOLFP4_KERNEL_MXFP4;
   *tile = edge;
   *workgroups = ((M + edge - 1) / edge) * ((N + edge - 1) / edge);
@@ -478,6 +733,8 @@ hipError_t launch_mx_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const
                           const uint8_t* b_scales, const uint16_t* bias, uint16_t* out, int64_t M,
                           int64_t N, int64_t K, hipStream_t stream) {
   if (M == 0 || N == 0) return hipSuccess;
+  if (use_mx_wavek(M, N, K))
+    return launch_mx_gemm_wavek(a_codes, a_scales, b_codes, b_scales, bias, out, M, N, K, stream);
   const int edge = mx_tile_edge(M, N);
   const dim3 grid((unsigned)(((M + edge - 1) / edge) * ((N + edge - 1) / edge))), block(kMxThreads);
   const bool fast = K % kMxBK == 0;

@@ -41,7 +41,7 @@ int main(void) {
   CHECK(kernel == SOLFP4_KERNEL_NVFP4_LANE && tile == 256 && splits == 2);
   CHECK(solfp4_gemm_plan(SOLFP4_FORMAT_MXFP4, 128, 1152, 1152, 0, &kernel, &tile, &wgs, &splits) ==
         SOLFP4_OK);
-  CHECK(kernel == SOLFP4_KERNEL_MXFP4 && tile == 64 && wgs == 36 && splits == 1);
+  CHECK(kernel == SOLFP4_KERNEL_MXFP4_WAVEK && tile == 32 && wgs == 144 && splits == 1);
   CHECK(solfp4_gemm_plan(7, 16, 16, 16, 0, &kernel, &tile, &wgs, &splits) == SOLFP4_EINVAL);
 
   /* argument errors, returned before any launch */

@@ -128,10 +128,15 @@ def test_gemm_plan_names_the_kernels():
                                                               "tile": 256, "workgroups": 2592,
                                                               "splits": 1}
     # MXFP4 tiles by token count (on a host without a device the library
-    # plans for 256 CUs): 64 x 64 while they take at most two rounds and
-    # 128 x 128 tiles one, 128 x 128 beyond
+    # plans for 256 CUs): the wave-K kernel's 32 x 32 tiles while they fit
+    # one per CU and K spans more than one stage, 64 x 64 while those take
+    # at most two rounds and 128 x 128 tiles one, 128 x 128 beyond
     mx = lambda M, N, K: B.gemm_plan(M, N, K, B.FORMAT_MXFP4)
-    assert (mx(128, 1152, 1152)["tile"], mx(128, 1152, 1152)["workgroups"]) == (64, 36)
+    assert mx(128, 1152, 1152) == {"kernel": "mxfp4_gemm_wavek_kernel", "tile": 32,
+                                   "workgroups": 144, "splits": 1}
+    assert mx(7, 33, 128)["tile"] == 64                      # one stage
+    assert mx(128, 1152, 1120)["tile"] == 64                 # K % 128 != 0
+    assert mx(128, 3072, 3072)["tile"] == 64                 # 384 tiles of 32 x 32
     assert mx(384, 3072, 3072)["tile"] == 64 and mx(512, 2240, 2240)["workgroups"] == 280
     assert mx(1024, 3072, 3072)["tile"] == 128 and mx(1000, 3000, 256)["tile"] == 128
     assert mx(2100, 9000, 3072)["tile"] == 256

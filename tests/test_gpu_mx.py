@@ -155,9 +155,10 @@ def test_golden_gemm():
         assert int(got[0, 0]) == c["bf16"], name
 
 
-# The small shapes run on 64 x 64 tiles, (1000, 3000, K) and (1024, 3072, K)
-# on 128 x 128 ones, (4200, 4360, K) and (6000, 6152, 1024) on 256 x 256 ones
-# (ragged M and N).  Scale groups (16 bytes of a row) are one 16-byte load;
+# The small shapes run on 64 x 64 tiles or, where K spans several 128-element
+# stages ((64, 96, 512), (260, 300, 1152)), on the wave-K kernel; (1000, 3000,
+# K) and (1024, 3072, K) on 128 x 128 tiles, (4200, 4360, K) and (6000, 6152,
+# 1024) on 256 x 256 ones (ragged M and N).  Scale groups (16 bytes of a row) are one 16-byte load;
 # with K % 128 != 0 (K = 96, 2240) rows start at any byte offset and the lane
 # of an operand's last row whose group reaches past the range loads bytes
 # instead, on every tile size.  K = 1152 (K % 512 !=
@@ -233,6 +234,46 @@ def test_random_vs_oracle(M, N, K, with_bias):
     assert mism <= 0.01
     sabs = abs_products(O.mxfp4_unscaled_ref(ac, as_), O.mxfp4_unscaled_ref(bc, bs))
     assert_per_element(got, ref, sabs, 1.0, K, bias)
+
+
+# Few tokens on the wave-K kernel (32 x 32 tiles, each workgroup's K stages
+# dealt to its four waves, their sums added in LDS in wave order): 2 stages
+# (two waves without one), 3, 5 (uneven shares), 9 and 36 stages; ragged M
+# and N, N % 8 != 0.
+MX_WAVEK_SHAPES = [(7, 33, 256), (100, 200, 384), (33, 40, 640), (65, 130, 1152),
+                   (128, 1152, 1152), (128, 1152, 4608)]
+
+
+@pytest.mark.parametrize("M,N,K", MX_WAVEK_SHAPES)
+def test_wavek_kernel_vs_oracle(M, N, K):
+    assert sol.gemm_plan(M, N, K, sol.FORMAT_MXFP4)["kernel"] == "mxfp4_gemm_wavek_kernel"
+    ac, as_ = O.mxfp4_quantize_ref(draw_activations("outlier4x20", M, K, 31 * M + K))
+    bc, bs = O.mxfp4_quantize_ref(draw_weights(N, K, 0.02, 37 * N + K))
+    bias = draw_bias(N, 0.02, N + 3)
+    got = gpu_gemm(ac, as_, bc, bs, bias)
+    assert np.array_equal(got, gpu_gemm(ac, as_, bc, bs, bias))   # fixed sum order
+    ref = O.mxfp4_gemm_ref(ac, as_, bc, bs, bias)
+    err = rel_fro(got, ref)
+    say(f"wave-K M={M} N={N} K={K}: rel_fro={err:.3e}")
+    assert err <= TOL
+    assert bf16_mismatch_fraction(got, ref) <= 0.01
+    sabs = abs_products(O.mxfp4_unscaled_ref(ac, as_), O.mxfp4_unscaled_ref(bc, bs))
+    assert_per_element(got, ref, sabs, 1.0, K, bias)
+
+
+@pytest.mark.parametrize("M,N,K", [(7, 33, 256), (33, 40, 640), (128, 1152, 4608)])
+def test_wavek_exact_sums_are_bit_exact(M, N, K):
+    """As test_exact_sums_are_bit_exact, on the wave-K kernel: the sum of
+    the four waves' partial sums is exact too."""
+    assert sol.gemm_plan(M, N, K, sol.FORMAT_MXFP4)["kernel"] == "mxfp4_gemm_wavek_kernel"
+    g = np.random.Generator(np.random.PCG64(M * 1000 + N + K + 7))
+    ac = g.integers(0, 256, size=(M, K // 2), dtype=np.uint8)
+    bc = g.integers(0, 256, size=(N, K // 2), dtype=np.uint8)
+    as_ = np.full((M, K // 32), 125, np.uint8)
+    bs = np.full((N, K // 32), 130, np.uint8)
+    ref = O.mxfp4_gemm_ref(ac, as_, bc, bs)
+    got = gpu_gemm(ac, as_, bc, bs)
+    assert np.array_equal(got, O.bf16_output(ref))
 
 
 def test_wide_dynamic_range_vs_oracle():

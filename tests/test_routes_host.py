@@ -11,5 +11,7 @@ def test_route_shapes_meet_every_kernel():
             ("nvfp4_gemm_lane_kernel", 128), ("nvfp4_gemm_lane_kernel", 256),
             ("nvfp4_gemm_kernel", 256)} <= nv
     assert any(sol.gemm_plan(*s)["splits"] == 2 for s in SHAPES)
-    mx = {sol.gemm_plan(M, N, K - K % 32, sol.FORMAT_MXFP4)["tile"] for M, N, K in SHAPES if K >= 32}
-    assert mx == {64, 128, 256}
+    mx = {(p["kernel"], p["tile"]) for p in (sol.gemm_plan(M, N, K - K % 32, sol.FORMAT_MXFP4)
+                                              for M, N, K in SHAPES if K >= 32)}
+    assert mx == {("mxfp4_gemm_wavek_kernel", 32), ("mxfp4_gemm_kernel", 64),
+                  ("mxfp4_gemm_kernel", 128), ("mxfp4_gemm_kernel", 256)}
