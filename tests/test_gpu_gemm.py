@@ -309,10 +309,11 @@ def test_small_tiles_match_the_lane_kernel(M, N, K):
 # Few tokens on the wave-K kernel (32 x 32 tiles, the K stages of a
 # workgroup dealt to its four waves, their sums added in LDS in wave
 # order): 1 stage (three waves without one), 3, 5 (uneven shares), 9 and 36
-# stages; ragged M and N, N % 8 != 0.  The exact-sum shapes (64, 96, 128),
-# (300, 260, 256) and (64, 1000, 1280) above take this kernel too.
+# stages; ragged M and N, N % 8 != 0; 384 tiles, so that two workgroups
+# share a CU.  The exact-sum shapes (64, 96, 128), (300, 260, 256) and
+# (64, 1000, 1280) above take this kernel too.
 WAVEK_SHAPES = [(7, 33, 128), (100, 200, 384), (33, 40, 640), (65, 130, 1152),
-                (128, 1152, 1152), (128, 1152, 4608)]
+                (128, 1152, 1152), (128, 1152, 4608), (128, 3072, 3072)]
 
 
 @pytest.mark.parametrize("M,N,K", WAVEK_SHAPES)

@@ -105,9 +105,12 @@ def oracle_check(fmt, x, layers, got):
     return err
 
 
+# (300, [256, 288, 160]): the wave-K GEMM (K = 256), then 128 x 128 tiles
+# (K % 128 != 0); (128, [1152, 1152, 4608]): 128 tokens, the wave-K GEMM
+# (K = 1152), then 64 x 64 tiles (1152 -> 4608)
 @pytest.mark.parametrize("fmt", ["nvfp4", "mxfp4"])
-def test_graph_replay_after_in_place_requantization(fmt):
-    M, dims = 300, [256, 288, 160]
+@pytest.mark.parametrize("M,dims", [(300, [256, 288, 160]), (128, [1152, 1152, 4608])])
+def test_graph_replay_after_in_place_requantization(fmt, M, dims):
     x, layers = setup(fmt, M, dims, 77)
     requantize(fmt, layers)
     forward(fmt, x, layers, "y")             # eager warm-up (loads the code objects)
