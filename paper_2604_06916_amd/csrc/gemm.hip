@@ -472,7 +472,21 @@ __global__ __launch_bounds__(kLThreads, 1) void nvfp4_gemm_lane_kernel(
   const int rem = sub < 0 ? -1 : sub / split.splits;
   const int part_idx = sub < 0 ? 0 : sub - rem * split.splits;
   int tm, tn;
-  tile_coords_at(sub < 0 ? (int)blockIdx.x : split.dp_tiles + rem, tiles_m, tiles_n, tm, tn);
+  const int tile_id = sub < 0 ? (int)blockIdx.x : split.dp_tiles + rem;
+  if constexpr (kWT == 64) {
+    if (split.quad_base >= 0) {
+      // quadrant tile_id % 4 of 256 x 256 tile quad_base + tile_id / 4
+      tile_coords_at(split.quad_base + tile_id / 4, (int)((M + 255) / 256), (int)((N + 255) / 256),
+                     tm, tn);
+      tm = 2 * tm + ((tile_id >> 1) & 1);
+      tn = 2 * tn + (tile_id & 1);
+      if ((int64_t)tm * kT >= M || (int64_t)tn * kT >= N) return;   // quadrant outside the output
+    } else {
+      tile_coords_at(tile_id, tiles_m, tiles_n, tm, tn);
+    }
+  } else {
+    tile_coords_at(tile_id, tiles_m, tiles_n, tm, tn);
+  }
   const int64_t m0 = (int64_t)tm * kT;
   const int64_t n0 = (int64_t)tn * kT;
   const int all_stages = (int)((K + kLBK - 1) / kLBK);
@@ -957,14 +971,32 @@ bool small_tiles_pay(int64_t tiles256, int64_t tiles128) {
   return small < big;
 }
 
+// Quadrants of the last round split in K halves from this many stages on
+// (measured: 8 stages 0.92x of whole quadrants, 18 stages 1.01x, 24-96
+// stages 1.05-1.10x).
+constexpr int64_t kQuadHalvesMinStages = 16;
+
 SplitPlan plan_split(int64_t tiles, int64_t nstages, double fixed_cost, double part_cost,
-                     size_t part_tile_bytes) {
+                     size_t part_tile_bytes, bool quad_ok) {
   SplitPlan plan;
   plan.dp_tiles = tiles;
   plan.stages = nstages;
   const int64_t cus = device_cu_count();
   const int64_t rem = tiles % cus;
-  if (rem == 0 || nstages < 2) return plan;
+  if (rem == 0) return plan;
+  if (quad_ok && tiles > cus && 4 * rem <= cus) {
+    plan.quad = true;
+    plan.rem_tiles = rem;
+    plan.dp_tiles = tiles - rem;
+    if (8 * rem <= cus && nstages >= kQuadHalvesMinStages) {
+      const int64_t quads = 4 * rem;
+      plan.splits = 2;
+      plan.stages = (nstages + 1) / 2;
+      plan.bytes = ((size_t)quads * 8 + 255) / 256 * 256 + (size_t)quads * 2 * (part_tile_bytes / 4);
+    }
+    return plan;
+  }
+  if (nstages < 2) return plan;
   // two K halves per remainder tile (the kernels add exactly two), when
   // both halves of every remainder tile fit in one round
   if (2 * rem > cus) return plan;
@@ -1031,8 +1063,9 @@ static SplitPlan gemm_plan(int64_t M, int64_t N, int64_t K, bool* small_out) {
   if (!lane_ok) return plan;
   const int64_t nstages = (K + kLBK - 1) / kLBK;
   if (small)
-    return plan_split(t128, nstages, SOLFP4_SPLIT_FIXED_SMALL, SOLFP4_SPLIT_PART_SMALL, 128 * 128 * 4);
-  return plan_split(t256, nstages, SOLFP4_SPLIT_FIXED, SOLFP4_SPLIT_PART, 256 * 256 * 4);
+    return plan_split(t128, nstages, SOLFP4_SPLIT_FIXED_SMALL, SOLFP4_SPLIT_PART_SMALL, 128 * 128 * 4,
+                      false);
+  return plan_split(t256, nstages, SOLFP4_SPLIT_FIXED, SOLFP4_SPLIT_PART, 256 * 256 * 4, true);
 }
 
 size_t gemm_workspace_bytes(int64_t M, int64_t N, int64_t K) {
@@ -1059,13 +1092,16 @@ void describe_gemm(int64_t M, int64_t N, int64_t K, bool with_workspace, int* ke
   bool small = false;
   SplitPlan plan = gemm_plan(M, N, K, &small);
   const bool split = plan.active() && with_workspace;
-  const bool lane = K % kLBK == 0 || K % 64 == 32 || (K % 32 == 0 && (small || split));
+  const bool lane = K % kLBK == 0 || K % 64 == 32 || (K % 32 == 0 && (small || split || plan.quad));
   *kernel = lane ? SOLFP4_KERNEL_NVFP4_LANE : SOLFP4_KERNEL_NVFP4_SHARED;
   *tile = small ? 128 : 256;
   *splits = split ? (int)plan.splits : 1;
   const int64_t tiles = small ? ((M + 127) / 128) * ((N + 127) / 128)
                               : ((M + 255) / 256) * ((N + 255) / 256);
-  *workgroups = split ? plan.dp_tiles + plan.rem_tiles * plan.splits : tiles;
+  if (plan.quad)
+    *workgroups = plan.dp_tiles + 4 * plan.rem_tiles * (split ? plan.splits : 1);
+  else
+    *workgroups = split ? plan.dp_tiles + plan.rem_tiles * plan.splits : tiles;
 }
 
 // The small-tile kernel takes the shapes whose 64 x 64 tiles fit in one
@@ -1121,6 +1157,60 @@ hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const fl
                              workspace, workspace_bytes, stream);
 }
 
+// The whole tiles in one launch of 256 x 256 tiles, then the last round's
+// tiles as four 128 x 128 quadrants each (their K halves added through the
+// workspace when the plan splits them).  The quadrants run the same MFMAs
+// per output element in the same order as whole tiles (or, split, as two K
+// halves of a whole tile), so the output is bit-identical to the one-launch
+// plan that leaves those tiles whole (or splits them in two).  Measured on
+// one box against the one-launch plans: shapes with one round plus 8 to 64
+// tiles 1.04-1.20x (K = 256 to 12288), 18432 x 9216 x 3072 1.017x.
+static hipError_t launch_gemm_quad(const uint8_t* a_codes, const uint8_t* a_scales,
+                                   const float* a_gs, const uint8_t* b_codes,
+                                   const uint8_t* b_scales, const float* b_gs,
+                                   const uint16_t* bias, uint16_t* out, int64_t M, int64_t N,
+                                   int64_t K, const SplitPlan& plan, void* workspace,
+                                   hipStream_t stream) {
+  const bool vec = N % 8 == 0, full = K % kLBK == 0;
+  const int all_stages = (int)((K + kLBK - 1) / kLBK);
+  SplitK whole{};
+  whole.dp_tiles = (int)plan.dp_tiles;
+  whole.splits = 1;
+  whole.stages = all_stages;
+  const int64_t quads = 4 * plan.rem_tiles;
+  SplitK tail{};
+  tail.quad_base = (int)plan.dp_tiles;
+  if (plan.active()) {
+    tail.dp_tiles = 0;
+    tail.splits = (int)plan.splits;
+    tail.stages = (int)plan.stages;
+    tail.slots = static_cast<uint64_t*>(workspace);
+    tail.part = reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) +
+                                         ((size_t)quads * 8 + 255) / 256 * 256);
+  } else {
+    tail.dp_tiles = (int)quads;
+    tail.splits = 1;
+    tail.stages = all_stages;
+  }
+  const dim3 block(kLThreads);
+#define SOLFP4_QUAD_LAUNCH(V, F, W, G, S)                                                       \
+  launch_kernel(nvfp4_gemm_lane_kernel<V, F, W>, G, block, stream, a_codes, a_scales, a_gs,     \
+                b_codes, b_scales, b_gs, bias, out, M, N, K, S)
+#define SOLFP4_QUAD_PICK(W, G, S)                                                               \
+  (vec && full ? SOLFP4_QUAD_LAUNCH(true, true, W, G, S)                                       \
+   : full      ? SOLFP4_QUAD_LAUNCH(false, true, W, G, S)                                      \
+   : vec       ? SOLFP4_QUAD_LAUNCH(true, false, W, G, S)                                      \
+               : SOLFP4_QUAD_LAUNCH(false, false, W, G, S))
+  if (plan.dp_tiles > 0) {
+    const hipError_t e = SOLFP4_QUAD_PICK(128, dim3((unsigned)plan.dp_tiles), whole);
+    if (e != hipSuccess) return e;
+  }
+  const hipError_t e = SOLFP4_QUAD_PICK(64, dim3((unsigned)(quads * tail.splits)), tail);
+#undef SOLFP4_QUAD_PICK
+#undef SOLFP4_QUAD_LAUNCH
+  return e;
+}
+
 hipError_t launch_gemm_regular(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_gs,
                                const uint8_t* b_codes, const uint8_t* b_scales, const float* b_gs,
                                const uint16_t* bias, uint16_t* out, int64_t M, int64_t N, int64_t K,
@@ -1134,10 +1224,21 @@ hipError_t launch_gemm_regular(const uint8_t* a_codes, const uint8_t* a_scales, 
   bool small = false;
   SplitPlan plan = gemm_plan(M, N, K, &small);
   if (plan.active() && (workspace == nullptr || workspace_bytes < plan.bytes)) {
-    plan = SplitPlan{};   // no room: every tile whole
+    // no room: every tile (or quadrant) whole
+    const bool quad = plan.quad;
+    const int64_t rem = plan.rem_tiles;
+    plan = SplitPlan{};
     plan.dp_tiles = small ? ((M + 127) / 128) * ((N + 127) / 128) : ((M + 255) / 256) * ((N + 255) / 256);
     plan.stages = (K + kLBK - 1) / kLBK;
+    if (quad) {
+      plan.quad = true;
+      plan.rem_tiles = rem;
+      plan.dp_tiles -= rem;
+    }
   }
+  if (plan.quad)
+    return launch_gemm_quad(a_codes, a_scales, a_gs, b_codes, b_scales, b_gs, bias, out, M, N, K,
+                            plan, workspace, stream);
   if (K % kLBK == 0 || K % 64 == 32 || (K % 32 == 0 && (small || plan.active()))) {
     const SplitK split = split_args(plan, workspace);
     const dim3 lgrid((unsigned)(plan.dp_tiles + plan.rem_tiles * plan.splits));

@@ -83,21 +83,30 @@ struct SplitK {
   int dp_tiles;         // workgroups that take whole tiles (all of them: no split)
   int splits;           // K ranges per remainder tile: 2 (1: no split)
   int stages;           // K stages of the first half (the second may have fewer)
+  int quad_base = -1;   // 128 x 128 tiles only: >= 0 when this launch covers the 256 x 256
+                        // tiles from this index on (in tile order), each as four quadrants
 };
 
 struct SplitPlan {
   int64_t dp_tiles = 0, rem_tiles = 0, splits = 1, stages = 0;
   size_t bytes = 0;      // workspace: slots (256-byte aligned), then partial sums
+  // the rem_tiles 256 x 256 tiles after the dp_tiles whole ones run in a
+  // launch of their own as four 128 x 128 quadrants each (splits: K ranges
+  // per quadrant)
+  bool quad = false;
   bool active() const { return splits > 1; }
 };
 
-// The plan for `tiles` output tiles of `nstages` K stages each: split the
-// remainder tiles when the estimated last round, ceil(nstages / 2) +
-// fixed_cost + 2 part_cost stages (a half, then writing its partial tile
-// and reading the other's), beats nstages + fixed_cost.  A tile's FP32
-// partial sums take part_tile_bytes.
+// The plan for `tiles` output tiles of `nstages` K stages each.  With
+// quad_ok (256 x 256 tiles), a last round of at most a quarter of the CUs'
+// worth of tiles runs as their 128 x 128 quadrants, and with at most an
+// eighth and at least kQuadHalvesMinStages stages each quadrant as two K
+// halves.  Otherwise the remainder tiles are split in two K halves when the
+// estimated last round, ceil(nstages / 2) + fixed_cost + 2 part_cost stages
+// (a half, then writing its partial tile and reading the other's), beats
+// nstages + fixed_cost.  A tile's FP32 partial sums take part_tile_bytes.
 SplitPlan plan_split(int64_t tiles, int64_t nstages, double fixed_cost, double part_cost,
-                     size_t part_tile_bytes);
+                     size_t part_tile_bytes, bool quad_ok);
 SplitK split_args(const SplitPlan& plan, void* workspace);
 // token of half h of remainder tile r: kSplitToken ^ (2 r + h), never 0
 constexpr uint64_t kSplitToken = 0xC6A4A7935BD1E995ull;

@@ -71,11 +71,12 @@ def test_workspace_queries():
 
 
 def test_gemm_workspace_plan():
-    """Which shapes split their last round's tiles into two K halves, and
-    the workspace that takes (an 8-byte slot per remainder tile, 256-byte
-    aligned, then two FP32 partial tiles per tile: 256 KB each for 256 x 256
-    tiles, 64 KB for 128 x 128).  Without a GPU the CU count is MI355X's
-    256."""
+    """Which shapes split their last round's tiles (or those tiles'
+    128 x 128 quadrants) into two K halves, and the workspace that takes (an
+    8-byte slot per split tile or quadrant, 256-byte aligned, then two FP32
+    partial tiles per tile: 256 KB each for 256 x 256 tiles, 64 KB for
+    128 x 128 ones and for quadrants).  Without a GPU the CU count is
+    MI355X's 256."""
     G = sol.nvfp4_gemm_workspace_bytes
 
     def bytes_for(rem, part=256 * 256 * 4):
@@ -83,8 +84,12 @@ def test_gemm_workspace_plan():
 
     def small_bytes_for(rem):
         return bytes_for(rem, 128 * 128 * 4)
-    # FLUX.1 layers, 18432 tokens: 2592, 864, 3456 and 864 tiles of 256 x 256
-    assert G(18432, 9216, 3072) == bytes_for(2592 % 256)
+
+    def quad_bytes_for(rem):
+        return small_bytes_for(4 * rem)
+    # FLUX.1 layers, 18432 tokens: 2592, 864, 3456 and 864 tiles of 256 x 256;
+    # a last round of 32 tiles runs as 128 quadrants, each in two K halves
+    assert G(18432, 9216, 3072) == quad_bytes_for(2592 % 256)
     assert G(18432, 3072, 3072) == bytes_for(864 % 256)
     assert G(18432, 12288, 3072) == bytes_for(3456 % 256)
     assert G(18432, 3072, 12288) == bytes_for(864 % 256)
@@ -95,8 +100,16 @@ def test_gemm_workspace_plan():
     assert G(18432, 3072, 512) == 0            # 4 K stages
     assert G(8192, 5600, 2240) == 0            # 704 tiles: 192 left over
     assert G(8192, 36, 48) == 0                # K % 32 == 16: shared-conversion kernel
-    # K % 128 == 64 (a half last stage) splits too: the split is what makes
-    # the lane kernel worth taking over the shared one there
+    # a last round of at most 64 tiles runs as whole quadrants, without a
+    # workspace, when it has more than 32 tiles or fewer than 16 K stages;
+    # 8 to 32 tiles of at least 16 stages split their quadrants
+    assert G(4352, 4200, 1440) == 0            # 289 tiles: 33 left over
+    assert G(4352, 4096, 1536) == 0            # 272 tiles: 12 K stages
+    assert G(8192, 2240, 2240) == quad_bytes_for(32)    # 288 tiles, 18 K stages
+    assert G(26574, 2432, 9728) == quad_bytes_for(16)   # 1040 tiles
+    # K % 128 == 64 (a half last stage) splits too: the split (or the
+    # quadrants) is what makes the lane kernel worth taking over the shared
+    # one there
     assert G(8192, 6720, 2240) == bytes_for(864 % 256)
     # 128 x 128 tiles split as well, given enough K stages: 72 tiles of 24
     # and of 36 stages, and 72 of 18 (a half last stage) do

@@ -112,10 +112,15 @@ def test_mxfp4_checks():
 
 
 def test_gemm_plan_names_the_kernels():
+    # FLUX QKV: 2560 whole 256 x 256 tiles, then the last 32 as 128 quadrants
+    # of 128 x 128, each in two K halves (without a workspace, whole)
     p = B.gemm_plan(18432, 9216, 3072)
-    assert p == {"kernel": "nvfp4_gemm_lane_kernel", "tile": 256, "workgroups": 2592 - 32 + 64,
+    assert p == {"kernel": "nvfp4_gemm_lane_kernel", "tile": 256, "workgroups": 2560 + 2 * 128,
                  "splits": 2}
-    assert B.gemm_plan(18432, 9216, 3072, with_workspace=False)["splits"] == 1
+    assert B.gemm_plan(18432, 9216, 3072, with_workspace=False) == {
+        "kernel": "nvfp4_gemm_lane_kernel", "tile": 256, "workgroups": 2560 + 128, "splits": 1}
+    # FLUX out: 864 tiles, the last 96 each in two K halves
+    assert B.gemm_plan(18432, 3072, 3072)["workgroups"] == 768 + 2 * 96
     assert B.gemm_plan(128, 1152, 1152) == {"kernel": "nvfp4_gemm_wavek_kernel", "tile": 32,
                                             "workgroups": 144, "splits": 1}
     assert B.gemm_plan(256, 3072, 1152) == {"kernel": "nvfp4_gemm_small_kernel", "tile": 64,

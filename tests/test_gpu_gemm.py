@@ -63,9 +63,20 @@ def test_golden_gemms():
 # (every small shape here) and 256 x 256 tiles otherwise (5376 x 5376: 441
 # of them).  With 256 x 256 tiles, a last round of at most half the CUs'
 # worth of tiles is split into K halves when K is long enough (SPLIT_SHAPES:
-# 272, 289, 306 and 272 tiles, the second with a partial last stage, the
-# third with N % 8 != 0, the fourth with a half last stage).
-SPLIT_SHAPES = [(4352, 4096, 1536), (4352, 4200, 1440), (4353, 4100, 1536), (4352, 4096, 1600)]
+# 336 and 342 tiles, 80 and 86 left over, the second with a partial last
+# stage and N % 8 != 0, the third with a half last stage).  A last round of
+# at most a quarter of the CUs' worth runs as 128 x 128 quadrants of those
+# tiles in a launch of their own (QUAD_SHAPES: 272, 289, 306 and 272 tiles,
+# 16 to 50 left over, 12 or 13 K stages; the second with a partial last
+# stage, the third ragged with N % 8 != 0, so that some quadrants fall
+# outside the output, the fourth with a half last stage), and with at most
+# an eighth and at least 16 K stages each quadrant as two K halves
+# (QUAD_SPLIT_SHAPES: 16 left over; the second with a partial last stage,
+# the third ragged with N % 8 != 0 and empty quadrants; 32 left over with a
+# half last stage).
+SPLIT_SHAPES = [(4096, 5376, 1536), (4353, 4700, 1440), (4096, 5376, 1600)]
+QUAD_SHAPES = [(4352, 4096, 1536), (4352, 4200, 1440), (4353, 4100, 1536), (4352, 4096, 1600)]
+QUAD_SPLIT_SHAPES = [(4352, 4096, 2048), (4352, 4096, 2080), (4224, 4001, 3072), (8192, 2240, 2240)]
 # 128 x 128 tiles split too when K is long: 72 tiles of 24 and of 36
 # stages, 72 of 18 (a half last stage), and a ragged 3 x 29 tiles with
 # N % 8 != 0 (shapes whose 64 x 64 tiles fit in one round take the small kernel)
@@ -77,7 +88,7 @@ SMALL_SPLIT_SHAPES = [(384, 3072, 3072), (256, 4608, 4608), (512, 2240, 2240), (
                                    (513, 700, 384), (64, 1000, 1280), (300, 260, 160),
                                    (513, 700, 224), (260, 300, 2240), (5376, 5376, 256),
                                    (5376, 5400, 96), (4200, 4360, 1120), (4096, 4096, 320)]
-                        + SPLIT_SHAPES + SMALL_SPLIT_SHAPES)
+                        + SPLIT_SHAPES + QUAD_SHAPES + QUAD_SPLIT_SHAPES[:3] + SMALL_SPLIT_SHAPES)
 def test_exact_sums_are_bit_exact(M, N, K):
     """Scales 1.0 and power-of-two alphas: every partial sum is a multiple of
     1/4 of magnitude at most 36 K < 2^16, exact in FP32 in any order, so the
@@ -205,11 +216,45 @@ def test_zero_k_writes_bias():
     assert np.array_equal(bf16_from_dev(out), np.broadcast_to(bias, (M, N)))
 
 
-@pytest.mark.parametrize("M,N,K", SPLIT_SHAPES + SMALL_SPLIT_SHAPES)
+def test_route_lists_take_their_plans():
+    for M, N, K in SPLIT_SHAPES:
+        tiles = ((M + 255) // 256) * ((N + 255) // 256)
+        assert sol.gemm_plan(M, N, K) == {"kernel": "nvfp4_gemm_lane_kernel", "tile": 256,
+                                          "workgroups": tiles + tiles % 256, "splits": 2}
+    for M, N, K in QUAD_SHAPES + QUAD_SPLIT_SHAPES:
+        tiles = ((M + 255) // 256) * ((N + 255) // 256)
+        splits = 2 if (M, N, K) in QUAD_SPLIT_SHAPES else 1
+        rem = tiles % 256
+        assert sol.gemm_plan(M, N, K) == {"kernel": "nvfp4_gemm_lane_kernel", "tile": 256,
+                                          "workgroups": tiles - rem + 4 * rem * splits,
+                                          "splits": splits}
+        assert (sol.nvfp4_gemm_workspace_bytes(M, N, K) > 0) == (splits == 2)
+
+
+@pytest.mark.parametrize("M,N,K", QUAD_SHAPES)
+def test_quadrant_tail_vs_oracle(M, N, K):
+    """The last round's tiles as whole 128 x 128 quadrants: the same bits as
+    the same GEMM without a workspace (which takes the same plan) and as
+    128 x 128 tiles would give (the same MFMAs per output element in the
+    same order); within the bar of the oracle."""
+    ac, as_, aa = quantized("normal", M, K, 7 * M + K)
+    bc, bs, ba = quantized(None, N, K, 11 * N + K, sigma=0.02)
+    bias = draw_bias(N, 0.02, N + 5)
+    got = gpu_gemm(ac, as_, aa, bc, bs, ba, bias)
+    assert np.array_equal(got, gpu_gemm(ac, as_, aa, bc, bs, ba, bias, split=False))
+    ref = O.nvfp4_gemm_ref(ac, as_, aa, bc, bs, ba, bias)
+    err = rel_fro(got, ref)
+    say(f"quadrants M={M} N={N} K={K}: rel_fro={err:.3e}")
+    assert err <= TOL
+    assert bf16_mismatch_fraction(got, ref) <= 0.01
+    check_elements(got, (ac, as_, aa), (bc, bs, ba), ref, bias, "quadrants ")
+
+
+@pytest.mark.parametrize("M,N,K", SPLIT_SHAPES + QUAD_SPLIT_SHAPES + SMALL_SPLIT_SHAPES)
 def test_split_last_round_vs_oracle(M, N, K):
-    """The last round's tiles as two K halves: within the bar of the oracle,
-    and the same bits on a second call (the workspace is reused, its
-    counters cleared by the call itself) as on the first."""
+    """The last round's tiles (or their quadrants) as two K halves: within
+    the bar of the oracle, and the same bits on a second call (the workspace
+    is reused, its counters cleared by the call itself) as on the first."""
     need = sol.nvfp4_gemm_workspace_bytes(M, N, K)
     assert need > 0
     ac, as_, aa = quantized("normal", M, K, 5 * M + K)
@@ -238,7 +283,8 @@ def test_split_last_round_vs_oracle(M, N, K):
     check_elements(whole, (ac, as_, aa), (bc, bs, ba), ref, bias, "unsplit ")
 
 
-@pytest.mark.parametrize("M,N,K", [SPLIT_SHAPES[0], SMALL_SPLIT_SHAPES[0]])
+@pytest.mark.parametrize("M,N,K", [SPLIT_SHAPES[0], QUAD_SPLIT_SHAPES[0], QUAD_SHAPES[0],
+                                   SMALL_SPLIT_SHAPES[0]])
 def test_split_gemm_in_a_replayed_graph(M, N, K):
     """A split GEMM captured once and replayed: the tile slots left by each
     replay (and by the eager calls between replays) must not confuse the
