@@ -169,11 +169,17 @@ SOLFP4_API int nvfp4_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const
  * on the current device (host only; 0 for invalid sizes).  The GEMM runs
  * one workgroup per 256 x 256 output tile (128 x 128 when there are too few
  * of those to fill the device), about ceil(tiles / CUs) rounds of one
- * tile's time; when the last round holds few tiles, each of those is
- * computed as two K halves by two workgroups, which add their FP32 partial
- * sums through this workspace (one partial tile per half: 256 KB, or 64 KB
- * for 128 x 128 tiles; plus an 8-byte slot per tile that tells the second
- * half to finish that it is second).  0 means the shape runs without it,
+ * tile's time.  A last round of at most a quarter of the CUs' worth of
+ * 256 x 256 tiles runs after the others as four 128 x 128 quadrants per
+ * tile (a second kernel launch, same results as whole tiles); with at most
+ * an eighth and at least 16 K stages of 128 (K > 1920), each quadrant is
+ * computed as two K halves by two workgroups.  Otherwise, when the last
+ * round holds at most half the CUs' worth of tiles and K is long enough,
+ * each of those tiles is computed as two K halves.  The halves add their
+ * FP32 partial sums through this workspace (one partial tile per half:
+ * 256 KB, or 64 KB for 128 x 128 tiles and quadrants; plus an 8-byte slot
+ * per tile or quadrant that tells the second half to finish that it is
+ * second).  0 means the shape runs without it,
  * which includes few-token shapes (K % 128 == 0 with at most one 64 x 64
  * tile per compute unit): they run on 64 x 64 tiles, or on 32 x 32 tiles
  * whose K stages the four waves of a workgroup share (their partial sums

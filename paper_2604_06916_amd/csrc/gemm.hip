@@ -27,8 +27,10 @@
 //     from HBM into LDS by DMA and each wave dequantizes its own MFMA operands
 //     in registers, so LDS carries 0.5 B/element of codes instead of 2 B of
 //     FP16 per operand read; with too few tiles for one 256 x 256 tile per
-//     CU it runs on 128 x 128 tiles, and a last round of at most half the
-//     CUs' worth of tiles runs as two K halves per tile (SplitK);
+//     CU it runs on 128 x 128 tiles; a last round of at most a quarter of
+//     the CUs' worth of 256 x 256 tiles runs in a second launch as their
+//     128 x 128 quadrants (launch_gemm_quad), and otherwise a last round of
+//     at most half the CUs' worth as two K halves per tile (SplitK);
 //   nvfp4_gemm_kernel (the other K % 16 == 0): the workgroup converts each
 //     stage once into FP16 tiles in LDS, which all waves read.
 // Few tokens (K % 128 == 0, at most one 64 x 64 tile per CU) take one of
