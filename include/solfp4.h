@@ -249,7 +249,8 @@ SOLFP4_API int nvfp4_linear(const uint16_t* x, const uint8_t* w_codes, const uin
  *                   nvfp4_gemm_workspace_bytes(M, N, K) (ignored for MXFP4)
  *   kernel          written: one of the SOLFP4_KERNEL_* ids below
  *   tile            written: output tile edge, 256, 128, 64 or 32
- *   workgroups      written: workgroups of the launch
+ *   workgroups      written: workgroups of the launch (of both launches
+ *                   where the last round runs as 128 x 128 quadrants)
  *   splits          written: K ranges per tile of the last round, each on
  *                   a workgroup of its own (1: none; the wave-K kernel's
  *                   four K shares inside one workgroup are not counted)
@@ -263,7 +264,10 @@ SOLFP4_API int nvfp4_linear(const uint16_t* x, const uint8_t* w_codes, const uin
 #define SOLFP4_KERNEL_NVFP4_LANE 1     /* codes to LDS by DMA, per-wave dequantization */
 #define SOLFP4_KERNEL_NVFP4_SHARED 2   /* workgroup-shared dequantization into LDS */
 #define SOLFP4_KERNEL_MXFP4 3          /* scaled FP4 matrix instructions (256 x 256,
-                                          128 x 128 or, for few tokens, 64 x 64 tiles) */
+                                          128 x 128 or, for few tokens, 64 x 64 tiles; a
+                                          last round of at most a quarter of the CUs'
+                                          worth of 256 x 256 tiles runs as their
+                                          128 x 128 quadrants in a second launch) */
 #define SOLFP4_KERNEL_NVFP4_SMALL 4    /* 64 x 64 tiles for few tokens (K % 128 == 0); in
                                           nvfp4_linear with K <= 512 it also quantizes the
                                           activations itself */

@@ -59,6 +59,10 @@ bool small_tiles_pay(int64_t tiles256, int64_t tiles128);
 // Output tile edge (256, 128 or 64) of the tiled MXFP4 GEMM kernel (host only).
 int mx_tile_edge(int64_t M, int64_t N);
 
+// 256 x 256 tiles of an MXFP4 GEMM's last round that run as 128 x 128
+// quadrants in a second launch (0: none; host only).
+int64_t mx_quad_tiles(int64_t M, int64_t N);
+
 // Whether an MXFP4 GEMM runs on the wave-K kernel (32 x 32 tiles, each
 // workgroup's K stages dealt to its four waves; host only).
 bool use_mx_wavek(int64_t M, int64_t N, int64_t K);

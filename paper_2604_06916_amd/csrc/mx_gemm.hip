@@ -17,7 +17,9 @@
 // 64 x 64 tiles with one 32 x 32 MFMA tile per wave (mx_tile_edge chooses;
 // every size runs the same sequence of MFMAs per output element, so the
 // results are bit-identical across sizes; the wave-K kernel further down,
-// for few tokens, sums in another order).  K advances 128
+// for few tokens, sums in another order).  A last round of few 256 x 256
+// tiles runs in a second launch as their 128 x 128 quadrants (quad_base;
+// mx_quad_tiles).  K advances 128
 // elements (64 code bytes per row) per stage.  Codes go from global memory straight into LDS by
 // buffer loads with the LDS-destination bit (no register staging), into four
 // stage buffers: the loads for stage s+3 are issued while stage s computes,
@@ -116,7 +118,7 @@ __global__ __launch_bounds__(kMxThreads, 1) void mxfp4_gemm_kernel(
     const uint8_t* __restrict__ a_codes, const uint8_t* __restrict__ a_scales,
     const uint8_t* __restrict__ b_codes, const uint8_t* __restrict__ b_scales,
     const uint16_t* __restrict__ bias, uint16_t* __restrict__ out, int64_t M, int64_t N,
-    int64_t K) {
+    int64_t K, int quad_base) {
   static_assert(kWT == 128 || kWT == 64 || kWT == 32, "wave tile edge");
   constexpr int kT = 2 * kWT;                // output tile edge (M and N)
   constexpr int kFr = kWT / 32;              // 32 x 32 MFMA tiles per wave edge
@@ -137,7 +139,20 @@ __global__ __launch_bounds__(kMxThreads, 1) void mxfp4_gemm_kernel(
   const int tiles_m = (int)((M + kT - 1) / kT);
   const int tiles_n = (int)((N + kT - 1) / kT);
   int tm, tn;
-  tile_coords(tiles_m, tiles_n, tm, tn);
+  if constexpr (kWT == 64) {
+    if (quad_base >= 0) {
+      // quadrant blockIdx % 4 of 256 x 256 tile quad_base + blockIdx / 4
+      const int b = (int)blockIdx.x;
+      tile_coords_at(quad_base + b / 4, (int)((M + 255) / 256), (int)((N + 255) / 256), tm, tn);
+      tm = 2 * tm + ((b >> 1) & 1);
+      tn = 2 * tn + (b & 1);
+      if ((int64_t)tm * kT >= M || (int64_t)tn * kT >= N) return;   // quadrant outside the output
+    } else {
+      tile_coords(tiles_m, tiles_n, tm, tn);
+    }
+  } else {
+    tile_coords(tiles_m, tiles_n, tm, tn);
+  }
   const int64_t m0 = (int64_t)tm * kT;
   const int64_t n0 = (int64_t)tn * kT;
 
@@ -716,6 +731,19 @@ bool use_mx_wavek(int64_t M, int64_t N, int64_t K) {
   return wavek < tiled;
 }
 
+// 256 x 256 tiles of the last round that run as 128 x 128 quadrants in a
+// launch of their own: the remainder R of the tiles over the CU count when
+// there are more tiles than CUs and 4R quadrants fit one round, else 0.
+// Quadrants run the same MFMAs per output element in the same order as
+// whole tiles, so the output is the same bit for bit.
+int64_t mx_quad_tiles(int64_t M, int64_t N) {
+  if (mx_tile_edge(M, N) != 256) return 0;
+  const int64_t tiles = ((M + 255) / 256) * ((N + 255) / 256);
+  const int64_t cus = device_cu_count();
+  const int64_t rem = tiles % cus;
+  return tiles > cus && 4 * rem <= cus ? rem : 0;
+}
+
 void describe_mx_gemm(int64_t M, int64_t N, int64_t K, int* kernel, int* tile, int64_t* workgroups) {
   if (use_mx_wavek(M, N, K)) {
     *kernel = SOLFP4_KERNEL_MXFP4_WAVEK;
@@ -726,7 +754,7 @@ void describe_mx_gemm(int64_t M, int64_t N, int64_t K, int* kernel, int* tile, i
   const int edge = mx_tile_edge(M, N);
   *kernel = SOLFP4_KERNEL_MXFP4;
   *tile = edge;
-  *workgroups = ((M + edge - 1) / edge) * ((N + edge - 1) / edge);
+  *workgroups = ((M + edge - 1) / edge) * ((N + edge - 1) / edge) + 3 * mx_quad_tiles(M, N);
 }
 
 hipError_t launch_mx_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const uint8_t* b_codes,
@@ -736,19 +764,33 @@ hipError_t launch_mx_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const
   if (use_mx_wavek(M, N, K))
     return launch_mx_gemm_wavek(a_codes, a_scales, b_codes, b_scales, bias, out, M, N, K, stream);
   const int edge = mx_tile_edge(M, N);
-  const dim3 grid((unsigned)(((M + edge - 1) / edge) * ((N + edge - 1) / edge))), block(kMxThreads);
+  const int64_t tiles = ((M + edge - 1) / edge) * ((N + edge - 1) / edge);
+  const int64_t quads = mx_quad_tiles(M, N);
+  const dim3 block(kMxThreads);
   const bool fast = K % kMxBK == 0;
   const bool vec = N % 8 == 0;
-#define SOLFP4_MX_LAUNCH(F, V)                                                                   \
-  (edge == 64 ? launch_kernel(mxfp4_gemm_kernel<F, V, 32>, grid, block, stream, a_codes, a_scales, \
-                              b_codes, b_scales, bias, out, M, N, K)                             \
-   : edge == 128 ? launch_kernel(mxfp4_gemm_kernel<F, V, 64>, grid, block, stream, a_codes,      \
-                                 a_scales, b_codes, b_scales, bias, out, M, N, K)                \
-                 : launch_kernel(mxfp4_gemm_kernel<F, V, 128>, grid, block, stream, a_codes,     \
-                                 a_scales, b_codes, b_scales, bias, out, M, N, K))
+#define SOLFP4_MX_LAUNCH(W, G, Q)                                                                \
+  (fast ? (vec ? launch_kernel(mxfp4_gemm_kernel<true, true, W>, G, block, stream, a_codes,       \
+                               a_scales, b_codes, b_scales, bias, out, M, N, K, Q)               \
+               : launch_kernel(mxfp4_gemm_kernel<true, false, W>, G, block, stream, a_codes,      \
+                               a_scales, b_codes, b_scales, bias, out, M, N, K, Q))              \
+        : (vec ? launch_kernel(mxfp4_gemm_kernel<false, true, W>, G, block, stream, a_codes,      \
+                               a_scales, b_codes, b_scales, bias, out, M, N, K, Q)               \
+               : launch_kernel(mxfp4_gemm_kernel<false, false, W>, G, block, stream, a_codes,     \
+                               a_scales, b_codes, b_scales, bias, out, M, N, K, Q)))
   hipError_t e;
-  if (fast) e = vec ? SOLFP4_MX_LAUNCH(true, true) : SOLFP4_MX_LAUNCH(true, false);
-  else e = vec ? SOLFP4_MX_LAUNCH(false, true) : SOLFP4_MX_LAUNCH(false, false);
+  if (edge == 64) {
+    e = SOLFP4_MX_LAUNCH(32, dim3((unsigned)tiles), -1);
+  } else if (edge == 128) {
+    e = SOLFP4_MX_LAUNCH(64, dim3((unsigned)tiles), -1);
+  } else if (quads == 0) {
+    e = SOLFP4_MX_LAUNCH(128, dim3((unsigned)tiles), -1);
+  } else {
+    // the whole tiles, then the last round's tiles as 128 x 128 quadrants
+    e = SOLFP4_MX_LAUNCH(128, dim3((unsigned)(tiles - quads)), -1);
+    if (e == hipSuccess)
+      e = SOLFP4_MX_LAUNCH(64, dim3((unsigned)(4 * quads)), (int)(tiles - quads));
+  }
 #undef SOLFP4_MX_LAUNCH
   return e;
 }

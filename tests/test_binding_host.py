@@ -129,9 +129,11 @@ def test_gemm_plan_names_the_kernels():
     assert B.gemm_plan(128, 12288, 3072)["kernel"] == "nvfp4_gemm_lane_kernel"
     assert B.gemm_plan(128, 1152, 1120)["tile"] == 128      # K % 128 != 0
     assert B.gemm_plan(4096, 4096, 320)["kernel"] == "nvfp4_gemm_kernel"
+    # MXFP4 FLUX QKV: 2560 whole tiles, then the last 32 as 128 quadrants
     assert B.gemm_plan(18432, 9216, 3072, B.FORMAT_MXFP4) == {"kernel": "mxfp4_gemm_kernel",
-                                                              "tile": 256, "workgroups": 2592,
+                                                              "tile": 256, "workgroups": 2560 + 128,
                                                               "splits": 1}
+    assert B.gemm_plan(18432, 3072, 3072, B.FORMAT_MXFP4)["workgroups"] == 864
     # MXFP4 tiles by token count (on a host without a device the library
     # plans for 256 CUs): the wave-K kernel's 32 x 32 tiles while they fit
     # one per CU and K spans more than one stage, 64 x 64 while those take

@@ -158,7 +158,9 @@ def test_golden_gemm():
 # The small shapes run on 64 x 64 tiles or, where K spans several 128-element
 # stages ((64, 96, 512), (260, 300, 1152)), on the wave-K kernel; (1000, 3000,
 # K) and (1024, 3072, K) on 128 x 128 tiles, (4200, 4360, K) and (6000, 6152,
-# 1024) on 256 x 256 ones (ragged M and N).  Scale groups (16 bytes of a row) are one 16-byte load;
+# 1024) on 256 x 256 ones (ragged M and N); (4353, 4100, 96) and (4224, 4001,
+# 1024) on 256 x 256 tiles whose last round (50 and 16 tiles) runs as 128 x 128
+# quadrants in a second launch, some of them outside the output.  Scale groups (16 bytes of a row) are one 16-byte load;
 # with K % 128 != 0 (K = 96, 2240) rows start at any byte offset and the lane
 # of an operand's last row whose group reaches past the range loads bytes
 # instead, on every tile size.  K = 1152 (K % 512 !=
@@ -169,7 +171,8 @@ def test_golden_gemm():
                                    (257, 513, 32), (64, 96, 512), (260, 300, 1152),
                                    (1000, 3000, 128), (1024, 3072, 96),
                                    (4200, 4360, 1024), (6000, 6152, 1024), (4200, 4360, 1152),
-                                   (300, 260, 2240), (4200, 4360, 2240), (4201, 4359, 96)])
+                                   (300, 260, 2240), (4200, 4360, 2240), (4201, 4359, 96),
+                                   (4353, 4100, 96), (4224, 4001, 1024)])
 def test_exact_sums_are_bit_exact(M, N, K):
     """Scales 2^-2 and 2^3: every partial sum is a multiple of 1/2 below
     2^17, exact in FP32, so the only rounding is the final BF16."""
@@ -213,7 +216,9 @@ SHAPES = [(1, 1, 32), (5, 7, 64), (64, 64, 128), (255, 257, 96), (300, 520, 288)
           # 128 x 128 tiles (the shapes above take 64 x 64 ones)
           (1000, 3000, 256), (1024, 3072, 160),
           # 256 x 256 tiles, more tiles than compute units
-          (4200, 4360, 1024), (2100, 9000, 3072)]
+          (4200, 4360, 1024), (2100, 9000, 3072),
+          # ... and a last round of 16 or 50 tiles as 128 x 128 quadrants
+          (4224, 4001, 1024), (4353, 4100, 2240)]
 
 
 @pytest.mark.parametrize("M,N,K", SHAPES)
@@ -274,6 +279,18 @@ def test_wavek_exact_sums_are_bit_exact(M, N, K):
     ref = O.mxfp4_gemm_ref(ac, as_, bc, bs)
     got = gpu_gemm(ac, as_, bc, bs)
     assert np.array_equal(got, O.bf16_output(ref))
+
+
+def test_quadrant_plans():
+    """The last round's 256 x 256 tiles as quadrants: 4 workgroups each in
+    a second launch (the plan counts both launches)."""
+    for M, N in [(4224, 4001), (4353, 4100), (18432, 9216)]:
+        tiles = ((M + 255) // 256) * ((N + 255) // 256)
+        rem = tiles % 256
+        assert 0 < rem <= 64
+        p = sol.gemm_plan(M, N, 1024, sol.FORMAT_MXFP4)
+        assert p == {"kernel": "mxfp4_gemm_kernel", "tile": 256, "workgroups": tiles + 3 * rem,
+                     "splits": 1}
 
 
 def test_wide_dynamic_range_vs_oracle():
