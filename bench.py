@@ -745,6 +745,9 @@ def gemm_roofline(r, layers, traffic=None):
         "traffic": traffic,
         "traffic_unit": "HBM bytes per launch (mean over the step's GEMMs)",
         "algorithmic_flops_per_launch": r["flops"] / len(layers),
+        "note": "a launch here is one nvfp4_gemm call, timed with HIP events on its stream; a call "
+                "whose last round of 256 x 256 tiles runs as 128 x 128 quadrants is two kernel "
+                "launches, counted together",
     }
 
 
